@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Paged-attention benchmark on one MI355X.
+
+A step is one pa_forward call over one batch (every kernel of the path:
+decode split-KV + log-sum-exp merge for single-token rows, the Q-block
+kernel for the rest), inputs resident in HBM.  The headline workload is the
+Llama-3-8B-shaped decode batch (64 sequences, context U[512, 8192], Hq 32 /
+Hkv 8, d 128, bf16, block size 16); the other four benchmark batches are
+measured in the same run and reported under "configs".
+
+Algorithmic work per batch (what the method must move / compute):
+  bytes = sum_i L_i*Hkv*d*2*b_kv + 2*T*Hq*d*2 + sum_i ceil(L_i/bs)*4 + (2S+1)*4
+  flops = 4*d*Hq*sum_i sum_j (c_i + j + 1)
+Roofline peaks: HBM 8.0 TB/s, dense bf16 MFMA 2516.6 TFLOP/s.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config k]
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6
+METRIC = "paged-attn decode HBM GB/s & prefill TFLOP/s (% of MI355X roofline), µs/batch"
+
+
+def alg_bytes(w):
+    b_kv = 1 if w.kv_fp8 else 2
+    L = w.seq_len_list
+    T = sum(w.q_lens)
+    return (sum(L) * w.num_kv_heads * w.head_dim * 2 * b_kv + 2 * T * w.num_q_heads * w.head_dim * 2
+            + sum(-(-x // w.block_size) for x in L) * 4 + (2 * w.num_seqs + 1) * 4)
+
+
+def alg_flops(w):
+    pairs = sum(q * c + q * (q + 1) // 2 for c, q in zip(w.ctx_lens, w.q_lens))
+    return 4 * w.head_dim * w.num_q_heads * pairs
+
+
+def decode_bytes(w):
+    """Bytes of the single-token (decode) rows only."""
+    b_kv = 1 if w.kv_fp8 else 2
+    L = [c + q for c, q in zip(w.ctx_lens, w.q_lens) if q == 1]
+    return (sum(L) * w.num_kv_heads * w.head_dim * 2 * b_kv + 2 * len(L) * w.num_q_heads * w.head_dim * 2
+            + sum(-(-x // w.block_size) for x in L) * 4)
+
+
+def prefill_flops(w):
+    pairs = sum(q * c + q * (q + 1) // 2 for c, q in zip(w.ctx_lens, w.q_lens) if q >= 2)
+    return 4 * w.head_dim * w.num_q_heads * pairs
+
+
+def make_attention(w, profile=False):
+    from paper_2511_11581_amd import pa
+    return pa.PagedAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size,
+                             w.k_cache.dtype, w.k_scale, w.v_scale, max_tokens=w.num_tokens,
+                             max_seqs=w.num_seqs, max_blocks_per_seq=int(w.block_table.shape[1]),
+                             profile=profile)
+
+
+def time_steps(w, att, out, steps, warmup):
+    """Mean ms per step over `steps` calls, events on the launch stream."""
+    import torch
+    args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
+    for _ in range(warmup):
+        att.forward(*args, w.scale, out=out)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        att.forward(*args, w.scale, out=out)
+    ev1.record()
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / steps
+
+
+def per_kernel_ms(w, out, steps, warmup):
+    """Average duration of each kernel (HIP events recorded by the library
+    around every launch on the same stream)."""
+    import torch
+    att = make_attention(w, profile=True)
+    args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
+    for _ in range(warmup):
+        att.forward(*args, w.scale, out=out)
+    torch.cuda.synchronize()
+    att.profile(reset=True)
+    for _ in range(steps):
+        att.forward(*args, w.scale, out=out)
+    prof = att.profile(reset=True)
+    att.close()
+    return {k: (tot / n if n else 0.0) for k, (n, tot) in prof.items()}
+
+
+def measure(k, steps, warmup):
+    import torch
+    from paper_2511_11581_amd import workloads as W
+    w = W.make_config(k, device="cuda", poison=False)
+    att = make_attention(w)
+    out = torch.empty_like(w.q)
+    ms = time_steps(w, att, out, steps, warmup)
+    kms = per_kernel_ms(w, out, steps, warmup)
+    plan = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]))
+    att.close()
+    B, F = alg_bytes(w), alg_flops(w)
+    res = {
+        "config": k, "name": W.CONFIG_NAMES[k], "seed": w.seed, "sum_L": sum(w.seq_len_list),
+        "us_per_batch": ms * 1e3, "alg_bytes": B, "alg_flops": F,
+        "GBps": B / (ms * 1e-3) / 1e9, "TFLOPs": F / (ms * 1e-3) / 1e12,
+        "per_kernel_us": {kk: v * 1e3 for kk, v in kms.items() if v > 0},
+        "plan": {kk: plan[kk] for kk in ("segment_len", "max_splits", "block_q",
+                                         "decode_grid", "prefill_grid")},
+    }
+    res["frac_hbm"] = res["GBps"] / HBM_PEAK_GBS
+    res["frac_mfma"] = res["TFLOPs"] / BF16_PEAK_TFLOPS
+    db, pf = decode_bytes(w), prefill_flops(w)
+    if kms.get("decode", 0) > 0 and db > 0:
+        res["decode_kernel_GBps"] = db / (kms["decode"] * 1e-3) / 1e9
+    if kms.get("prefill", 0) > 0 and pf > 0:
+        res["prefill_kernel_TFLOPs"] = pf / (kms["prefill"] * 1e-3) / 1e12
+    return w, res
+
+
+def cpu_baseline(w, budget_s=15.0, flops=False):
+    """The fp64 oracle on the host cores over the first m sequences of the
+    batch (m chosen so the run takes about budget_s), in the headline's unit
+    (GB/s of algorithmic bytes, or TFLOP/s of algorithmic flops)."""
+    import oracle
+    import dataclasses
+    wc = w.to("cpu")
+    threads = oracle.default_threads()
+
+    def sub(m):
+        t_end = int(wc.query_start_loc[m])
+        return dataclasses.replace(
+            wc, q=wc.q[:t_end].contiguous(), block_table=wc.block_table[:m].contiguous(),
+            seq_lens=wc.seq_lens[:m].contiguous(), query_start_loc=wc.query_start_loc[:m + 1].contiguous(),
+            ctx_lens=wc.ctx_lens[:m], q_lens=wc.q_lens[:m])
+
+    def run(s):
+        t = time.perf_counter()
+        oracle.forward(s.q, s.k_cache, s.v_cache, s.block_table, s.seq_lens, s.query_start_loc,
+                       s.scale, k_scale=s.k_scale, v_scale=s.v_scale, threads=threads)
+        return time.perf_counter() - t
+
+    probe = sub(min(threads, w.num_seqs))
+    tp = run(probe)
+    per_seq = tp / probe.num_seqs
+    m = max(1, min(w.num_seqs, int(budget_s / max(per_seq, 1e-6))))
+    s = sub(m)
+    t = run(s) if m != probe.num_seqs else tp
+    value, unit = (alg_flops(s) / t / 1e12, "TFLOP/s") if flops else (alg_bytes(s) / t / 1e9, "GB/s")
+    return {"value": value, "unit": unit, "cores": threads, "kind": "oracle",
+            "sample": f"first {m} of {w.num_seqs} sequences (sum_L={sum(s.seq_len_list)}), "
+                      f"fp64 C oracle, {t:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="headline batch (1..5)")
+    ap.add_argument("--only", action="store_true", help="measure the headline batch only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this path has no multi-GPU mode (asked for {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_11581_amd import pa
+    if not os.path.exists(pa.LIB_PATH):
+        from paper_2511_11581_amd import build as hip_build
+        hip_build.build()
+    pa.load_library()
+    torch.cuda.set_device(0)
+
+    configs = {}
+    headline_w, headline = measure(args.config, args.steps, args.warmup)
+    configs[args.config] = headline
+    if not args.only:
+        for k in (1, 2, 3, 4, 5):
+            if k != args.config:
+                _, r = measure(k, args.steps, args.warmup)
+                configs[k] = r
+                torch.cuda.empty_cache()
+    for k in sorted(configs):
+        r = configs[k]
+        print(f"# config {k}: {r['us_per_batch']:.1f} us/batch, {r['GBps']:.0f} GB/s "
+              f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
+              f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}", file=sys.stderr)
+
+    decode_like = args.config != 3
+    h = headline
+    if decode_like:
+        value, unit = h["GBps"], "GB/s"
+        dom_ms = h["per_kernel_us"].get("decode", 0) / 1e3
+        achieved = decode_bytes(headline_w) / (dom_ms * 1e-3) / 1e9 if dom_ms else None
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS if achieved else None, "traffic": None,
+                "kernel": "decode_kernel", "kernel_us": dom_ms * 1e3}
+    else:
+        value, unit = h["TFLOPs"], "TFLOP/s"
+        dom_ms = h["per_kernel_us"].get("prefill", 0) / 1e3
+        achieved = prefill_flops(headline_w) / (dom_ms * 1e-3) / 1e12 if dom_ms else None
+        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / BF16_PEAK_TFLOPS if achieved else None, "traffic": None,
+                "kernel": "prefill_kernel", "kernel_us": dom_ms * 1e3}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(headline_w, flops=not decode_like)
+    line = {
+        "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": h["us_per_batch"] / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if not headline_w.kv_fp8 else "bf16/fp8-kv",
+        "data": "synthetic (seeded N(0,1) bf16 Q/K/V, random block tables)",
+        "config": {"workload": h["name"], "seq_lens_sum": h["sum_L"], "seed": h["seed"],
+                   "us_per_batch": h["us_per_batch"], "parallelism": "single GPU"},
+        "roofline": roof, "cpu_baseline": cpu,
+        "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * pa.h -- C ABI of libpa.so, paged attention for AMD MI355X (gfx950).
+ *
+ * What is computed (arxiv 2511.11581, Sec. 4.1 Eq. 1 and Eq. 2; Sec. 4.2
+ * terminology; Sec. 4.3 paged KV cache and block table): for a batch of
+ * sequences described by query_start_loc (the accumulated query lengths,
+ * App. A) and seq_lens (sequence length = context length + query length),
+ * every query token j of sequence i (absolute position c_i + j, where
+ * c_i = seq_lens[i] - q_i) and every query head h attends causally to keys
+ * 0 .. c_i + j of its sequence, using kv head h / (Hq / Hkv) (grouped-query
+ * attention, Sec. 4.1):
+ *     out[t, h, :] = softmax_p(scale * <q[t, h, :], K[p]>) . V[p]
+ * Key position p of sequence i is stored in physical block
+ * block_table[i][p / block_size], slot p % block_size.  Q, K and V are
+ * already computed and K/V of the query tokens are already in the cache
+ * (Sec. 4.3).
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers inside pa_tensor are device pointers; the caller owns all
+ *    device memory and keeps it alive until the stream work completes.
+ *  - Host-visible problems (dtype, ndim, shapes, strides, alignment, head
+ *    configuration, workspace size) are reported by the return value BEFORE
+ *    anything is enqueued; a thread-local message is then available from
+ *    pa_last_error().
+ *  - Device-resident metadata (query_start_loc, seq_lens, block ids) is not
+ *    read by the host.  Malformed metadata gives unspecified output values
+ *    but never an out-of-bounds access: kernels clamp block ids into
+ *    [0, num_blocks), sequence lengths to the table capacity and token
+ *    ranges to [0, num_tokens).  With PA_FLAG_VALIDATE the metadata is
+ *    checked on the device first and pa_forward synchronises to report it.
+ *  - Nothing here allocates device memory or synchronises the stream
+ *    (except the PA_FLAG_VALIDATE check), so pa_forward can be captured in
+ *    a HIP graph.
+ */
+#ifndef PA_H_
+#define PA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A hipStream_t, declared opaquely so that this header needs no HIP
+ * headers.  NULL means the default stream. */
+typedef struct ihipStream_t *pa_stream;
+
+typedef enum pa_status {
+  PA_OK = 0,
+  PA_ERR_INVALID_ARG = 1,  /* malformed argument (shape, dtype, stride, null) */
+  PA_ERR_UNSUPPORTED = 2,  /* well-formed but not supported by this build */
+  PA_ERR_WORKSPACE = 3,    /* workspace missing or too small */
+  PA_ERR_DEVICE = 4,       /* HIP error, or PA_FLAG_VALIDATE found bad metadata */
+} pa_status;
+
+typedef enum pa_dtype {
+  PA_DTYPE_BF16 = 0,       /* bfloat16 */
+  PA_DTYPE_FP8_E4M3 = 1,   /* OCP 8-bit e4m3fn, stored as bytes */
+  PA_DTYPE_I32 = 2,
+  PA_DTYPE_F32 = 3,
+} pa_dtype;
+
+#define PA_MAX_DIMS 4
+
+/* A strided device array.  shape/stride are in elements; the innermost
+ * dimension must have stride 1. */
+typedef struct pa_tensor {
+  void *data;
+  int32_t dtype;              /* pa_dtype */
+  int32_t ndim;
+  int64_t shape[PA_MAX_DIMS];
+  int64_t stride[PA_MAX_DIMS];
+} pa_tensor;
+
+/* Check query_start_loc / seq_lens / block ids on the device before the
+ * attention kernels run; pa_forward then synchronises its stream and
+ * returns PA_ERR_DEVICE on a violation.  Debug only. */
+#define PA_FLAG_VALIDATE 1u
+
+/* Record a pair of HIP events around every kernel launch of pa_forward, on
+ * the caller's stream, so that pa_profile_read can report per-kernel
+ * durations.  Adds two event records per launch; off by default. */
+#define PA_FLAG_PROFILE 2u
+
+typedef struct pa_config {
+  int32_t num_q_heads;     /* Hq */
+  int32_t num_kv_heads;    /* Hkv; Hq % Hkv == 0; G = Hq / Hkv must divide 128 and be <= 16 */
+  int32_t head_dim;        /* d: 64 or 128 */
+  int32_t block_size;      /* tokens per KV-cache block: a positive multiple of 16 */
+  int32_t kv_dtype;        /* PA_DTYPE_BF16 or PA_DTYPE_FP8_E4M3 */
+  float k_scale;           /* fp8 dequantisation: K = decode(k_cache) * k_scale (1 for bf16) */
+  float v_scale;           /* V = decode(v_cache) * v_scale (1 for bf16) */
+  uint32_t flags;          /* PA_FLAG_* */
+  void *workspace;         /* device scratch owned by the caller, 256-byte aligned */
+  uint64_t workspace_bytes;
+} pa_config;
+
+typedef struct pa_handle pa_handle;
+
+/* Kernel kinds reported by pa_profile_read. */
+enum { PA_KERNEL_DECODE = 0, PA_KERNEL_MERGE = 1, PA_KERNEL_PREFILL = 2, PA_KERNEL_KINDS = 3 };
+
+typedef struct pa_profile {
+  int64_t launches[PA_KERNEL_KINDS];  /* timed launches since the last reset */
+  double total_ms[PA_KERNEL_KINDS];   /* summed event-to-event durations */
+} pa_profile;
+
+/* The launch decisions for one batch shape (host-visible sizes only). */
+typedef struct pa_plan_info {
+  int32_t decode_launch;     /* 1 if the decode (q_len == 1) kernel is launched */
+  int32_t decode_tile;       /* keys per wave iteration */
+  int32_t decode_waves;      /* waves per decode workgroup */
+  int32_t segment_len;       /* keys per split-KV segment (Sec. 4.5) */
+  int32_t max_splits;        /* segments per sequence at most */
+  int32_t merge_launch;      /* 1 if the log-sum-exp merge kernel is launched */
+  int32_t prefill_launch;    /* 1 if the Q-block (q_len >= 2) kernel is launched */
+  int32_t block_m;           /* rows per Q-block (BLOCK_M, Sec. 4.4) */
+  int32_t block_q;           /* query tokens per Q-block (BLOCK_Q = BLOCK_M / G) */
+  int32_t prefill_tile;      /* keys per prefill tile */
+  int64_t decode_grid[3];
+  int64_t merge_grid[3];
+  int64_t prefill_grid[3];
+  uint64_t workspace_bytes;  /* workspace this batch shape needs */
+} pa_plan_info;
+
+/* Workspace bytes that suffice for every batch with at most max_seqs
+ * sequences, max_tokens query rows and max_blocks_per_seq table entries per
+ * sequence, under cfg's head configuration.  cfg->workspace is ignored. */
+pa_status pa_workspace_bytes(const pa_config *cfg, int64_t max_tokens, int64_t max_seqs,
+                             int64_t max_blocks_per_seq, uint64_t *bytes);
+
+/* Validate cfg and create a handle bound to the current HIP device.  The
+ * handle holds host state only (device properties, the workspace pointer);
+ * it is immutable after creation.  Concurrent pa_forward calls on different
+ * streams need handles with distinct workspaces. */
+pa_status pa_create(const pa_config *cfg, pa_handle **out);
+
+/* Enqueue attention for one batch on `stream`.
+ *   q               bf16 [T, Hq, d]
+ *   k_cache/v_cache kv_dtype [num_blocks, block_size, Hkv, d]
+ *   block_table     int32 [S, MB]; entries past a sequence's last block are ignored
+ *   seq_lens        int32 [S]
+ *   query_start_loc int32 [S + 1]; query_start_loc[0] = 0, non-decreasing,
+ *                   query_start_loc[S] <= T
+ *   scale           softmax scale (1/sqrt(d) for Eq. 1)
+ *   out             bf16 [T, Hq, d]; rows [0, query_start_loc[S]) are written
+ *                   exactly once, other rows are untouched.
+ * All base pointers and all non-unit strides must be 16-byte aligned in
+ * bytes.  Sequences with query length 1 run on the split-KV decode kernel
+ * (+ merge), the others on the Q-block kernel. */
+pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
+                     const pa_tensor *v_cache, const pa_tensor *block_table,
+                     const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,
+                     const pa_tensor *out, pa_stream stream);
+
+/* Debug: copy the stored bytes of every valid K and V row (positions
+ * p < seq_lens[i]) in logical order into k_dense / v_dense, both of the
+ * cache dtype and shape [S, MB * block_size, Hkv, d], walking the block
+ * table with the same addressing as the attention kernels.  Rows at
+ * positions >= seq_lens[i] are untouched. */
+pa_status pa_debug_gather(pa_handle *h, const pa_tensor *k_cache, const pa_tensor *v_cache,
+                          const pa_tensor *block_table, const pa_tensor *seq_lens,
+                          const pa_tensor *k_dense, const pa_tensor *v_dense, pa_stream stream);
+
+/* The launch plan pa_forward would use for a batch with these host-visible
+ * sizes on a device with num_cus compute units (num_cus <= 0: the handle's
+ * device, or 256 without a handle).  Host only; no HIP call.  h may be NULL,
+ * then cfg is used. */
+pa_status pa_plan(const pa_handle *h, const pa_config *cfg, int32_t num_cus, int64_t num_tokens,
+                  int64_t num_seqs, int64_t max_blocks_per_seq, pa_plan_info *out);
+
+/* Per-kernel durations recorded under PA_FLAG_PROFILE (zeros otherwise).
+ * Waits for the recorded events to complete; with reset != 0 the counters
+ * restart from zero afterwards. */
+pa_status pa_profile_read(pa_handle *h, pa_profile *out, int reset);
+
+/* Release the handle (and its profiling events). */
+void pa_destroy(pa_handle *h);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *pa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PA_H_ */

@@ -1,0 +1,539 @@
+// Host side of libpa.so: argument validation, the launch planner and the
+// kernel launches behind the C ABI declared in include/pa.h.
+//
+// The planner sees host-visible sizes only (T, S, the block-table width MB,
+// the head configuration and the CU count); it never reads device metadata,
+// so pa_forward neither synchronises nor copies anything to the host.
+//   - Sequences with one query token (decode, Sec. 4.2) go to the split-KV
+//     decode kernel.  The segment length is chosen so that
+//     S * Hkv * max_splits covers about 8 workgroups per CU when every
+//     sequence is as long as the table allows (Sec. 4.5: split the tiles of
+//     long sequences over several program instances when the batch alone
+//     cannot fill the GPU).  Sequences that need more than one segment are
+//     merged by the log-sum-exp kernel.
+//   - Sequences with two or more query tokens go to the Q-block kernel
+//     (Sec. 4.4) with BLOCK_M = 128 rows, i.e. BLOCK_Q = 128 / G tokens.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/pa.h"
+#include "kernels.h"
+
+// Ring of event pairs of one kernel kind (PA_FLAG_PROFILE).
+struct pa_event_ring {
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+};
+
+struct pa_handle {
+  pa_config cfg;
+  int device;
+  int cus;
+  bool profile;
+  pa_event_ring ring[PA_KERNEL_KINDS];
+  int64_t launches[PA_KERNEL_KINDS];
+  double total_ms[PA_KERNEL_KINDS];
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+pa_status fail(pa_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+constexpr int kMaxCus = 256;
+constexpr int kDecodeTile = 32;
+constexpr int kDecodeWaves = 4;
+constexpr int kSegQuantum = kDecodeTile * kDecodeWaves;  // keys per workgroup step
+constexpr int kMinSeg = 256;
+constexpr int kWgPerCu = 8;
+constexpr int kBlockM = 128;
+constexpr int kPrefillTile = 64;
+constexpr uint64_t kHeader = 256;  // validation word + alignment
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+int elem_bytes(int dt) {
+  switch (dt) {
+    case PA_DTYPE_BF16: return 2;
+    case PA_DTYPE_FP8_E4M3: return 1;
+    case PA_DTYPE_I32: return 4;
+    case PA_DTYPE_F32: return 4;
+    default: return 0;
+  }
+}
+
+pa_status check_config(const pa_config* c) {
+  if (!c) return fail(PA_ERR_INVALID_ARG, "config is NULL");
+  if (c->num_q_heads <= 0 || c->num_kv_heads <= 0)
+    return fail(PA_ERR_INVALID_ARG, "head counts must be positive (Hq=%d, Hkv=%d)", c->num_q_heads,
+                c->num_kv_heads);
+  if (c->num_q_heads % c->num_kv_heads != 0)
+    return fail(PA_ERR_INVALID_ARG, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)",
+                c->num_q_heads, c->num_kv_heads);
+  const int G = c->num_q_heads / c->num_kv_heads;
+  if (G > 16 || (kBlockM % G) != 0)
+    return fail(PA_ERR_UNSUPPORTED, "query heads per kv head must be 1, 2, 4, 8 or 16 (got %d)", G);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(PA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
+  if (c->block_size <= 0 || c->block_size % 16 != 0)
+    return fail(PA_ERR_UNSUPPORTED, "block_size must be a positive multiple of 16 (got %d)",
+                c->block_size);
+  if (c->kv_dtype != PA_DTYPE_BF16 && c->kv_dtype != PA_DTYPE_FP8_E4M3)
+    return fail(PA_ERR_UNSUPPORTED, "kv_dtype must be bf16 or fp8 e4m3 (got %d)", c->kv_dtype);
+  if (!(c->k_scale > 0.f) || !(c->v_scale > 0.f))
+    return fail(PA_ERR_INVALID_ARG, "k_scale and v_scale must be positive");
+  if (c->flags & ~(PA_FLAG_VALIDATE | PA_FLAG_PROFILE))
+    return fail(PA_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
+  if (c->workspace && (reinterpret_cast<uintptr_t>(c->workspace) & 255))
+    return fail(PA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  return PA_OK;
+}
+
+void make_plan(const pa_config& c, int cus, int64_t T, int64_t S, int64_t MB, pa_plan_info* p) {
+  std::memset(p, 0, sizeof *p);
+  cus = std::min(std::max(cus, 1), kMaxCus);
+  const int G = c.num_q_heads / c.num_kv_heads;
+  const int64_t max_len = MB * c.block_size;
+  p->decode_tile = kDecodeTile;
+  p->decode_waves = kDecodeWaves;
+  p->block_m = kBlockM;
+  p->block_q = kBlockM / G;
+  p->prefill_tile = kPrefillTile;
+  uint64_t ws = kHeader;
+  if (S >= 1 && T >= 1 && max_len >= 1) {
+    p->decode_launch = 1;
+    const int64_t units = S * c.num_kv_heads;
+    const int64_t want = cdiv((int64_t)kWgPerCu * cus, units);
+    int64_t seg = cdiv(cdiv(max_len, want), kSegQuantum) * kSegQuantum;
+    seg = std::max<int64_t>(seg, kMinSeg);
+    const int64_t splits = cdiv(max_len, seg);
+    p->segment_len = (int32_t)seg;
+    p->max_splits = (int32_t)splits;
+    p->decode_grid[0] = splits;
+    p->decode_grid[1] = S;
+    p->decode_grid[2] = c.num_kv_heads;
+    if (splits > 1) {
+      p->merge_launch = 1;
+      p->merge_grid[0] = S;
+      p->merge_grid[1] = c.num_kv_heads;
+      p->merge_grid[2] = 1;
+      const uint64_t rows = (uint64_t)S * splits * c.num_q_heads;
+      ws += align256(rows * c.head_dim * 4) + align256(rows * 2 * 4);
+    }
+  }
+  if (S >= 1 && T >= 2 && max_len >= 2) {
+    p->prefill_launch = 1;
+    const int64_t items = cdiv(T, p->block_q) + std::min<int64_t>(S, T / 2);
+    p->prefill_grid[0] = items * c.num_kv_heads;
+    p->prefill_grid[1] = 1;
+    p->prefill_grid[2] = 1;
+  }
+  p->workspace_bytes = ws;
+}
+
+// ---- tensor checks -------------------------------------------------------
+
+pa_status check_tensor(const pa_tensor* t, const char* name, int dtype, int ndim) {
+  if (!t) return fail(PA_ERR_INVALID_ARG, "%s is NULL", name);
+  if (t->dtype != dtype) return fail(PA_ERR_INVALID_ARG, "%s has dtype %d, expected %d", name, t->dtype, dtype);
+  if (t->ndim != ndim) return fail(PA_ERR_INVALID_ARG, "%s has %d dims, expected %d", name, t->ndim, ndim);
+  for (int i = 0; i < ndim; ++i) {
+    if (t->shape[i] < 0 || t->shape[i] > INT32_MAX)
+      return fail(PA_ERR_INVALID_ARG, "%s dim %d has size %lld", name, i, (long long)t->shape[i]);
+    if (t->stride[i] < 0) return fail(PA_ERR_INVALID_ARG, "%s has a negative stride", name);
+  }
+  if (t->stride[ndim - 1] != 1 && t->shape[ndim - 1] > 1)
+    return fail(PA_ERR_INVALID_ARG, "%s must be contiguous in its last dimension", name);
+  int64_t numel = 1;
+  for (int i = 0; i < ndim; ++i) numel *= t->shape[i];
+  if (numel > 0 && !t->data) return fail(PA_ERR_INVALID_ARG, "%s has a NULL data pointer", name);
+  return PA_OK;
+}
+
+// 16-byte alignment of the base and of every outer stride, in bytes.
+pa_status check_aligned16(const pa_tensor* t, const char* name) {
+  const int eb = elem_bytes(t->dtype);
+  if (reinterpret_cast<uintptr_t>(t->data) & 15)
+    return fail(PA_ERR_INVALID_ARG, "%s base pointer must be 16-byte aligned", name);
+  for (int i = 0; i + 1 < t->ndim; ++i)
+    if ((t->stride[i] * eb) & 15)
+      return fail(PA_ERR_INVALID_ARG, "%s stride %d (%lld elements) must be a multiple of 16 bytes",
+                  name, i, (long long)t->stride[i]);
+  return PA_OK;
+}
+
+#define TRY(x)                   \
+  do {                           \
+    pa_status st_ = (x);         \
+    if (st_ != PA_OK) return st_; \
+  } while (0)
+
+struct Shapes {
+  int64_t T, S, MB, NB;
+};
+
+pa_status check_batch(const pa_config& c, const pa_tensor* q, const pa_tensor* k, const pa_tensor* v,
+                      const pa_tensor* bt, const pa_tensor* sl, const pa_tensor* qsl,
+                      const pa_tensor* out, Shapes* sh) {
+  TRY(check_tensor(q, "q", PA_DTYPE_BF16, 3));
+  TRY(check_tensor(k, "k_cache", c.kv_dtype, 4));
+  TRY(check_tensor(v, "v_cache", c.kv_dtype, 4));
+  TRY(check_tensor(bt, "block_table", PA_DTYPE_I32, 2));
+  TRY(check_tensor(sl, "seq_lens", PA_DTYPE_I32, 1));
+  TRY(check_tensor(qsl, "query_start_loc", PA_DTYPE_I32, 1));
+  if (out) TRY(check_tensor(out, "out", PA_DTYPE_BF16, 3));
+  const int64_t T = q->shape[0], S = sl->shape[0], NB = k->shape[0], MB = bt->shape[1];
+  if (q->shape[1] != c.num_q_heads || q->shape[2] != c.head_dim)
+    return fail(PA_ERR_INVALID_ARG, "q must be [T, %d, %d]", c.num_q_heads, c.head_dim);
+  for (const pa_tensor* kv : {k, v}) {
+    if (kv->shape[1] != c.block_size || kv->shape[2] != c.num_kv_heads || kv->shape[3] != c.head_dim)
+      return fail(PA_ERR_INVALID_ARG, "caches must be [num_blocks, %d, %d, %d]", c.block_size,
+                  c.num_kv_heads, c.head_dim);
+  }
+  if (v->shape[0] != NB) return fail(PA_ERR_INVALID_ARG, "k_cache and v_cache block counts differ");
+  if (bt->shape[0] != S) return fail(PA_ERR_INVALID_ARG, "block_table has %lld rows, seq_lens %lld",
+                                     (long long)bt->shape[0], (long long)S);
+  if (qsl->shape[0] != S + 1)
+    return fail(PA_ERR_INVALID_ARG, "query_start_loc must have num_seqs + 1 = %lld entries", (long long)(S + 1));
+  if (out && (out->shape[0] != T || out->shape[1] != c.num_q_heads || out->shape[2] != c.head_dim))
+    return fail(PA_ERR_INVALID_ARG, "out must have the shape of q");
+  if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
+  if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences per call (got %lld)", (long long)S);
+  if (MB * c.block_size > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
+  TRY(check_aligned16(q, "q"));
+  TRY(check_aligned16(k, "k_cache"));
+  TRY(check_aligned16(v, "v_cache"));
+  if (out) TRY(check_aligned16(out, "out"));
+  if (reinterpret_cast<uintptr_t>(bt->data) & 3 || reinterpret_cast<uintptr_t>(sl->data) & 3 ||
+      reinterpret_cast<uintptr_t>(qsl->data) & 3)
+    return fail(PA_ERR_INVALID_ARG, "int32 metadata must be 4-byte aligned");
+  sh->T = T;
+  sh->S = S;
+  sh->MB = MB;
+  sh->NB = NB;
+  return PA_OK;
+}
+
+pa::KvGeom geom(const pa_tensor* t) {
+  const int eb = elem_bytes(t->dtype);
+  return pa::KvGeom{t->stride[0] * eb, t->stride[1] * eb, t->stride[2] * eb};
+}
+
+pa_status hip_fail(hipError_t e, const char* what) {
+  return fail(PA_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kRingCap = 512;
+
+// Wait for the recorded events of one kind and add their durations.
+hipError_t flush_ring(pa_handle* h, int kind) {
+  pa_event_ring& r = h->ring[kind];
+  for (int i = 0; i < r.used; ++i) {
+    hipError_t e = hipEventSynchronize(r.stop[i]);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.start[i], r.stop[i]);
+    if (e != hipSuccess) return e;
+    h->total_ms[kind] += ms;
+    h->launches[kind] += 1;
+  }
+  r.used = 0;
+  return hipSuccess;
+}
+
+// Launch through `fn`, bracketed by an event pair when profiling.
+template <class F>
+hipError_t timed_launch(pa_handle* h, int kind, hipStream_t st, F&& fn) {
+  if (!h->profile) return fn();
+  pa_event_ring& r = h->ring[kind];
+  if (r.used == kRingCap) {
+    hipError_t e = flush_ring(h, kind);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = hipEventRecord(r.start[r.used], st);
+  if (e != hipSuccess) return e;
+  e = fn();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(r.stop[r.used], st);
+  if (e != hipSuccess) return e;
+  r.used += 1;
+  return hipSuccess;
+}
+
+void destroy_events(pa_handle* h) {
+  for (auto& r : h->ring) {
+    for (hipEvent_t ev : r.start) hipEventDestroy(ev);
+    for (hipEvent_t ev : r.stop) hipEventDestroy(ev);
+    r.start.clear();
+    r.stop.clear();
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pa_last_error(void) { return g_err.c_str(); }
+
+pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t max_seqs,
+                             int64_t max_blocks_per_seq, uint64_t* bytes) {
+  TRY(check_config(cfg));
+  if (!bytes) return fail(PA_ERR_INVALID_ARG, "bytes is NULL");
+  if (max_tokens < 0 || max_seqs < 0 || max_blocks_per_seq < 0)
+    return fail(PA_ERR_INVALID_ARG, "negative maximum");
+  // The split count grows with the table width and shrinks with the batch;
+  // take the largest requirement over all batch sizes up to max_seqs, with
+  // the fewest CUs the plan can assume (1), so any device is covered.
+  uint64_t best = kHeader;
+  const int64_t max_len = max_blocks_per_seq * cfg->block_size;
+  if (max_seqs >= 1 && max_len >= 1) {
+    // splits(S) <= min(ceil(max_len / kMinSeg), ceil(kWgPerCu * kMaxCus / (S * Hkv))); the
+    // product S * splits(S) is bounded by min(S * ceil(max_len / kMinSeg),
+    // kWgPerCu * kMaxCus / Hkv + S).
+    const int64_t by_len = max_seqs * cdiv(max_len, kMinSeg);
+    const int64_t by_target = (int64_t)kWgPerCu * kMaxCus / cfg->num_kv_heads + max_seqs;
+    const uint64_t rows = (uint64_t)std::min(by_len, by_target) * cfg->num_q_heads;
+    best += align256(rows * cfg->head_dim * 4) + align256(rows * 2 * 4);
+  }
+  *bytes = best;
+  return PA_OK;
+}
+
+pa_status pa_plan(const pa_handle* h, const pa_config* cfg, int32_t num_cus, int64_t num_tokens,
+                  int64_t num_seqs, int64_t max_blocks_per_seq, pa_plan_info* out) {
+  const pa_config* c = h ? &h->cfg : cfg;
+  TRY(check_config(c));
+  if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
+  if (num_tokens < 0 || num_seqs < 0 || max_blocks_per_seq < 0)
+    return fail(PA_ERR_INVALID_ARG, "negative size");
+  int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
+  make_plan(*c, cus, num_tokens, num_seqs, max_blocks_per_seq, out);
+  return PA_OK;
+}
+
+pa_status pa_create(const pa_config* cfg, pa_handle** out) {
+  TRY(check_config(cfg));
+  if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  pa_handle* h = new (std::nothrow) pa_handle;
+  if (!h) return fail(PA_ERR_INVALID_ARG, "out of host memory");
+  h->cfg = *cfg;
+  h->device = dev;
+  h->cus = cus > 0 ? cus : kMaxCus;
+  h->profile = (cfg->flags & PA_FLAG_PROFILE) != 0;
+  for (int k = 0; k < PA_KERNEL_KINDS; ++k) {
+    h->launches[k] = 0;
+    h->total_ms[k] = 0.0;
+  }
+  if (h->profile) {
+    for (auto& r : h->ring) {
+      r.start.resize(kRingCap);
+      r.stop.resize(kRingCap);
+      for (int i = 0; i < kRingCap; ++i) {
+        hipError_t e1 = hipEventCreate(&r.start[i]);
+        hipError_t e2 = hipEventCreate(&r.stop[i]);
+        if (e1 != hipSuccess || e2 != hipSuccess) {
+          r.start.resize(e1 == hipSuccess ? i + 1 : i);
+          r.stop.resize(e2 == hipSuccess ? i + 1 : i);
+          destroy_events(h);
+          delete h;
+          return hip_fail(e1 != hipSuccess ? e1 : e2, "hipEventCreate");
+        }
+      }
+    }
+  }
+  *out = h;
+  return PA_OK;
+}
+
+void pa_destroy(pa_handle* h) {
+  if (!h) return;
+  destroy_events(h);
+  delete h;
+}
+
+pa_status pa_profile_read(pa_handle* h, pa_profile* out, int reset) {
+  if (!h || !out) return fail(PA_ERR_INVALID_ARG, "handle or out is NULL");
+  for (int k = 0; k < PA_KERNEL_KINDS; ++k) {
+    hipError_t e = flush_ring(h, k);
+    if (e != hipSuccess) return hip_fail(e, "profile events");
+    out->launches[k] = h->launches[k];
+    out->total_ms[k] = h->total_ms[k];
+    if (reset) {
+      h->launches[k] = 0;
+      h->total_ms[k] = 0.0;
+    }
+  }
+  return PA_OK;
+}
+
+pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                     const pa_tensor* v_cache, const pa_tensor* block_table,
+                     const pa_tensor* seq_lens, const pa_tensor* query_start_loc, float scale,
+                     const pa_tensor* out, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
+  const pa_config& c = h->cfg;
+  if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
+  Shapes sh;
+  TRY(check_batch(c, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, &sh));
+  if (!(scale > 0.f) || !(scale < 1e30f)) return fail(PA_ERR_INVALID_ARG, "scale must be positive and finite");
+  pa_plan_info p;
+  make_plan(c, h->cus, sh.T, sh.S, sh.MB, &p);
+  if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
+    return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
+                (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
+  if (sh.S == 0 || sh.T == 0) return PA_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(c.workspace);
+
+  if (c.flags & PA_FLAG_VALIDATE) {
+    uint32_t* word = reinterpret_cast<uint32_t*>(ws);
+    hipError_t e = hipMemsetAsync(word, 0, 4, st);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    pa::ValidateArgs va{static_cast<const int32_t*>(block_table->data), block_table->stride[0],
+                        (int32_t)sh.MB, static_cast<const int32_t*>(seq_lens->data),
+                        static_cast<const int32_t*>(query_start_loc->data), (int32_t)sh.S,
+                        (int32_t)sh.T, (int32_t)sh.NB, c.block_size, word};
+    e = pa::launch_validate(va, st);
+    if (e != hipSuccess) return hip_fail(e, "validate launch");
+    uint32_t host_word = 0;
+    e = hipMemcpyAsync(&host_word, word, 4, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "validate readback");
+    if (host_word)
+      return fail(PA_ERR_DEVICE, "metadata check failed (code 0x%x: 1 qsl[0]!=0, 2 qsl decreasing, "
+                  "4 q_len>seq_len, 8 seq_len>table capacity, 16 block id out of range, "
+                  "32 qsl[S]>num_tokens)", host_word);
+  }
+
+  const bool fp8 = c.kv_dtype == PA_DTYPE_FP8_E4M3;
+  pa::BatchArgs a;
+  a.q = static_cast<const uint8_t*>(q->data);
+  a.q_tok = q->stride[0] * 2;
+  a.q_head = q->stride[1] * 2;
+  a.k = static_cast<const uint8_t*>(k_cache->data);
+  a.v = static_cast<const uint8_t*>(v_cache->data);
+  a.kg = geom(k_cache);
+  a.vg = geom(v_cache);
+  a.bt = static_cast<const int32_t*>(block_table->data);
+  a.bt_row = block_table->stride[0];
+  a.mb = (int32_t)sh.MB;
+  a.seq_lens = static_cast<const int32_t*>(seq_lens->data);
+  a.qsl = static_cast<const int32_t*>(query_start_loc->data);
+  a.out = static_cast<uint8_t*>(out->data);
+  a.o_tok = out->stride[0] * 2;
+  a.o_head = out->stride[1] * 2;
+  a.num_seqs = (int32_t)sh.S;
+  a.num_tokens = (int32_t)sh.T;
+  a.num_blocks = (int32_t)std::min<int64_t>(sh.NB, INT32_MAX);
+  a.block_size = c.block_size;
+  a.num_q_heads = c.num_q_heads;
+  a.num_kv_heads = c.num_kv_heads;
+  a.group = c.num_q_heads / c.num_kv_heads;
+  a.sl2 = scale * c.k_scale * 1.4426950408889634f;
+  a.v_scale = c.v_scale;
+
+  if (p.decode_launch) {
+    pa::DecodePlan dp;
+    dp.seg_len = p.segment_len;
+    dp.max_splits = p.max_splits;
+    const uint64_t rows = (uint64_t)sh.S * p.max_splits * c.num_q_heads;
+    dp.part_o = reinterpret_cast<float*>(ws + kHeader);
+    dp.part_ml = reinterpret_cast<float*>(ws + kHeader + align256(rows * c.head_dim * 4));
+    hipError_t e = timed_launch(h, PA_KERNEL_DECODE, st,
+                                [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    if (p.merge_launch) {
+      e = timed_launch(h, PA_KERNEL_MERGE, st,
+                       [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+      if (e != hipSuccess) return hip_fail(e, "merge launch");
+    }
+  }
+  if (p.prefill_launch) {
+    pa::PrefillPlan pp;
+    pp.block_q = p.block_q;
+    pp.work_items = (int32_t)(p.prefill_grid[0] / c.num_kv_heads);
+    hipError_t e = timed_launch(h, PA_KERNEL_PREFILL, st,
+                                [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
+    if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  }
+  return PA_OK;
+}
+
+pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tensor* v_cache,
+                          const pa_tensor* block_table, const pa_tensor* seq_lens,
+                          const pa_tensor* k_dense, const pa_tensor* v_dense, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
+  const pa_config& c = h->cfg;
+  TRY(check_tensor(k_cache, "k_cache", c.kv_dtype, 4));
+  TRY(check_tensor(v_cache, "v_cache", c.kv_dtype, 4));
+  TRY(check_tensor(block_table, "block_table", PA_DTYPE_I32, 2));
+  TRY(check_tensor(seq_lens, "seq_lens", PA_DTYPE_I32, 1));
+  TRY(check_tensor(k_dense, "k_dense", c.kv_dtype, 4));
+  TRY(check_tensor(v_dense, "v_dense", c.kv_dtype, 4));
+  const int64_t S = seq_lens->shape[0], MB = block_table->shape[1], NB = k_cache->shape[0];
+  for (const pa_tensor* kv : {k_cache, v_cache})
+    if (kv->shape[0] != NB || kv->shape[1] != c.block_size || kv->shape[2] != c.num_kv_heads ||
+        kv->shape[3] != c.head_dim)
+      return fail(PA_ERR_INVALID_ARG, "caches must be [num_blocks, %d, %d, %d]", c.block_size,
+                  c.num_kv_heads, c.head_dim);
+  if (block_table->shape[0] != S) return fail(PA_ERR_INVALID_ARG, "block_table rows != num_seqs");
+  for (const pa_tensor* dn : {k_dense, v_dense})
+    if (dn->shape[0] != S || dn->shape[1] != MB * c.block_size || dn->shape[2] != c.num_kv_heads ||
+        dn->shape[3] != c.head_dim)
+      return fail(PA_ERR_INVALID_ARG, "dense outputs must be [S, MB * block_size, Hkv, d]");
+  if (k_dense->stride[0] != v_dense->stride[0] || k_dense->stride[1] != v_dense->stride[1] ||
+      k_dense->stride[2] != v_dense->stride[2])
+    return fail(PA_ERR_INVALID_ARG, "k_dense and v_dense must share strides");
+  if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences");
+  if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
+  TRY(check_aligned16(k_cache, "k_cache"));
+  TRY(check_aligned16(v_cache, "v_cache"));
+  TRY(check_aligned16(k_dense, "k_dense"));
+  TRY(check_aligned16(v_dense, "v_dense"));
+  const int eb = elem_bytes(c.kv_dtype);
+  pa::GatherArgs g;
+  g.k = static_cast<const uint8_t*>(k_cache->data);
+  g.v = static_cast<const uint8_t*>(v_cache->data);
+  g.kg = geom(k_cache);
+  g.vg = geom(v_cache);
+  g.bt = static_cast<const int32_t*>(block_table->data);
+  g.bt_row = block_table->stride[0];
+  g.mb = (int32_t)MB;
+  g.seq_lens = static_cast<const int32_t*>(seq_lens->data);
+  g.kd = static_cast<uint8_t*>(k_dense->data);
+  g.vd = static_cast<uint8_t*>(v_dense->data);
+  g.d_seq = k_dense->stride[0] * eb;
+  g.d_tok = k_dense->stride[1] * eb;
+  g.d_head = k_dense->stride[2] * eb;
+  g.num_seqs = (int32_t)S;
+  g.num_blocks = (int32_t)std::min<int64_t>(NB, INT32_MAX);
+  g.block_size = c.block_size;
+  g.num_kv_heads = c.num_kv_heads;
+  g.row_bytes = c.head_dim * eb;
+  hipError_t e = pa::launch_gather(g, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return PA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,370 @@
+// Varlen / chunked-prefill attention over a paged KV cache
+// (arxiv 2511.11581, Sec. 4.4 Q-Blocks, Sec. 4.1 tiled softmax, Eq. 1-2).
+//
+// One workgroup = (Q-block, kv head g), 4 waves, BLOCK_M = 128 rows.  A
+// Q-block packs BLOCK_Q = 128 / G consecutive query tokens of one sequence
+// times the G query heads of kv head g; row r is (token r / G, head r % G).
+// Only sequences with at least 2 query tokens are handled here (single-token
+// rows go to the decode kernel).  K/V tiles of 64 keys are gathered through
+// the block table with 16-byte loads into registers (prefetching the next
+// tile while the current one is computed) and staged in LDS: K in natural
+// row layout, V transposed.  Each wave owns 32 rows:
+//   S^T[64 keys x 32 rows] = K Q^T   (v_mfma_f32_32x32x16_bf16)
+//   online softmax, one lane per row; max/sum finish with a permlane32 swap
+//   O^T[d x 32 rows]  += V^T P^T     (P^T taken from the S^T registers)
+// Keys run from 0 to the largest prefix of the block; only tiles that cross
+// the diagonal are masked.
+//
+// Work order: the grid enumerates (Q-block, kv head) with the kv head
+// fastest, so all workgroups of one kv head land on the same XCD when
+// Hkv = 8.  Q-blocks are dealt in rounds: round r holds the r-th Q-block
+// from the end of every sequence that has more than r of them, so the
+// heaviest (latest) Q-blocks start first.
+#include "common.hpp"
+#include "kernels.h"
+
+namespace pa {
+
+namespace {
+
+constexpr int kTileN = 64;     // keys per tile
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ int wave_sum(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+__device__ __forceinline__ int wave_max(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = max(x, __shfl_xor(x, o));
+  return x;
+}
+
+// Number of Q-blocks of sequence i (0 for decode / empty rows).
+__device__ __forceinline__ int nqb_of(const int32_t* qsl, int i, int bq) {
+  const int q = qsl[i + 1] - qsl[i];
+  return q >= 2 ? (q + bq - 1) / bq : 0;
+}
+
+// Map work item wi to (sequence, Q-block index), rounds order.  Returns
+// false if wi is beyond the batch's Q-blocks.  Executed by every wave.
+__device__ bool find_work(const int32_t* qsl, int S, int bq, int wi, int& seq, int& qb) {
+  const int lane = threadIdx.x & 63;
+  int mx = 0;
+  for (int i = lane; i < S; i += 64) mx = max(mx, nqb_of(qsl, i, bq));
+  mx = wave_max(mx);
+  // C(r) = sum_i min(nqb_i, r): items in rounds < r.  Find largest r with C(r) <= wi.
+  int lo = 0, hi = mx;  // C(mx) = total
+  {
+    int tot = 0;
+    for (int i = lane; i < S; i += 64) tot += nqb_of(qsl, i, bq);
+    tot = wave_sum(tot);
+    if (wi >= tot) return false;
+  }
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    int c = 0;
+    for (int i = lane; i < S; i += 64) c += min(nqb_of(qsl, i, bq), mid);
+    c = wave_sum(c);
+    if (c <= wi) lo = mid; else hi = mid;
+  }
+  const int r = lo;
+  int c = 0;
+  for (int i = lane; i < S; i += 64) c += min(nqb_of(qsl, i, bq), r);
+  int idx = wi - wave_sum(c);
+  // idx-th sequence (in order) with nqb > r
+  for (int base = 0; base < S; base += 64) {
+    const int i = base + lane;
+    const int n = i < S ? nqb_of(qsl, i, bq) : 0;
+    const bool pred = n > r;
+    const uint64_t b = __ballot(pred);
+    const int cnt = __popcll(b);
+    if (idx < cnt) {
+      const uint64_t below = b & ((1ull << lane) - 1ull);
+      const bool hit = pred && __popcll(below) == idx;
+      const uint64_t hb = __ballot(hit);
+      const int src = __ffsll((unsigned long long)hb) - 1;
+      const int nq = __shfl(n, src);
+      seq = base + src;
+      qb = nq - 1 - r;
+      return true;
+    }
+    idx -= cnt;
+  }
+  return false;
+}
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, PrefillPlan pp) {
+  constexpr int EB = FP8 ? 1 : 2;
+  constexpr int CH = D * EB / 16;                 // 16-byte chunks per cached row
+  constexpr int KLD = kTileN * CH / kThreads;     // K loads per thread
+  constexpr int VTASKS = 16 * CH;                 // (4-key group, chunk) pairs
+  constexpr int DPC = 16 / EB;                    // d values per chunk
+  constexpr int KROW = 2 * D + 16;                // LDS bytes per K row (bf16 + pad)
+  constexpr int VROW = 2 * kTileN + 16;           // LDS bytes per V^T row
+  constexpr int NT = D / 16;                      // 16-wide d steps of Q K^T
+  constexpr int NDB = D / 32;                     // 32-row d blocks of O^T
+  static_assert(KLD >= 1, "tile too small");
+
+  __shared__ __attribute__((aligned(16))) uint8_t ks[kTileN * KROW];
+  __shared__ __attribute__((aligned(16))) uint8_t vts[D * VROW];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, hf = lane >> 5;
+  const int Hkv = a.num_kv_heads;
+  const int g = blockIdx.x % Hkv;
+  const int wi = blockIdx.x / Hkv;
+  const int G = a.group, BQ = pp.block_q, bs = a.block_size;
+
+  int seq, qb;
+  if (!find_work(a.qsl, a.num_seqs, BQ, wi, seq, qb)) return;
+  seq = uniform(seq);
+  qb = uniform(qb);
+
+  const int t0 = a.qsl[seq];
+  const int qlen = a.qsl[seq + 1] - t0;
+  const int L = min(a.seq_lens[seq], a.mb * a.block_size);
+  const int ctx = L - qlen;
+  if (ctx < 0 || t0 < 0 || t0 + qlen > a.num_tokens) return;
+  const int tok_lo = qb * BQ;                              // first token of the block
+  const int tok_hi = min(tok_lo + BQ, qlen);               // one past the last
+  const int kv_len = ctx + tok_hi;                         // keys needed by the block
+  const int ntiles = (kv_len + kTileN - 1) / kTileN;
+  const int32_t* bt_row = a.bt + (int64_t)seq * a.bt_row;
+
+  // This lane's row.
+  const int row = wave * 32 + n;
+  const int tl = tok_lo + row / G;                         // token index inside the query
+  const int hh = row % G;
+  const bool rvalid = tl < tok_hi;
+  const int pos = ctx + (rvalid ? tl : tok_hi - 1);        // absolute position (causal bound)
+  const int wave_pos_max = ctx + min(tok_lo + (wave * 32 + 31) / G, tok_hi - 1);
+  const int blk_pos_min = ctx + tok_lo;
+
+  // Q^T B operands: d = 16t + 8hf + j of this row.
+  bf16x8 qt[NT];
+  {
+    const uint8_t* qrow = a.q + (int64_t)(t0 + (rvalid ? tl : tok_hi - 1)) * a.q_tok +
+                          (int64_t)(g * G + hh) * a.q_head;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      qt[t] = __builtin_bit_cast(bf16x8, ld16_cached(qrow + 2 * (16 * t + 8 * hf)));
+  }
+
+  const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
+  const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
+
+  // ---- tile loader: global -> registers
+  u32x4 kreg[KLD];
+  u32x4 vreg[4];
+  auto load_tile = [&](int tile) {
+    const int tb = tile * kTileN;
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      const int flat = tid + kThreads * i;
+      const int c = flat % CH, key = flat / CH;
+      const int p = tb + key;
+      u32x4 w = {0, 0, 0, 0};
+      if (p < kv_len) {
+        const int pg = page_of(bt_row, p, bs, a.num_blocks);
+        w = ld16(kbase + (int64_t)pg * a.kg.blk + (int64_t)(p % bs) * a.kg.slot + 16 * c);
+      }
+      kreg[i] = w;
+    }
+    {
+      const int c = tid % CH, m = tid / CH;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int p = tb + 4 * m + r;
+        u32x4 w = {0, 0, 0, 0};
+        if (tid < VTASKS && p < kv_len) {
+          const int pg = page_of(bt_row, p, bs, a.num_blocks);
+          w = ld16(vbase + (int64_t)pg * a.vg.blk + (int64_t)(p % bs) * a.vg.slot + 16 * c);
+        }
+        vreg[r] = w;
+      }
+    }
+  };
+  // ---- registers -> LDS (K natural bf16 rows, V transposed bf16)
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      const int flat = tid + kThreads * i;
+      const int c = flat % CH, key = flat / CH;
+      uint8_t* dst = ks + key * KROW + 2 * DPC * c;
+      if constexpr (FP8) {
+        bf16x8 lo, hi;
+        fp8x16_to_bf16(kreg[i], lo, hi);
+        *(bf16x8*)dst = lo;
+        *(bf16x8*)(dst + 16) = hi;
+      } else {
+        *(u32x4*)dst = kreg[i];
+      }
+    }
+    if (tid < VTASKS) {
+      const int c = tid % CH, m = tid / CH;
+      // keys 4m..4m+3 -> V^T positions: bits 2 and 3 of the key swapped
+      const int pb = 16 * (m >> 2) + 8 * (m & 1) + 4 * ((m >> 1) & 1);
+      uint8_t* wp = vts + (c * DPC) * VROW + 2 * pb;
+      if constexpr (FP8) {
+        uint32_t w[4][8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            u32x2 cv = fp8x4_to_bf16x4(vreg[r][q]);
+            w[r][2 * q] = cv[0];
+            w[r][2 * q + 1] = cv[1];
+          }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int dw = e >> 1;
+          uint32_t lo, hi;
+          if (e & 1) {
+            lo = (w[0][dw] >> 16) | (w[1][dw] & 0xFFFF0000u);
+            hi = (w[2][dw] >> 16) | (w[3][dw] & 0xFFFF0000u);
+          } else {
+            lo = (w[0][dw] & 0xFFFFu) | (w[1][dw] << 16);
+            hi = (w[2][dw] & 0xFFFFu) | (w[3][dw] << 16);
+          }
+          *(u32x2*)(wp + e * VROW) = u32x2{lo, hi};
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int dw = e >> 1;
+          uint32_t lo, hi;
+          if (e & 1) {
+            lo = (vreg[0][dw] >> 16) | (vreg[1][dw] & 0xFFFF0000u);
+            hi = (vreg[2][dw] >> 16) | (vreg[3][dw] & 0xFFFF0000u);
+          } else {
+            lo = (vreg[0][dw] & 0xFFFFu) | (vreg[1][dw] << 16);
+            hi = (vreg[2][dw] & 0xFFFFu) | (vreg[3][dw] << 16);
+          }
+          *(u32x2*)(wp + e * VROW) = u32x2{lo, hi};
+        }
+      }
+    }
+  };
+
+  float m_run = kNegInf, l_run = 0.f;
+  f32x16 o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+
+  load_tile(0);
+  store_tile();
+  __syncthreads();
+
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const int tb = tile * kTileN;
+    if (tile + 1 < ntiles) load_tile(tile + 1);
+
+    if (tb <= wave_pos_max) {
+      // ---- S^T = K Q^T for 2 blocks of 32 keys
+      f32x16 sacc[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x16 acc;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+        const uint8_t* kr = ks + (32 * kb + n) * KROW + 16 * hf;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          acc = mfma32(*(const bf16x8*)(kr + 32 * t), qt[t], acc);
+        sacc[kb] = acc;
+      }
+      // ---- online softmax; lane holds keys 32kb + 8(i/4) + 4hf + i%4 of its row
+      const bool diag = tb + kTileN - 1 > blk_pos_min;
+      float mx = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float x = sacc[kb][i] * a.sl2;
+          if (diag) {
+            const int key = tb + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
+            x = key <= pos ? x : kNegInf;
+          }
+          sacc[kb][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = xor32_max(mx);
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - m_new);
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float pv = fast_exp2(sacc[kb][i] - m_new);
+          sacc[kb][i] = pv;
+          psum += pv;
+        }
+      l_run = l_run * alpha + psum;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+      // ---- O^T += V^T P^T over 4 steps of 16 keys
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const f32x16& sp = sacc[u >> 1];
+        const int r0 = 8 * (u & 1);
+        u32x4 pw = {pack_bf16(sp[r0 + 0], sp[r0 + 1]), pack_bf16(sp[r0 + 2], sp[r0 + 3]),
+                    pack_bf16(sp[r0 + 4], sp[r0 + 5]), pack_bf16(sp[r0 + 6], sp[r0 + 7])};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8 va = *(const bf16x8*)(vts + (32 * db + n) * VROW + 2 * (16 * u + 8 * hf));
+          o[db] = mfma32(va, pb, o[db]);
+        }
+      }
+    }
+    __syncthreads();
+    if (tile + 1 < ntiles) {
+      store_tile();
+      __syncthreads();
+    }
+  }
+
+  // ---- finalise: out = O / l, bf16
+  const float l_tot = xor32_sum(l_run);
+  if (rvalid) {
+    const float inv = a.v_scale / l_tot;
+    uint8_t* orow = a.out + (int64_t)(t0 + tl) * a.o_tok + (int64_t)(g * G + hh) * a.o_head;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int d0 = 32 * db + 8 * q + 4 * hf;
+        u32x2 w = {pack_bf16(o[db][4 * q] * inv, o[db][4 * q + 1] * inv),
+                   pack_bf16(o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv)};
+        *(u32x2*)(orow + 2 * d0) = w;
+      }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
+                          hipStream_t st) {
+  const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
+  if (blocks <= 0) return hipSuccess;
+  dim3 grid((unsigned)blocks), block(kThreads);
+  if (head_dim == 128) {
+    if (fp8) prefill_kernel<128, true><<<grid, block, 0, st>>>(a, p);
+    else prefill_kernel<128, false><<<grid, block, 0, st>>>(a, p);
+  } else if (head_dim == 64) {
+    if (fp8) prefill_kernel<64, true><<<grid, block, 0, st>>>(a, p);
+    else prefill_kernel<64, false><<<grid, block, 0, st>>>(a, p);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace pa

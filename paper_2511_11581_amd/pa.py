@@ -1,0 +1,271 @@
+"""ctypes binding of libpa.so (declared in include/pa.h).
+
+Argument marshalling only: torch tensors are described by ``pa_tensor``
+(device pointer, dtype, shape, strides) and the current HIP stream is
+passed through.  Every attention step runs in the library's HIP kernels;
+there is no fallback: if ``libpa.so`` is missing or fails to load, the first
+call raises.
+
+The functions keep the C names: ``pa_workspace_bytes``, ``pa_create``,
+``pa_forward``, ``pa_debug_gather``, ``pa_plan``, ``pa_destroy``,
+``pa_last_error``.  ``PagedAttention`` bundles a handle with a
+workspace allocated through torch.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpa.so")
+
+PA_OK = 0
+PA_ERR_INVALID_ARG = 1
+PA_ERR_UNSUPPORTED = 2
+PA_ERR_WORKSPACE = 3
+PA_ERR_DEVICE = 4
+STATUS_NAMES = {0: "PA_OK", 1: "PA_ERR_INVALID_ARG", 2: "PA_ERR_UNSUPPORTED",
+                3: "PA_ERR_WORKSPACE", 4: "PA_ERR_DEVICE"}
+
+PA_DTYPE_BF16 = 0
+PA_DTYPE_FP8_E4M3 = 1
+PA_DTYPE_I32 = 2
+PA_DTYPE_F32 = 3
+PA_FLAG_VALIDATE = 1
+PA_FLAG_PROFILE = 2
+PA_KERNEL_KINDS = 3
+KERNEL_NAMES = ("decode", "merge", "prefill")
+PA_MAX_DIMS = 4
+
+# Every function declared in include/pa.h.
+EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
+           "pa_profile_read", "pa_destroy", "pa_last_error")
+
+
+class pa_tensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * PA_MAX_DIMS), ("stride", ctypes.c_int64 * PA_MAX_DIMS)]
+
+
+class pa_config(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float),
+                ("v_scale", ctypes.c_float), ("flags", ctypes.c_uint32),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_uint64)]
+
+
+class pa_plan_info(ctypes.Structure):
+    _fields_ = [("decode_launch", ctypes.c_int32), ("decode_tile", ctypes.c_int32),
+                ("decode_waves", ctypes.c_int32), ("segment_len", ctypes.c_int32),
+                ("max_splits", ctypes.c_int32), ("merge_launch", ctypes.c_int32),
+                ("prefill_launch", ctypes.c_int32), ("block_m", ctypes.c_int32),
+                ("block_q", ctypes.c_int32), ("prefill_tile", ctypes.c_int32),
+                ("decode_grid", ctypes.c_int64 * 3), ("merge_grid", ctypes.c_int64 * 3),
+                ("prefill_grid", ctypes.c_int64 * 3), ("workspace_bytes", ctypes.c_uint64)]
+
+    def as_dict(self):
+        d = {}
+        for name, _ in self._fields_:
+            v = getattr(self, name)
+            d[name] = list(v) if hasattr(v, "__len__") else int(v)
+        return d
+
+
+class pa_profile(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64 * PA_KERNEL_KINDS),
+                ("total_ms", ctypes.c_double * PA_KERNEL_KINDS)]
+
+
+class PaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libpa.so; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2511_11581_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    T = ctypes.POINTER(pa_tensor)
+    C = ctypes.POINTER(pa_config)
+    lib.pa_workspace_bytes.argtypes = [C, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                       ctypes.POINTER(ctypes.c_uint64)]
+    lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
+    lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
+    lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, T, P]
+    lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                            ctypes.POINTER(pa_plan_info)]
+    lib.pa_profile_read.argtypes = [P, ctypes.POINTER(pa_profile), ctypes.c_int]
+    lib.pa_destroy.argtypes = [P]
+    lib.pa_destroy.restype = None
+    lib.pa_last_error.argtypes = []
+    lib.pa_last_error.restype = ctypes.c_char_p
+    for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
+                 "pa_profile_read"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def pa_last_error() -> str:
+    return load_library().pa_last_error().decode()
+
+
+def _check(st: int):
+    if st != PA_OK:
+        raise PaError(st, pa_last_error())
+
+
+_DTYPES = {torch.bfloat16: PA_DTYPE_BF16, torch.float8_e4m3fn: PA_DTYPE_FP8_E4M3,
+           torch.int32: PA_DTYPE_I32, torch.float32: PA_DTYPE_F32}
+
+
+def describe(t: torch.Tensor) -> pa_tensor:
+    """pa_tensor descriptor of a torch tensor (no copy)."""
+    if t.dim() > PA_MAX_DIMS:
+        raise ValueError("at most 4 dimensions")
+    d = pa_tensor()
+    d.data = t.data_ptr() if t.numel() > 0 else 0
+    d.dtype = _DTYPES.get(t.dtype, -1)
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.stride[i] = t.stride(i)
+    return d
+
+
+def make_config(num_q_heads, num_kv_heads, head_dim, block_size=16, kv_dtype=PA_DTYPE_BF16,
+                k_scale=1.0, v_scale=1.0, flags=0, workspace=0, workspace_bytes=0) -> pa_config:
+    c = pa_config()
+    c.num_q_heads, c.num_kv_heads, c.head_dim, c.block_size = (num_q_heads, num_kv_heads,
+                                                              head_dim, block_size)
+    c.kv_dtype = kv_dtype
+    c.k_scale, c.v_scale = k_scale, v_scale
+    c.flags = flags
+    c.workspace = workspace
+    c.workspace_bytes = workspace_bytes
+    return c
+
+
+def pa_workspace_bytes(cfg: pa_config, max_tokens: int, max_seqs: int,
+                       max_blocks_per_seq: int) -> int:
+    out = ctypes.c_uint64()
+    _check(load_library().pa_workspace_bytes(ctypes.byref(cfg), max_tokens, max_seqs,
+                                             max_blocks_per_seq, ctypes.byref(out)))
+    return int(out.value)
+
+
+def pa_create(cfg: pa_config) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    _check(load_library().pa_create(ctypes.byref(cfg), ctypes.byref(h)))
+    return h
+
+
+def pa_destroy(h) -> None:
+    if h:
+        load_library().pa_destroy(h)
+
+
+def pa_plan(h=None, cfg: Optional[pa_config] = None, num_cus: int = 0, num_tokens: int = 0,
+            num_seqs: int = 0, max_blocks_per_seq: int = 0) -> dict:
+    info = pa_plan_info()
+    _check(load_library().pa_plan(h, ctypes.byref(cfg) if cfg is not None else None, num_cus,
+                                  num_tokens, num_seqs, max_blocks_per_seq, ctypes.byref(info)))
+    return info.as_dict()
+
+
+def pa_profile_read(h, reset: bool = True) -> dict:
+    """{kernel: (launches, total_ms)} recorded under PA_FLAG_PROFILE."""
+    prof = pa_profile()
+    _check(load_library().pa_profile_read(h, ctypes.byref(prof), int(reset)))
+    return {KERNEL_NAMES[k]: (int(prof.launches[k]), float(prof.total_ms[k]))
+            for k in range(PA_KERNEL_KINDS)}
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(stream)
+
+
+def pa_forward(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+               stream=None) -> None:
+    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
+    _check(load_library().pa_forward(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
+                                     ctypes.byref(ds[6]), _stream(stream)))
+
+
+def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, k_dense, v_dense,
+                    stream=None) -> None:
+    ds = [describe(t) for t in (k_cache, v_cache, block_table, seq_lens, k_dense, v_dense)]
+    _check(load_library().pa_debug_gather(h, *(ctypes.byref(d) for d in ds), _stream(stream)))
+
+
+class PagedAttention:
+    """A handle plus a torch-allocated workspace sized for the given maxima."""
+
+    def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, block_size: int = 16,
+                 kv_dtype: torch.dtype = torch.bfloat16, k_scale: float = 1.0,
+                 v_scale: float = 1.0, max_tokens: int = 1, max_seqs: int = 1,
+                 max_blocks_per_seq: int = 1, validate: bool = False, profile: bool = False,
+                 device="cuda"):
+        kvd = _DTYPES.get(kv_dtype, -1)
+        flags = (PA_FLAG_VALIDATE if validate else 0) | (PA_FLAG_PROFILE if profile else 0)
+        cfg = make_config(num_q_heads, num_kv_heads, head_dim, block_size, kvd, k_scale, v_scale,
+                          flags)
+        nbytes = pa_workspace_bytes(cfg, max_tokens, max_seqs, max_blocks_per_seq)
+        self._ws_raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        base = self._ws_raw.data_ptr()
+        cfg.workspace = (base + 255) & ~255
+        cfg.workspace_bytes = nbytes
+        self.cfg = cfg
+        self.handle = pa_create(cfg)
+
+    def plan(self, num_tokens: int, num_seqs: int, max_blocks_per_seq: int) -> dict:
+        return pa_plan(self.handle, None, 0, num_tokens, num_seqs, max_blocks_per_seq)
+
+    def forward(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
+                scale: Optional[float] = None, out: Optional[torch.Tensor] = None, stream=None):
+        if out is None:
+            out = torch.empty_like(q)
+        if scale is None:
+            scale = q.shape[-1] ** -0.5
+        pa_forward(self.handle, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
+                   scale, out, stream)
+        return out
+
+    def profile(self, reset: bool = True) -> dict:
+        return pa_profile_read(self.handle, reset)
+
+    def gather(self, k_cache, v_cache, block_table, seq_lens, stream=None):
+        S, MB = block_table.shape
+        shape = (S, MB * k_cache.shape[1], k_cache.shape[2], k_cache.shape[3])
+        kd = torch.zeros(shape, dtype=k_cache.dtype, device=k_cache.device)
+        vd = torch.zeros(shape, dtype=v_cache.dtype, device=v_cache.device)
+        pa_debug_gather(self.handle, k_cache, v_cache, block_table, seq_lens, kd, vd, stream)
+        return kd, vd
+
+    def close(self):
+        if getattr(self, "handle", None):
+            pa_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

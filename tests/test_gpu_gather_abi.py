@@ -1,0 +1,122 @@
+"""Bit-exact block-table addressing (gather-only debug mode) and the ABI's
+error reporting on a GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_11581_amd import pa
+from paper_2511_11581_amd import workloads as W
+from gpu_util import attention_for, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def gather_check(w):
+    att = attention_for(w)
+    wd = w.to("cuda")
+    kd, vd = att.gather(wd.k_cache, wd.v_cache, wd.block_table, wd.seq_lens)
+    torch.cuda.synchronize()
+    wc = w.to("cpu")
+    rk, rv = oracle.gather(wc.k_cache, wc.v_cache, wc.block_table, wc.seq_lens)
+    eb = 1 if w.kv_fp8 else 2
+    kb = kd.cpu().view(torch.uint8).numpy().reshape(rk.shape)
+    vb = vd.cpu().view(torch.uint8).numpy().reshape(rv.shape)
+    for i, L in enumerate(wc.seq_lens.tolist()):
+        assert np.array_equal(kb[i, :L], rk[i, :L]), f"K bytes differ in sequence {i}"
+        assert np.array_equal(vb[i, :L], rv[i, :L]), f"V bytes differ in sequence {i}"
+        assert not kb[i, L:].any(), "positions past seq_len were written"
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_gather_benchmark_batches(k):
+    gather_check(W.make_config(k))
+
+
+def test_gather_long_fp8_subset():
+    w = W.make_config(5, device="cuda")
+    sub = W.Workload(**{**w.__dict__})
+    sub.block_table = w.block_table[:3].contiguous()
+    sub.seq_lens = w.seq_lens[:3].contiguous()
+    sub.query_start_loc = w.query_start_loc[:4].contiguous()
+    sub.q = w.q[:3].contiguous()
+    sub.ctx_lens, sub.q_lens = w.ctx_lens[:3], w.q_lens[:3]
+    gather_check(sub)
+
+
+@pytest.mark.parametrize("bs,kv", [(16, "bf16"), (32, "fp8"), (64, "bf16")])
+def test_gather_random_small(bs, kv):
+    w = W.make_batch([(37, 1), (0, 100), (250, 7), (1, 0)], 8, 2, 64, kv_dtype=kv, block_size=bs,
+                     seed=bs, pool_blocks=64, table_width=20)
+    gather_check(w)
+
+
+# ---- error reporting -----------------------------------------------------------
+
+def _w():
+    return W.make_batch([(30, 1), (0, 20)], 8, 2, 128, seed=3).to("cuda")
+
+
+def _call(att, w, **over):
+    args = dict(q=w.q, k_cache=w.k_cache, v_cache=w.v_cache, block_table=w.block_table,
+                seq_lens=w.seq_lens, query_start_loc=w.query_start_loc, scale=w.scale,
+                out=torch.empty_like(w.q))
+    args.update(over)
+    pa.pa_forward(att.handle, args["q"], args["k_cache"], args["v_cache"], args["block_table"],
+                  args["seq_lens"], args["query_start_loc"], args["scale"], args["out"])
+
+
+@pytest.mark.parametrize("bad", ["q_dtype", "out_shape", "q_misaligned", "table_rows", "qsl_len",
+                                 "cache_heads", "scale", "kv_dtype"])
+def test_invalid_arguments_are_reported_before_launch(bad):
+    w = _w()
+    att = attention_for(w)
+    over = {}
+    if bad == "q_dtype":
+        over["q"] = w.q.float()
+    elif bad == "out_shape":
+        over["out"] = torch.empty(w.q.shape[0] + 1, *w.q.shape[1:], dtype=torch.bfloat16, device="cuda")
+    elif bad == "q_misaligned":
+        buf = torch.empty(w.q.numel() + 1, dtype=torch.bfloat16, device="cuda")
+        over["q"] = buf[1:].view(w.q.shape)
+    elif bad == "table_rows":
+        over["block_table"] = w.block_table[:1]
+    elif bad == "qsl_len":
+        over["query_start_loc"] = w.query_start_loc[:-1]
+    elif bad == "cache_heads":
+        over["k_cache"] = w.k_cache[:, :, :1]
+    elif bad == "scale":
+        over["scale"] = float("nan")
+    elif bad == "kv_dtype":
+        over["k_cache"] = w.k_cache.view(torch.float8_e4m3fn)[..., :128]
+    with pytest.raises(pa.PaError) as ei:
+        _call(att, w, **over)
+    assert ei.value.status == pa.PA_ERR_INVALID_ARG, str(ei.value)
+
+
+def test_workspace_too_small():
+    w = W.make_batch([(3000, 1), (2000, 1)], 8, 2, 128, seed=4).to("cuda")
+    att = attention_for(w, max_blocks=2)  # sized for short sequences only
+    with pytest.raises(pa.PaError) as ei:
+        _call(att, w)
+    assert ei.value.status == pa.PA_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("bad", ["block_id", "q_gt_L", "qsl_order"])
+def test_validate_flag_reports_bad_metadata(bad):
+    w = _w()
+    att = attention_for(w, validate=True)
+    bt, sl, qsl = w.block_table.clone(), w.seq_lens.clone(), w.query_start_loc.clone()
+    if bad == "block_id":
+        bt[0, 0] = w.num_blocks + 5
+    elif bad == "q_gt_L":
+        sl[1] = 3
+    elif bad == "qsl_order":
+        qsl[1] = 25
+        qsl[2] = 21
+    with pytest.raises(pa.PaError) as ei:
+        _call(att, w, block_table=bt, seq_lens=sl, query_start_loc=qsl)
+    assert ei.value.status == pa.PA_ERR_DEVICE
+    # the well-formed batch passes validation and runs
+    _call(att, w)
+    torch.cuda.synchronize()

@@ -1,0 +1,109 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Tolerances: max abs 2e-2 / mean abs 2e-3 with bf16 K/V, 5e-2 / 5e-3 with
+fp8 K/V.  Small batches are compared element by element on every valid
+row; the five benchmark batches at full size on sampled rows (first and
+last token of every sequence plus random rows), in the launch configuration
+the benchmark times.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2511_11581_amd import workloads as W
+from gpu_util import (SENTINEL, attention_for, check_close, oracle_full, oracle_rows, run_gpu,
+                      sample_rows, valid_token_count)
+
+pytestmark = pytest.mark.gpu
+
+
+def full_check(w):
+    out = run_gpu(w)
+    ref = oracle_full(w)
+    T = valid_token_count(w)
+    check_close(out[:T], ref[:T], w.kv_fp8, w.name)
+    assert (out[T:].float() == SENTINEL).all(), "rows past query_start_loc[S] were written"
+    return out
+
+
+SMALL = {
+    # name: (seqs [(ctx, q)], Hq, Hkv, d, kv, block_size, extra kwargs)
+    "decode_g4_d64": ([(17, 1), (64, 1), (100, 1), (255, 1)], 8, 2, 64, "bf16", 16, {}),
+    "decode_g1": ([(40, 1), (700, 1), (1, 1)], 4, 4, 128, "bf16", 16, {}),
+    "decode_g8_split": ([(3000, 1), (257, 1), (0, 1), (1500, 1)], 16, 2, 128, "bf16", 16, {}),
+    "decode_g16_split": ([(2200, 1), (31, 1)], 16, 1, 128, "bf16", 16, {}),
+    "decode_g2_d64_split": ([(1025, 1), (4096, 1), (15, 1)], 4, 2, 64, "bf16", 16, {}),
+    "decode_bs32": ([(990, 1), (33, 1)], 8, 2, 128, "bf16", 32, {}),
+    "decode_fp8": ([(1800, 1), (77, 1), (4000, 1)], 8, 1, 128, "fp8", 16, {}),
+    "decode_fp8_d64": ([(600, 1), (9, 1)], 8, 2, 64, "fp8", 16, {}),
+    "prefill_g4": ([(0, 100), (0, 33), (0, 2)], 8, 2, 128, "bf16", 16, {}),
+    "prefill_g1": ([(0, 300), (0, 129)], 2, 2, 128, "bf16", 16, {}),
+    "prefill_g8_d64": ([(0, 77), (0, 16), (0, 17)], 16, 2, 64, "bf16", 16, {}),
+    "prefill_g16": ([(0, 45), (0, 9)], 16, 1, 128, "bf16", 16, {}),
+    "chunked": ([(500, 64), (17, 130), (1000, 3)], 8, 2, 128, "bf16", 16, {}),
+    "chunked_bs32": ([(45, 80), (300, 40)], 8, 2, 128, "bf16", 32, {}),
+    "prefill_fp8": ([(0, 150), (200, 70)], 8, 2, 128, "fp8", 16, {}),
+    "mixed": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1), (0, 2)], 32, 8, 128, "bf16", 16, {}),
+    "mixed_d64_g4": ([(0, 50), (130, 1), (60, 20)], 8, 2, 64, "bf16", 16, {}),
+    "empty_queries": ([(50, 0), (30, 1), (0, 0), (20, 5)], 8, 2, 128, "bf16", 16, {}),
+    "padded_rows_wide_table": ([(70, 1), (0, 40)], 8, 2, 128, "bf16", 16,
+                               dict(token_pad=5, table_width=20, pool_blocks=64)),
+    "ragged_tails": ([(15, 1), (16, 1), (17, 1), (31, 2), (33, 31), (0, 63), (0, 65)], 8, 2, 128,
+                     "bf16", 16, {}),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_batches_match_oracle(name):
+    seqs, Hq, Hkv, d, kv, bs, extra = SMALL[name]
+    w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=hash(name) % 1000,
+                     name=name, **extra)
+    full_check(w)
+
+
+def test_shuffled_mixed_order():
+    seqs = [(c, 1) for c in (900, 20, 3000, 450)] + [(c, q) for c, q in ((0, 70), (250, 33))]
+    order = [4, 0, 2, 5, 1, 3]
+    w = W.make_batch([seqs[i] for i in order], 16, 4, 128, seed=5, name="shuffled")
+    full_check(w)
+
+
+def test_config1_full():
+    full_check(W.make_config(1))
+
+
+@pytest.mark.parametrize("k,nrows", [(2, 512), (3, 384), (4, 512), (5, 96)])
+def test_benchmark_batches_sampled(k, nrows):
+    w = W.make_config(k, device="cuda")
+    out = run_gpu(w)
+    rows = sample_rows(w, nrows, seed=k)
+    ref = oracle_rows(w, rows)
+    got = torch.stack([out[t, h] for t, h in rows])
+    check_close(got, ref, w.kv_fp8, w.name)
+    T = valid_token_count(w)
+    assert torch.isfinite(out[:T].float()).all()
+
+
+def test_config4_shuffled_sampled():
+    w = W.make_config(4, device="cuda", shuffle=True)
+    out = run_gpu(w)
+    rows = sample_rows(w, 256, seed=44)
+    ref = oracle_rows(w, rows)
+    check_close(torch.stack([out[t, h] for t, h in rows]), ref, False, "config4-shuffled")
+
+
+def test_deterministic_bitwise():
+    w = W.make_config(4, device="cuda")
+    att = attention_for(w)
+    a = run_gpu(w, att)
+    b = run_gpu(w, att)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_empty_batch_is_a_no_op():
+    w = W.make_batch([], 8, 2, 128, seed=1, pool_blocks=2)
+    out = run_gpu(w)
+    assert out.shape[0] == 0
+    w = W.make_batch([(10, 0)], 8, 2, 128, seed=1, token_pad=3)
+    out = run_gpu(w)
+    assert (out.float() == SENTINEL).all()
