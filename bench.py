@@ -170,6 +170,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="headline batch (1..5)")
     ap.add_argument("--only", action="store_true", help="measure the headline batch only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
+                    help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this path has no multi-GPU mode (asked for {args.gpus}).",
@@ -183,6 +185,15 @@ def main():
         hip_build.build()
     pa.load_library()
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(max(1, args.steps)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "copies": max(1, args.steps)}))
+        return
 
     configs = {}
     headline_w, headline = measure(args.config, args.steps, args.warmup)

@@ -18,6 +18,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -31,10 +32,19 @@ struct pa_event_ring {
   int used = 0;
 };
 
+// Launch-planner knobs; defaults can be overridden for tuning sweeps with
+// PA_DECODE_WG_PER_CU (1..64) and PA_DECODE_MIN_SEG (128..2^20 keys, rounded
+// to a multiple of 128), read when a handle is created.
+struct pa_tunables {
+  int decode_wg_per_cu;
+  int decode_min_seg;
+};
+
 struct pa_handle {
   pa_config cfg;
   int device;
   int cus;
+  pa_tunables tun;
   bool profile;
   pa_event_ring ring[PA_KERNEL_KINDS];
   int64_t launches[PA_KERNEL_KINDS];
@@ -59,8 +69,10 @@ constexpr int kMaxCus = 256;
 constexpr int kDecodeTile = 32;
 constexpr int kDecodeWaves = 4;
 constexpr int kSegQuantum = kDecodeTile * kDecodeWaves;  // keys per workgroup step
-constexpr int kMinSeg = 256;
-constexpr int kWgPerCu = 8;
+constexpr int kMinSegDefault = 256;
+constexpr int kMinSegFloor = 128;
+constexpr int kWgPerCuDefault = 32;
+constexpr int kWgPerCuMax = 64;
 constexpr int kBlockM = 128;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
@@ -91,8 +103,8 @@ pa_status check_config(const pa_config* c) {
     return fail(PA_ERR_UNSUPPORTED, "query heads per kv head must be 1, 2, 4, 8 or 16 (got %d)", G);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
-  if (c->block_size <= 0 || c->block_size % 16 != 0)
-    return fail(PA_ERR_UNSUPPORTED, "block_size must be a positive multiple of 16 (got %d)",
+  if (c->block_size < 16 || (c->block_size & (c->block_size - 1)) != 0 || c->block_size > (1 << 20))
+    return fail(PA_ERR_UNSUPPORTED, "block_size must be a power of two >= 16 (got %d)",
                 c->block_size);
   if (c->kv_dtype != PA_DTYPE_BF16 && c->kv_dtype != PA_DTYPE_FP8_E4M3)
     return fail(PA_ERR_UNSUPPORTED, "kv_dtype must be bf16 or fp8 e4m3 (got %d)", c->kv_dtype);
@@ -105,7 +117,21 @@ pa_status check_config(const pa_config* c) {
   return PA_OK;
 }
 
-void make_plan(const pa_config& c, int cus, int64_t T, int64_t S, int64_t MB, pa_plan_info* p) {
+pa_tunables tunables_from_env() {
+  pa_tunables t{kWgPerCuDefault, kMinSegDefault};
+  if (const char* e = std::getenv("PA_DECODE_WG_PER_CU")) {
+    const int v = std::atoi(e);
+    if (v >= 1) t.decode_wg_per_cu = std::min(v, kWgPerCuMax);
+  }
+  if (const char* e = std::getenv("PA_DECODE_MIN_SEG")) {
+    const long v = std::atol(e);
+    if (v >= kMinSegFloor) t.decode_min_seg = (int)(std::min(v, 1L << 20) / 128 * 128);
+  }
+  return t;
+}
+
+void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S,
+               int64_t MB, pa_plan_info* p) {
   std::memset(p, 0, sizeof *p);
   cus = std::min(std::max(cus, 1), kMaxCus);
   const int G = c.num_q_heads / c.num_kv_heads;
@@ -119,9 +145,9 @@ void make_plan(const pa_config& c, int cus, int64_t T, int64_t S, int64_t MB, pa
   if (S >= 1 && T >= 1 && max_len >= 1) {
     p->decode_launch = 1;
     const int64_t units = S * c.num_kv_heads;
-    const int64_t want = cdiv((int64_t)kWgPerCu * cus, units);
+    const int64_t want = cdiv((int64_t)tun.decode_wg_per_cu * cus, units);
     int64_t seg = cdiv(cdiv(max_len, want), kSegQuantum) * kSegQuantum;
-    seg = std::max<int64_t>(seg, kMinSeg);
+    seg = std::max<int64_t>(seg, tun.decode_min_seg);
     const int64_t splits = cdiv(max_len, seg);
     p->segment_len = (int32_t)seg;
     p->max_splits = (int32_t)splits;
@@ -130,8 +156,8 @@ void make_plan(const pa_config& c, int cus, int64_t T, int64_t S, int64_t MB, pa
     p->decode_grid[2] = c.num_kv_heads;
     if (splits > 1) {
       p->merge_launch = 1;
-      p->merge_grid[0] = S;
-      p->merge_grid[1] = c.num_kv_heads;
+      p->merge_grid[0] = c.num_q_heads;
+      p->merge_grid[1] = S;
       p->merge_grid[2] = 1;
       const uint64_t rows = (uint64_t)S * splits * c.num_q_heads;
       ws += align256(rows * c.head_dim * 4) + align256(rows * 2 * 4);
@@ -303,11 +329,11 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   uint64_t best = kHeader;
   const int64_t max_len = max_blocks_per_seq * cfg->block_size;
   if (max_seqs >= 1 && max_len >= 1) {
-    // splits(S) <= min(ceil(max_len / kMinSeg), ceil(kWgPerCu * kMaxCus / (S * Hkv))); the
-    // product S * splits(S) is bounded by min(S * ceil(max_len / kMinSeg),
-    // kWgPerCu * kMaxCus / Hkv + S).
-    const int64_t by_len = max_seqs * cdiv(max_len, kMinSeg);
-    const int64_t by_target = (int64_t)kWgPerCu * kMaxCus / cfg->num_kv_heads + max_seqs;
+    // splits(S) <= min(ceil(max_len / min_seg), ceil(wg_per_cu * cus / (S * Hkv))); the
+    // product S * splits(S) is bounded by min(S * ceil(max_len / min_seg),
+    // wg_per_cu * cus / Hkv + S), taken at the extreme knob values.
+    const int64_t by_len = max_seqs * cdiv(max_len, kMinSegFloor);
+    const int64_t by_target = (int64_t)kWgPerCuMax * kMaxCus / cfg->num_kv_heads + max_seqs;
     const uint64_t rows = (uint64_t)std::min(by_len, by_target) * cfg->num_q_heads;
     best += align256(rows * cfg->head_dim * 4) + align256(rows * 2 * 4);
   }
@@ -323,7 +349,7 @@ pa_status pa_plan(const pa_handle* h, const pa_config* cfg, int32_t num_cus, int
   if (num_tokens < 0 || num_seqs < 0 || max_blocks_per_seq < 0)
     return fail(PA_ERR_INVALID_ARG, "negative size");
   int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
-  make_plan(*c, cus, num_tokens, num_seqs, max_blocks_per_seq, out);
+  make_plan(*c, h ? h->tun : tunables_from_env(), cus, num_tokens, num_seqs, max_blocks_per_seq, out);
   return PA_OK;
 }
 
@@ -340,6 +366,7 @@ pa_status pa_create(const pa_config* cfg, pa_handle** out) {
   h->cfg = *cfg;
   h->device = dev;
   h->cus = cus > 0 ? cus : kMaxCus;
+  h->tun = tunables_from_env();
   h->profile = (cfg->flags & PA_FLAG_PROFILE) != 0;
   for (int k = 0; k < PA_KERNEL_KINDS; ++k) {
     h->launches[k] = 0;
@@ -398,7 +425,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   TRY(check_batch(c, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, &sh));
   if (!(scale > 0.f) || !(scale < 1e30f)) return fail(PA_ERR_INVALID_ARG, "scale must be positive and finite");
   pa_plan_info p;
-  make_plan(c, h->cus, sh.T, sh.S, sh.MB, &p);
+  make_plan(c, h->tun, h->cus, sh.T, sh.S, sh.MB, &p);
   if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
     return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
                 (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
@@ -447,6 +474,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   a.num_tokens = (int32_t)sh.T;
   a.num_blocks = (int32_t)std::min<int64_t>(sh.NB, INT32_MAX);
   a.block_size = c.block_size;
+  a.bs_log2 = __builtin_ctz(c.block_size);
   a.num_q_heads = c.num_q_heads;
   a.num_kv_heads = c.num_kv_heads;
   a.group = c.num_q_heads / c.num_kv_heads;
@@ -529,6 +557,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   g.num_seqs = (int32_t)S;
   g.num_blocks = (int32_t)std::min<int64_t>(NB, INT32_MAX);
   g.block_size = c.block_size;
+  g.bs_log2 = __builtin_ctz(c.block_size);
   g.num_kv_heads = c.num_kv_heads;
   g.row_bytes = c.head_dim * eb;
   hipError_t e = pa::launch_gather(g, reinterpret_cast<hipStream_t>(stream));

@@ -26,6 +26,7 @@ struct BatchArgs {
   uint8_t* out;
   int64_t o_tok, o_head;        // out strides (bytes)
   int32_t num_seqs, num_tokens, num_blocks, block_size;
+  int32_t bs_log2;              // block_size = 1 << bs_log2
   int32_t num_q_heads, num_kv_heads, group;  // group = Hq / Hkv
   float sl2;                    // softmax scale * log2(e) * k_scale
   float v_scale;
@@ -55,6 +56,7 @@ struct GatherArgs {
   uint8_t* vd;
   int64_t d_seq, d_tok, d_head;  // dense output strides (bytes)
   int32_t num_seqs, num_blocks, block_size, num_kv_heads;
+  int32_t bs_log2;
   int32_t row_bytes;             // bytes of one head's row (head_dim * elem)
 };
 

@@ -23,8 +23,8 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   const int L = min(a.seq_lens[s], a.mb * a.block_size);
   if (key >= L) return;
   const int32_t* bt_row = a.bt + (int64_t)s * a.bt_row;
-  const int pg = page_of(bt_row, key, a.block_size, a.num_blocks);
-  const int slot = key % a.block_size;
+  const int pg = page_of(bt_row, key, a.bs_log2, a.num_blocks);
+  const int slot = key & (a.block_size - 1);
   for (int c = lane; c * 16 < a.row_bytes; c += 64) {
     const u32x4 kw = ld16(a.k + (int64_t)pg * a.kg.blk + (int64_t)slot * a.kg.slot +
                           (int64_t)g * a.kg.head + 16 * c);

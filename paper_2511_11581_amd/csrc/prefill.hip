@@ -116,7 +116,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
   const int Hkv = a.num_kv_heads;
   const int g = blockIdx.x % Hkv;
   const int wi = blockIdx.x / Hkv;
-  const int G = a.group, BQ = pp.block_q, bs = a.block_size;
+  const int G = a.group, BQ = pp.block_q, bsl = a.bs_log2, bsm = a.block_size - 1;
 
   int seq, qb;
   if (!find_work(a.qsl, a.num_seqs, BQ, wi, seq, qb)) return;
@@ -156,55 +156,67 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
   const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
   const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
 
-  // ---- tile loader: global -> registers
+  // ---- tile loader: block-table lookups one tile ahead of the K/V loads,
+  //      K/V rows into registers one tile ahead of their use.  Loads are
+  //      unconditional from clamped (in-range) positions; rows past kv_len are
+  //      zeroed when written to LDS.
+  int pg_k[KLD], pg_v;
+  auto load_pages = [&](int tile, int (&pk)[KLD], int& pv) {
+    const int tb = tile * kTileN;
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      const int p = min(tb + (tid + kThreads * i) / CH, kv_len - 1);
+      pk[i] = page_of(bt_row, p, bsl, a.num_blocks);
+    }
+    pv = page_of(bt_row, min(tb + 4 * ((tid % VTASKS) & 15), kv_len - 1), bsl, a.num_blocks);
+  };
   u32x4 kreg[KLD];
   u32x4 vreg[4];
-  auto load_tile = [&](int tile) {
+  auto load_tile = [&](int tile, const int (&pk)[KLD], int pv) {
+    const int tb = tile * kTileN;
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      const int flat = tid + kThreads * i;
+      const int c = flat % CH;
+      const int p = min(tb + flat / CH, kv_len - 1);
+      kreg[i] = ld16(kbase + (int64_t)pk[i] * a.kg.blk + (int64_t)(p & bsm) * a.kg.slot + 16 * c);
+    }
+    {
+      const int vt = tid % VTASKS;
+      const int m = vt & 15, c = vt >> 4;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int p = min(tb + 4 * m + r, kv_len - 1);
+        vreg[r] = ld16(vbase + (int64_t)pv * a.vg.blk + (int64_t)(p & bsm) * a.vg.slot + 16 * c);
+      }
+    }
+  };
+  // ---- registers -> LDS (K natural bf16 rows, V transposed bf16)
+  auto store_tile = [&](int tile) {
     const int tb = tile * kTileN;
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
       const int flat = tid + kThreads * i;
       const int c = flat % CH, key = flat / CH;
-      const int p = tb + key;
-      u32x4 w = {0, 0, 0, 0};
-      if (p < kv_len) {
-        const int pg = page_of(bt_row, p, bs, a.num_blocks);
-        w = ld16(kbase + (int64_t)pg * a.kg.blk + (int64_t)(p % bs) * a.kg.slot + 16 * c);
-      }
-      kreg[i] = w;
-    }
-    {
-      const int c = tid % CH, m = tid / CH;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int p = tb + 4 * m + r;
-        u32x4 w = {0, 0, 0, 0};
-        if (tid < VTASKS && p < kv_len) {
-          const int pg = page_of(bt_row, p, bs, a.num_blocks);
-          w = ld16(vbase + (int64_t)pg * a.vg.blk + (int64_t)(p % bs) * a.vg.slot + 16 * c);
-        }
-        vreg[r] = w;
-      }
-    }
-  };
-  // ---- registers -> LDS (K natural bf16 rows, V transposed bf16)
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int flat = tid + kThreads * i;
-      const int c = flat % CH, key = flat / CH;
+      const u32x4 kw = tb + key < kv_len ? kreg[i] : u32x4{0, 0, 0, 0};
       uint8_t* dst = ks + key * KROW + 2 * DPC * c;
       if constexpr (FP8) {
         bf16x8 lo, hi;
-        fp8x16_to_bf16(kreg[i], lo, hi);
+        fp8x16_to_bf16(kw, lo, hi);
         *(bf16x8*)dst = lo;
         *(bf16x8*)(dst + 16) = hi;
       } else {
-        *(u32x4*)dst = kreg[i];
+        *(u32x4*)dst = kw;
       }
     }
     if (tid < VTASKS) {
-      const int c = tid % CH, m = tid / CH;
+      // 16 consecutive threads share a chunk c and cover the 16 key groups,
+      // so each 8-byte transposing write of a 16-lane group fills one
+      // 128-byte V^T row segment without bank conflicts.
+      const int m = tid & 15, c = tid >> 4;
+      u32x4 v4[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v4[r] = tb + 4 * m + r < kv_len ? vreg[r] : u32x4{0, 0, 0, 0};
       // keys 4m..4m+3 -> V^T positions: bits 2 and 3 of the key swapped
       const int pb = 16 * (m >> 2) + 8 * (m & 1) + 4 * ((m >> 1) & 1);
       uint8_t* wp = vts + (c * DPC) * VROW + 2 * pb;
@@ -214,7 +226,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
         for (int r = 0; r < 4; ++r)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            u32x2 cv = fp8x4_to_bf16x4(vreg[r][q]);
+            u32x2 cv = fp8x4_to_bf16x4(v4[r][q]);
             w[r][2 * q] = cv[0];
             w[r][2 * q + 1] = cv[1];
           }
@@ -237,11 +249,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
           const int dw = e >> 1;
           uint32_t lo, hi;
           if (e & 1) {
-            lo = (vreg[0][dw] >> 16) | (vreg[1][dw] & 0xFFFF0000u);
-            hi = (vreg[2][dw] >> 16) | (vreg[3][dw] & 0xFFFF0000u);
+            lo = (v4[0][dw] >> 16) | (v4[1][dw] & 0xFFFF0000u);
+            hi = (v4[2][dw] >> 16) | (v4[3][dw] & 0xFFFF0000u);
           } else {
-            lo = (vreg[0][dw] & 0xFFFFu) | (vreg[1][dw] << 16);
-            hi = (vreg[2][dw] & 0xFFFFu) | (vreg[3][dw] << 16);
+            lo = (v4[0][dw] & 0xFFFFu) | (v4[1][dw] << 16);
+            hi = (v4[2][dw] & 0xFFFFu) | (v4[3][dw] << 16);
           }
           *(u32x2*)(wp + e * VROW) = u32x2{lo, hi};
         }
@@ -256,13 +268,19 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
 
-  load_tile(0);
-  store_tile();
+  load_pages(0, pg_k, pg_v);
+  load_tile(0, pg_k, pg_v);
+  if (ntiles > 1) load_pages(1, pg_k, pg_v);
+  store_tile(0);
   __syncthreads();
 
   for (int tile = 0; tile < ntiles; ++tile) {
     const int tb = tile * kTileN;
-    if (tile + 1 < ntiles) load_tile(tile + 1);
+    // Unconditional (clamped) prefetch keeps the waits exact: the store of
+    // tile + 1 waits only for its own loads, not the younger page lookups.
+    load_tile(min(tile + 1, ntiles - 1), pg_k, pg_v);
+    load_pages(min(tile + 2, ntiles - 1), pg_k, pg_v);
+    __builtin_amdgcn_sched_barrier(0);
 
     if (tb <= wave_pos_max) {
       // ---- S^T = K Q^T for 2 blocks of 32 keys
@@ -278,14 +296,18 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
           acc = mfma32(*(const bf16x8*)(kr + 32 * t), qt[t], acc);
         sacc[kb] = acc;
       }
-      // ---- online softmax; lane holds keys 32kb + 8(i/4) + 4hf + i%4 of its row
+      // ---- online softmax; lane holds keys 32kb + 8(i/4) + 4hf + i%4 of its row.
+      // The running max m_run is kept in scaled log2 units and only raised when
+      // some row's tile max exceeds it by more than 8; otherwise the tile is
+      // exponentiated against the stale max (weights stay below 2^8, and the
+      // final division uses the same reference, so the result is unchanged).
       const bool diag = tb + kTileN - 1 > blk_pos_min;
       float mx = kNegInf;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float x = sacc[kb][i] * a.sl2;
+          float x = sacc[kb][i];
           if (diag) {
             const int key = tb + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
             x = key <= pos ? x : kNegInf;
@@ -293,22 +315,25 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
           sacc[kb][i] = x;
           mx = fmaxf(mx, x);
         }
-      mx = xor32_max(mx);
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = fast_exp2(m_run - m_new);
+      mx = xor32_max(mx) * a.sl2;
+      if (__ballot(mx > m_run + 8.f)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+      }
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float pv = fast_exp2(sacc[kb][i] - m_new);
+          const float pv = fast_exp2(__builtin_fmaf(sacc[kb][i], a.sl2, -m_run));
           sacc[kb][i] = pv;
           psum += pv;
         }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+      l_run += psum;
       // ---- O^T += V^T P^T over 4 steps of 16 keys
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -326,7 +351,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     }
     __syncthreads();
     if (tile + 1 < ntiles) {
-      store_tile();
+      store_tile(tile + 1);
       __syncthreads();
     }
   }
