@@ -38,6 +38,7 @@ struct pa_event_ring {
 struct pa_tunables {
   int decode_wg_per_cu;
   int decode_min_seg;
+  int decode_head_major;   // PA_DECODE_HEAD_MAJOR: kv head fastest in the decode grid
 };
 
 struct pa_handle {
@@ -118,7 +119,8 @@ pa_status check_config(const pa_config* c) {
 }
 
 pa_tunables tunables_from_env() {
-  pa_tunables t{kWgPerCuDefault, kMinSegDefault};
+  pa_tunables t{kWgPerCuDefault, kMinSegDefault, 1};
+  if (const char* e = std::getenv("PA_DECODE_HEAD_MAJOR")) t.decode_head_major = std::min(std::max(std::atoi(e), 0), 2);
   if (const char* e = std::getenv("PA_DECODE_WG_PER_CU")) {
     const int v = std::atoi(e);
     if (v >= 1) t.decode_wg_per_cu = std::min(v, kWgPerCuMax);
@@ -485,6 +487,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
     pa::DecodePlan dp;
     dp.seg_len = p.segment_len;
     dp.max_splits = p.max_splits;
+    dp.head_major = h->tun.decode_head_major;
     const uint64_t rows = (uint64_t)sh.S * p.max_splits * c.num_q_heads;
     dp.part_o = reinterpret_cast<float*>(ws + kHeader);
     dp.part_ml = reinterpret_cast<float*>(ws + kHeader + align256(rows * c.head_dim * 4));

@@ -2,7 +2,7 @@
 // (arxiv 2511.11581, Sec. 4.4 GQA packing and Sec. 4.5 parallel tiled
 // softmax; Eq. 1-2 for what is computed).
 //
-// One workgroup = (segment k, sequence s, kv head g), 4 waves.  Only
+// One workgroup = (kv head g, segment k, sequence s), 4 waves.  Only
 // sequences whose query length is 1 are handled here.  All G = Hq/Hkv query
 // heads of kv head g are packed into the columns of one 16-wide MFMA tile,
 // so each K/V row of the segment is read from HBM exactly once.  The segment
@@ -12,14 +12,18 @@
 // segment writes bf16 output directly; otherwise the segment stores its
 // unnormalised partials for the log-sum-exp merge kernel.
 //
-// Per tile and wave:
-//   S^T[16 keys x 16 heads] = K Q^T  (v_mfma_f32_16x16x32_bf16, 2 key blocks)
-//   online softmax in the log2 domain (one lane = one head column)
-//   O^T[d x heads] += V^T P^T         (V transposed through LDS)
-// K is loaded straight into MFMA A-operand registers with 16-byte loads:
-// lane (q4 = l/16, c16 = l%16) reads key c16 of a 16-key block, 16 bytes at
-// byte offset 64*i + 16*q4 of the row.  The d-permutation this implies is
-// applied identically to Q, so the dot products are unchanged.
+// Memory path per wave and tile: K and V rows are read with whole-row
+// coalesced loads (16 lanes per row, 4 rows per instruction: lane l reads
+// key 4r + (l & 3), bytes (l >> 2) * LB of the row, r = 0..7), the next
+// tile's loads in flight while the current one is consumed.  Through the
+// wave's private LDS area they are rearranged for the matrix cores:
+//   K  -> natural bf16 rows, read back as MFMA A operands (key rows),
+//   V  -> V^T rows (one row per d), 16-byte transposing writes,
+//   S^T[16 keys x 16 heads] = K Q^T, P = online softmax (log2 domain),
+//   O^T[d x heads] += V^T P^T      (v_mfma_f32_16x16x32_bf16).
+// MFMA row m of key block kb holds key 16kb + (m >> 2) + 4(m & 3), so the 8
+// keys of one lane's P^T / V^T operand slots are exactly the 8 keys that one
+// loading lane holds (all keys of the tile congruent to l & 3 mod 4).
 #include "common.hpp"
 #include "kernels.h"
 
@@ -30,43 +34,70 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kTile = 32;      // keys per wave iteration
 
-// Keys of a 32-key tile sit in a V^T row so that the 8 keys feeding one
-// lane's MFMA A-operand slots (keys 16j + 4*q4 + r, j = 0..1, r = 0..3) are
-// contiguous: key kk is at position 8*((kk >> 2) & 3) + 4*(kk >> 4) + (kk & 3).
-//
-// Byte offset of 16-byte column group cg (0..3) of V^T row r in a wave's LDS
-// area.  Rows are 64 bytes, 64 bytes of padding follow every 2^PS rows and the
-// column group is XOR-swizzled with bits 2..3 of the row.  With PS = log2 of
-// the d rows one lane writes (8 for bf16, 16 for fp8) both the transposing
-// 8-byte writes (16-lane groups) and the 16-byte operand reads (32-lane
-// groups) hit distinct LDS banks.
-template <int PS>
+// V^T row r (a d index), 16-byte column group cg (8 keys): rows are 64 bytes,
+// 64 bytes of padding follow every 2^PSH rows (PSH = log2 of the d values a
+// lane writes per row) and the column group is XOR-swizzled with bits 2..3
+// of the row, so the transposing writes (8- and 16-lane groups) and the
+// operand reads (32-lane groups) hit distinct LDS banks.
+template <int PSH>
 __device__ __forceinline__ int vt_off(int r, int cg) {
-  return 16 * (4 * r + 4 * (r >> PS) + (cg ^ ((r >> 2) & 3)));
+  return 16 * (4 * r + 4 * (r >> PSH) + (cg ^ ((r >> 2) & 3)));
 }
-template <int D, int PS>
-constexpr int vt_bytes() { return 16 * (4 * D + 4 * (D >> PS)); }
+
+template <int LB> struct LoadT;
+template <> struct LoadT<16> { typedef u32x4 T; };
+template <> struct LoadT<8> { typedef u32x2 T; };
+template <> struct LoadT<4> { typedef uint32_t T; };
+
+template <int LB>
+__device__ __forceinline__ typename LoadT<LB>::T ldn(const uint8_t* p) {
+  return __builtin_nontemporal_load((const typename LoadT<LB>::T*)p);
+}
+template <int LB>
+__device__ __forceinline__ uint32_t dw(const typename LoadT<LB>::T& v, int i) {
+  if constexpr (LB == 4) return v;
+  else return v[i];
+}
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan p) {
   constexpr int EB = FP8 ? 1 : 2;          // bytes per cached element
+  constexpr int LB = D * EB / 16;          // bytes one lane loads per row
+  constexpr int DPL = LB / EB;             // d values one lane loads per row
+  constexpr int PSH = DPL == 8 ? 3 : 2;    // log2(DPL)
+  constexpr int NW = DPL / 2;              // bf16 dwords per lane per row
   constexpr int NSTEP = D / 32;            // MFMA k-steps over d
-  constexpr int NKLD = D * EB / 64;        // 16-byte K loads per lane per key block
   constexpr int NDB = D / 16;              // 16-row d blocks of O^T
-  constexpr int CH = D * EB / 16;          // 16-byte chunks per cached row
-  constexpr int TASKS = 8 * CH;            // (4-key group, chunk) pairs per tile
-  constexpr int NT = (TASKS + 63) / 64;    // tasks per lane
-  constexpr int DPC = 16 / EB;             // d values per chunk
+  constexpr int KRB = 2 * D + 32;          // LDS bytes per K row (bf16 + pad)
+  constexpr int KT = kTile * KRB;          // K tile bytes
+  constexpr int VT = 16 * (4 * D + 4 * (D >> PSH));  // V^T tile bytes
+  constexpr int WB = KT + VT;              // LDS bytes per wave
   constexpr int RED = D + 2;               // floats per (wave, head) in the merge area
-  constexpr int PS = FP8 ? 4 : 3;          // log2(DPC)
-  constexpr int VT = vt_bytes<D, PS>();    // LDS bytes per wave
-  static_assert(kWaves * 16 * RED * 4 <= kWaves * VT, "merge area must fit");
+  typedef typename LoadT<LB>::T LT;
+  static_assert(DPL == 8 || DPL == 4, "head_dim 64 or 128");
+  static_assert(kWaves * 16 * RED * 4 <= kWaves * WB, "merge area must fit");
 
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves * VT];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves * WB];
 
   const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
-  const int q4 = lane >> 4, c16 = lane & 15;
-  const int g = blockIdx.x, ks = blockIdx.y, s = blockIdx.z;
+  const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
+  const int lq = lane & 3, lc = lane >> 2;     // loading coordinates
+  int g, ks, s;
+  if (p.head_major == 2) {
+    // XCD-grouped: workgroups are dealt round-robin to the 8 XCDs; the j-th
+    // workgroup of XCD x handles head j % Hkv of unit (j / Hkv) * 8 + x, so
+    // the Hkv heads of one (sequence, segment) run together on one XCD.
+    const int i = blockIdx.x, x = i & 7, j = i >> 3;
+    const int u = (j / a.num_kv_heads) * 8 + x;
+    if (u >= a.num_seqs * p.max_splits) return;
+    g = j % a.num_kv_heads;
+    s = u / p.max_splits;
+    ks = u % p.max_splits;
+  } else {
+    g = p.head_major ? blockIdx.x : blockIdx.y;
+    ks = p.head_major ? blockIdx.y : blockIdx.x;
+    s = blockIdx.z;
+  }
 
   const int t0 = a.qsl[s];
   if (a.qsl[s + 1] - t0 != 1 || t0 < 0 || t0 >= a.num_tokens) return;
@@ -80,15 +111,15 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   const int32_t* bt_row = a.bt + (int64_t)s * a.bt_row;
   const int G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
 
-  // Q^T as MFMA B operands: column c16 = head g*G + c16 (zero if c16 >= G).
+  // Q^T as MFMA B operands: column c16 = head g*G + c16 (zero if c16 >= G),
+  // k-step st covers d = 32 st + 8 q4 + j.
   bf16x8 qt[NSTEP];
   {
     const bool hv = c16 < G;
     const uint8_t* qrow = a.q + (int64_t)t0 * a.q_tok + (int64_t)(g * G + (hv ? c16 : 0)) * a.q_head;
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) {
-      const int dbase = FP8 ? (64 * (st >> 1) + 16 * q4 + 8 * (st & 1)) : (32 * st + 8 * q4);
-      u32x4 w = hv ? ld16_cached(qrow + dbase * 2) : u32x4{0, 0, 0, 0};
+      u32x4 w = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
       qt[st] = __builtin_bit_cast(bf16x8, w);
     }
   }
@@ -97,9 +128,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   f32x4 o[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) o[db] = f32x4{0, 0, 0, 0};
-  uint8_t* vt = lds + wave * VT;
-  const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
-  const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
+  uint8_t* kl = lds + wave * WB;
+  uint8_t* vt = kl + KT;
+  const uint8_t* kbase = a.k + (int64_t)g * a.kg.head + lc * LB;
+  const uint8_t* vbase = a.v + (int64_t)g * a.vg.head + lc * LB;
 
   // This wave's tiles are wave, wave + 4, ...; it holds the physical block
   // of each of their 16-key blocks in a per-lane page cache (lane j: tile
@@ -112,8 +144,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
     cache = key < kend ? page_of(bt_row, key, bsl, a.num_blocks) : 0;
     cache_base = i0;
   };
-  // Issue the loads of the i-th tile of this wave into (kr, vr).
-  auto issue = [&](int i, u32x4 (&kr)[2][NKLD], u32x4 (&vr)[NT][4]) {
+  // Issue the loads of the i-th tile of this wave: lane holds keys 4r + lq.
+  auto issue = [&](int i, LT (&kr)[8], LT (&vr)[8]) {
     if (i - cache_base >= 32) refill(i);
     const int tb = kbeg + (wave + kWaves * i) * kTile;
     const int pg0 = __builtin_amdgcn_readlane(cache, 2 * (i - cache_base));
@@ -121,59 +153,64 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
     pg1 = (tb + 16 < kend) ? pg1 : pg0;
     const int sl0 = tb & bsm, sl1 = (tb + 16) & bsm;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const uint8_t* rp = kbase + (int64_t)(kb ? pg1 : pg0) * a.kg.blk +
-                          (int64_t)((kb ? sl1 : sl0) + c16) * a.kg.slot + 16 * q4;
-#pragma unroll
-      for (int j = 0; j < NKLD; ++j) kr[kb][j] = ld16(rp + 64 * j);
-    }
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int task = min(lane + 64 * t, TASKS - 1);
-      const int m = task & 7, c = task >> 3;
-      const int kb = m >> 2;
-      const uint8_t* rp = vbase + (int64_t)(kb ? pg1 : pg0) * a.vg.blk +
-                          (int64_t)((kb ? sl1 : sl0) + 4 * (m & 3)) * a.vg.slot + 16 * c;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vr[t][r] = ld16(rp + (int64_t)r * a.vg.slot);
+    for (int r = 0; r < 8; ++r) {
+      const int kb = r >> 2;
+      const int slot = (kb ? sl1 : sl0) + 4 * (r & 3) + lq;
+      const int64_t pg = kb ? pg1 : pg0;
+      kr[r] = ldn<LB>(kbase + pg * a.kg.blk + (int64_t)slot * a.kg.slot);
+      vr[r] = ldn<LB>(vbase + pg * a.vg.blk + (int64_t)slot * a.vg.slot);
     }
   };
-  // Attention update with the i-th tile of this wave held in (kr, vr).
-  auto consume = [&](int i, u32x4 (&kr)[2][NKLD], u32x4 (&vr)[NT][4]) {
+  // bf16 words of one loaded row chunk (DPL values of one key).
+  auto to_bf16 = [&](const LT& v, uint32_t (&w)[NW]) {
+    if constexpr (FP8) {
+#pragma unroll
+      for (int q = 0; q < LB / 4; ++q) {
+        const u32x2 cv = fp8x4_to_bf16x4(dw<LB>(v, q));
+        w[2 * q] = cv[0];
+        w[2 * q + 1] = cv[1];
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < NW; ++q) w[q] = dw<LB>(v, q);
+    }
+  };
+  // Attention update with the i-th tile of this wave.
+  auto consume = [&](int i, LT (&kr)[8], LT (&vr)[8]) {
     const int tb = kbeg + (wave + kWaves * i) * kTile;
-    // ---- S^T = K Q^T
+    // ---- K rows -> LDS (bf16, natural layout)
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      uint32_t w[NW];
+      to_bf16(kr[r], w);
+      uint8_t* dst = kl + (4 * r + lq) * KRB + lc * (2 * DPL);
+      if constexpr (NW == 4) *(u32x4*)dst = u32x4{w[0], w[1], w[2], w[3]};
+      else *(u32x2*)dst = u32x2{w[0], w[1]};
+    }
+    // ---- S^T = K Q^T; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
     f32x4 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x4 acc = {0, 0, 0, 0};
-      if constexpr (FP8) {
+      const uint8_t* kp = kl + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
 #pragma unroll
-        for (int j = 0; j < NKLD; ++j) {
-          bf16x8 lo, hi;
-          fp8x16_to_bf16(kr[kb][j], lo, hi);
-          acc = mfma16(lo, qt[2 * j], acc);
-          acc = mfma16(hi, qt[2 * j + 1], acc);
-        }
-      } else {
-#pragma unroll
-        for (int st = 0; st < NSTEP; ++st)
-          acc = mfma16(__builtin_bit_cast(bf16x8, kr[kb][st]), qt[st], acc);
-      }
+      for (int st = 0; st < NSTEP; ++st)
+        acc = mfma16(*(const bf16x8*)(kp + 64 * st), qt[st], acc);
       sacc[kb] = acc;
     }
-    // ---- online softmax (log2 domain); lane holds keys 16kb + 4q4 + r of head c16
+    // ---- online softmax (log2 domain); lane holds keys 16kb + q4 + 4r of head c16
     float x[2][4];
     float mx = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int key = tb + 16 * kb + 4 * q4 + r;
-        x[kb][r] = key < kend ? sacc[kb][r] * a.sl2 : kNegInf;
+        const int key = tb + 16 * kb + q4 + 4 * r;
+        x[kb][r] = key < kend ? sacc[kb][r] : kNegInf;
         mx = fmaxf(mx, x[kb][r]);
       }
     mx = xor16_max(mx);
-    mx = xor32_max(mx);
+    mx = xor32_max(mx) * a.sl2;
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
     float psum = 0.f;
@@ -181,7 +218,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        x[kb][r] = fast_exp2(x[kb][r] - m_new);
+        x[kb][r] = fast_exp2(__builtin_fmaf(x[kb][r], a.sl2, -m_new));
         psum += x[kb][r];
       }
     l_run = l_run * alpha + psum;
@@ -192,75 +229,45 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
                 pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
     const bf16x8 pt = __builtin_bit_cast(bf16x8, pw);
 
-    // ---- V -> V^T in this wave's LDS area (bf16), 8 bytes = 4 keys per d row;
-    //      rows of keys past the segment end are zeroed (their slots may hold NaN).
+    // ---- V -> V^T: this lane's 8 keys (4r + lq, r = 0..7) are the 8
+    //      consecutive positions of column group lq; keys past the segment end
+    //      are zeroed (their slots may hold NaN).
+    uint32_t vw[8][NW];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int task = lane + 64 * t;
-      if (task < TASKS) {
-        const int m = task & 7, c = task >> 3;
-        // keys 4m..4m+3 occupy 8 bytes (half m>>2 of column group m&3) of row DPC*c + e
-        const int cg = m & 3, half8 = 8 * (m >> 2);
-        u32x4 v4[4];
+    for (int r = 0; r < 8; ++r) {
+      to_bf16(vr[r], vw[r]);
+      if (tb + 4 * r + lq >= kend) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          v4[r] = (tb + 4 * m + r < kend) ? vr[t][r] : u32x4{0, 0, 0, 0};
-        if constexpr (FP8) {
-          uint32_t w[4][8];
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              u32x2 cv = fp8x4_to_bf16x4(v4[r][q]);
-              w[r][2 * q] = cv[0];
-              w[r][2 * q + 1] = cv[1];
-            }
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int dw = e >> 1;
-            uint32_t lo, hi;
-            if (e & 1) {
-              lo = (w[0][dw] >> 16) | (w[1][dw] & 0xFFFF0000u);
-              hi = (w[2][dw] >> 16) | (w[3][dw] & 0xFFFF0000u);
-            } else {
-              lo = (w[0][dw] & 0xFFFFu) | (w[1][dw] << 16);
-              hi = (w[2][dw] & 0xFFFFu) | (w[3][dw] << 16);
-            }
-            *(u32x2*)(vt + vt_off<PS>(DPC * c + e, cg) + half8) = u32x2{lo, hi};
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int dw = e >> 1;
-            uint32_t lo, hi;
-            if (e & 1) {
-              lo = (v4[0][dw] >> 16) | (v4[1][dw] & 0xFFFF0000u);
-              hi = (v4[2][dw] >> 16) | (v4[3][dw] & 0xFFFF0000u);
-            } else {
-              lo = (v4[0][dw] & 0xFFFFu) | (v4[1][dw] << 16);
-              hi = (v4[2][dw] & 0xFFFFu) | (v4[3][dw] << 16);
-            }
-            *(u32x2*)(vt + vt_off<PS>(DPC * c + e, cg) + half8) = u32x2{lo, hi};
-          }
-        }
+        for (int q = 0; q < NW; ++q) vw[r][q] = 0u;
       }
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) {
+      const int wi = e >> 1;
+      u32x4 col;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = vw[2 * j][wi], hi = vw[2 * j + 1][wi];
+        col[j] = (e & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = col;
     }
     // ---- O^T += V^T P^T
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const u32x4 va = *(const u32x4*)(vt + vt_off<PS>(16 * db + c16, q4));
+      const u32x4 va = *(const u32x4*)(vt + vt_off<PSH>(16 * db + c16, q4));
       o[db] = mfma16(__builtin_bit_cast(bf16x8, va), pt, o[db]);
     }
   };
 
   // Software pipeline: the loads of tile i+1 are in flight while tile i is
   // consumed (two register sets, loop unrolled by two).  The steady-state
-  // body issues unconditionally so that each wait covers only the older set.
-  u32x4 krA[2][NKLD], vrA[NT][4], krB[2][NKLD], vrB[NT][4];
-  int i = 0;
-  if (nt > 0) issue(0, krA, vrA);
+  // body issues unconditionally so that each wait covers only the older set;
   // sched_barrier keeps the compiler from hoisting the consumer's first
   // instructions above the new loads (which would force a full wait).
+  LT krA[8], vrA[8], krB[8], vrB[8];
+  int i = 0;
+  if (nt > 0) issue(0, krA, vrA);
   for (; i + 2 < nt; i += 2) {
     issue(i + 1, krB, vrB);
     __builtin_amdgcn_sched_barrier(0);
@@ -356,7 +363,12 @@ __global__ __launch_bounds__(D) void merge_kernel(BatchArgs a, DecodePlan p) {
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st) {
   // kv head fastest: the workgroups reading the same cache blocks run together
-  dim3 grid(a.num_kv_heads, p.max_splits, a.num_seqs), block(256);
+  dim3 grid(p.head_major ? a.num_kv_heads : p.max_splits,
+            p.head_major ? p.max_splits : a.num_kv_heads, a.num_seqs), block(256);
+  if (p.head_major == 2) {
+    const int64_t units = (int64_t)a.num_seqs * p.max_splits;
+    grid = dim3((unsigned)(((units + 7) / 8) * 8 * a.num_kv_heads), 1, 1);
+  }
   if (head_dim == 128) {
     if (fp8) decode_kernel<128, true><<<grid, block, 0, st>>>(a, p);
     else decode_kernel<128, false><<<grid, block, 0, st>>>(a, p);

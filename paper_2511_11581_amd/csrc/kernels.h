@@ -35,6 +35,7 @@ struct BatchArgs {
 struct DecodePlan {
   int32_t seg_len;     // keys per segment (multiple of 128)
   int32_t max_splits;  // segments per sequence at most
+  int32_t head_major;  // grid order: kv head fastest (1) or segment fastest (0)
   float* part_o;       // [num_seqs, max_splits, Hq, head_dim] unnormalised
   float* part_ml;      // [num_seqs, max_splits, Hq, 2] (max in log2 units, sum)
 };
