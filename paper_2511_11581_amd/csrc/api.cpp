@@ -244,6 +244,10 @@ pa_status check_batch(const pa_config& c, const pa_tensor* q, const pa_tensor* k
   if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
   if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences per call (got %lld)", (long long)S);
   if (MB * c.block_size > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
+  for (const pa_tensor* kv : {k, v})
+    if ((int64_t)c.block_size * kv->stride[1] * elem_bytes(kv->dtype) >= INT32_MAX ||
+        kv->stride[2] * elem_bytes(kv->dtype) >= INT32_MAX)
+      return fail(PA_ERR_UNSUPPORTED, "cache slot/head strides too large for 32-bit in-block offsets");
   TRY(check_aligned16(q, "q"));
   TRY(check_aligned16(k, "k_cache"));
   TRY(check_aligned16(v, "v_cache"));

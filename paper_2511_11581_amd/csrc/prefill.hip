@@ -108,8 +108,10 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
   constexpr int NDB = D / 32;                     // 32-row d blocks of O^T
   static_assert(KLD >= 1, "tile too small");
 
-  __shared__ __attribute__((aligned(16))) uint8_t ks[kTileN * KROW];
-  __shared__ __attribute__((aligned(16))) uint8_t vts[D * VROW];
+  // Two stages of (K tile, V^T tile): tile t lives in stage t & 1, so the
+  // next tile is written while the current one is read (one barrier a tile).
+  constexpr int KS_BYTES = kTileN * KROW, VT_BYTES = D * VROW;
+  __shared__ __attribute__((aligned(16))) uint8_t stage_mem[2 * (KS_BYTES + VT_BYTES)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hf = lane >> 5;
@@ -153,47 +155,57 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
       qt[t] = __builtin_bit_cast(bf16x8, ld16_cached(qrow + 2 * (16 * t + 8 * hf)));
   }
 
+  // ---- loader geometry.  Tile t covers keys [64t, 64t + 64).  K load i of
+  // this thread reads key kk_i = (tid + 256 i) / CH, 16-byte chunk tid % CH;
+  // all keys of one wave's K load fall in one 16-key block, so its block-table
+  // lookup is wave-uniform (scalar).  V: thread (m = vt & 15, c = vt >> 4)
+  // reads keys 4m..4m+3, chunk c (one lookup per thread).  Keys past kv_len
+  // read clamped block-table entries and are zeroed when written to LDS.
+  const int vtask = tid % VTASKS;
+  const int vm = vtask & 15, vc = vtask >> 4;
+  // (Offsets inside one block fit in 32 bits: the host checks
+  // block_size * slot stride < 2^31.)
+  int koff[KLD];
+  int kkw[KLD];
+#pragma unroll
+  for (int i = 0; i < KLD; ++i) {
+    const int kk = (tid + kThreads * i) / CH;
+    kkw[i] = uniform(kk);
+    koff[i] = (kk & bsm) * (int)a.kg.slot + 16 * ((tid + kThreads * i) % CH);
+  }
+  const int voff = ((4 * vm) & bsm) * (int)a.vg.slot + 16 * vc;
   const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
   const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
+  const int last_blk = (kv_len - 1) >> bsl;
 
-  // ---- tile loader: block-table lookups one tile ahead of the K/V loads,
-  //      K/V rows into registers one tile ahead of their use.  Loads are
-  //      unconditional from clamped (in-range) positions; rows past kv_len are
-  //      zeroed when written to LDS.
   int pg_k[KLD], pg_v;
   auto load_pages = [&](int tile, int (&pk)[KLD], int& pv) {
     const int tb = tile * kTileN;
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
-      const int p = min(tb + (tid + kThreads * i) / CH, kv_len - 1);
-      pk[i] = page_of(bt_row, p, bsl, a.num_blocks);
+      const int bi = min((tb + kkw[i]) >> bsl, last_blk);
+      pk[i] = uniform(page_of(bt_row, bi << bsl, bsl, a.num_blocks));
     }
-    pv = page_of(bt_row, min(tb + 4 * ((tid % VTASKS) & 15), kv_len - 1), bsl, a.num_blocks);
+    pv = page_of(bt_row, min((tb + 4 * vm) >> bsl, last_blk) << bsl, bsl, a.num_blocks);
   };
   u32x4 kreg[KLD];
   u32x4 vreg[4];
   auto load_tile = [&](int tile, const int (&pk)[KLD], int pv) {
-    const int tb = tile * kTileN;
+    const int64_t toff = (int64_t)((tile * kTileN) & bsm);   // slot of the tile start when bs > 64
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
-      const int flat = tid + kThreads * i;
-      const int c = flat % CH;
-      const int p = min(tb + flat / CH, kv_len - 1);
-      kreg[i] = ld16(kbase + (int64_t)pk[i] * a.kg.blk + (int64_t)(p & bsm) * a.kg.slot + 16 * c);
+      const uint8_t* base = kbase + (int64_t)pk[i] * a.kg.blk + toff * a.kg.slot;
+      kreg[i] = ld16_cached(base + koff[i]);   // K/V are reused by other Q-blocks
     }
-    {
-      const int vt = tid % VTASKS;
-      const int m = vt & 15, c = vt >> 4;
+    const uint8_t* vb = vbase + (int64_t)pv * a.vg.blk + toff * a.vg.slot + voff;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int p = min(tb + 4 * m + r, kv_len - 1);
-        vreg[r] = ld16(vbase + (int64_t)pv * a.vg.blk + (int64_t)(p & bsm) * a.vg.slot + 16 * c);
-      }
-    }
+    for (int r = 0; r < 4; ++r) vreg[r] = ld16_cached(vb + r * (int)a.vg.slot);
   };
   // ---- registers -> LDS (K natural bf16 rows, V transposed bf16)
   auto store_tile = [&](int tile) {
     const int tb = tile * kTileN;
+    uint8_t* ks = stage_mem + (tile & 1) * (KS_BYTES + VT_BYTES);
+    uint8_t* vts = ks + KS_BYTES;
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
       const int flat = tid + kThreads * i;
@@ -213,13 +225,12 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
       // 16 consecutive threads share a chunk c and cover the 16 key groups,
       // so each 8-byte transposing write of a 16-lane group fills one
       // 128-byte V^T row segment without bank conflicts.
-      const int m = tid & 15, c = tid >> 4;
       u32x4 v4[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v4[r] = tb + 4 * m + r < kv_len ? vreg[r] : u32x4{0, 0, 0, 0};
+      for (int r = 0; r < 4; ++r) v4[r] = tb + 4 * vm + r < kv_len ? vreg[r] : u32x4{0, 0, 0, 0};
       // keys 4m..4m+3 -> V^T positions: bits 2 and 3 of the key swapped
-      const int pb = 16 * (m >> 2) + 8 * (m & 1) + 4 * ((m >> 1) & 1);
-      uint8_t* wp = vts + (c * DPC) * VROW + 2 * pb;
+      const int pb = 16 * (vm >> 2) + 8 * (vm & 1) + 4 * ((vm >> 1) & 1);
+      uint8_t* wp = vts + (vc * DPC) * VROW + 2 * pb;
       if constexpr (FP8) {
         uint32_t w[4][8];
 #pragma unroll
@@ -268,12 +279,94 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
 
+  // One tile of attention from LDS.  MASKED: the tile crosses the diagonal
+  // of some row of the block (keys above a row's position are dropped).
+  // The running max m_run is kept in scaled log2 units and only raised when
+  // some row's tile max exceeds it by more than 8; otherwise the tile is
+  // exponentiated against the stale max (weights stay below 2^8, and the
+  // final division uses the same reference, so the result is unchanged).
+  auto attend = [&](int tile, bool masked) {
+    const int tb = tile * kTileN;
+    const uint8_t* ks = stage_mem + (tile & 1) * (KS_BYTES + VT_BYTES);
+    const uint8_t* vts = ks + KS_BYTES;
+    // ---- S^T = K Q^T for 2 blocks of 32 keys; all K operands of a block are
+    //      read before its MFMA chain so the LDS latency is paid once.
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 kop[NT];
+      const uint8_t* kr = ks + (32 * kb + n) * KROW + 16 * hf;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) kop[t] = *(const bf16x8*)(kr + 32 * t);
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 acc;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc = mfma32(kop[t], qt[t], acc);
+      sacc[kb] = acc;
+    }
+    if (masked) {
+      // key (tb + 32kb + 8(i/4) + 4hf + i%4) is dropped when it exceeds pos
+      const int lim = pos - tb - 4 * hf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          sacc[kb][i] = (32 * kb + 8 * (i >> 2) + (i & 3)) <= lim ? sacc[kb][i] : kNegInf;
+    }
+    float mx = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
+    mx = xor32_max(mx) * a.sl2;
+    if (__ballot(mx > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float pv = fast_exp2(__builtin_fmaf(sacc[kb][i], a.sl2, -m_run));
+        sacc[kb][i] = pv;
+        psum += pv;
+      }
+    l_run += psum;
+    // ---- O^T += V^T P^T over 4 steps of 16 keys
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const f32x16& sp = sacc[u >> 1];
+      const int r0 = 8 * (u & 1);
+      u32x4 pw = {pack_bf16(sp[r0 + 0], sp[r0 + 1]), pack_bf16(sp[r0 + 2], sp[r0 + 3]),
+                  pack_bf16(sp[r0 + 4], sp[r0 + 5]), pack_bf16(sp[r0 + 6], sp[r0 + 7])};
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+      bf16x8 vop[NDB];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        vop[db] = *(const bf16x8*)(vts + (32 * db + n) * VROW + 2 * (16 * u + 8 * hf));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] = mfma32(vop[db], pb, o[db]);
+    }
+  };
+
   load_pages(0, pg_k, pg_v);
   load_tile(0, pg_k, pg_v);
-  if (ntiles > 1) load_pages(1, pg_k, pg_v);
+  load_pages(min(1, ntiles - 1), pg_k, pg_v);
   store_tile(0);
   __syncthreads();
 
+  // Tiles below every row's diagonal need no mask.  Per iteration: issue
+  // the loads of tile + 1, attend to tile (stage tile & 1), write tile + 1
+  // into the other stage, one barrier.
+  const int nfull = min(ntiles, (blk_pos_min + 1) / kTileN);
   for (int tile = 0; tile < ntiles; ++tile) {
     const int tb = tile * kTileN;
     // Unconditional (clamped) prefetch keeps the waits exact: the store of
@@ -281,79 +374,9 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     load_tile(min(tile + 1, ntiles - 1), pg_k, pg_v);
     load_pages(min(tile + 2, ntiles - 1), pg_k, pg_v);
     __builtin_amdgcn_sched_barrier(0);
-
-    if (tb <= wave_pos_max) {
-      // ---- S^T = K Q^T for 2 blocks of 32 keys
-      f32x16 sacc[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 acc;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-        const uint8_t* kr = ks + (32 * kb + n) * KROW + 16 * hf;
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          acc = mfma32(*(const bf16x8*)(kr + 32 * t), qt[t], acc);
-        sacc[kb] = acc;
-      }
-      // ---- online softmax; lane holds keys 32kb + 8(i/4) + 4hf + i%4 of its row.
-      // The running max m_run is kept in scaled log2 units and only raised when
-      // some row's tile max exceeds it by more than 8; otherwise the tile is
-      // exponentiated against the stale max (weights stay below 2^8, and the
-      // final division uses the same reference, so the result is unchanged).
-      const bool diag = tb + kTileN - 1 > blk_pos_min;
-      float mx = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float x = sacc[kb][i];
-          if (diag) {
-            const int key = tb + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
-            x = key <= pos ? x : kNegInf;
-          }
-          sacc[kb][i] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = xor32_max(mx) * a.sl2;
-      if (__ballot(mx > m_run + 8.f)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-      }
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float pv = fast_exp2(__builtin_fmaf(sacc[kb][i], a.sl2, -m_run));
-          sacc[kb][i] = pv;
-          psum += pv;
-        }
-      l_run += psum;
-      // ---- O^T += V^T P^T over 4 steps of 16 keys
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const f32x16& sp = sacc[u >> 1];
-        const int r0 = 8 * (u & 1);
-        u32x4 pw = {pack_bf16(sp[r0 + 0], sp[r0 + 1]), pack_bf16(sp[r0 + 2], sp[r0 + 3]),
-                    pack_bf16(sp[r0 + 4], sp[r0 + 5]), pack_bf16(sp[r0 + 6], sp[r0 + 7])};
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const bf16x8 va = *(const bf16x8*)(vts + (32 * db + n) * VROW + 2 * (16 * u + 8 * hf));
-          o[db] = mfma32(va, pb, o[db]);
-        }
-      }
-    }
+    if (tb <= wave_pos_max) attend(tile, uniform(tile >= nfull) != 0);
+    if (tile + 1 < ntiles) store_tile(tile + 1);
     __syncthreads();
-    if (tile + 1 < ntiles) {
-      store_tile(tile + 1);
-      __syncthreads();
-    }
   }
 
   // ---- finalise: out = O / l, bf16
