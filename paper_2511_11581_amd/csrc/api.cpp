@@ -118,6 +118,14 @@ pa_status check_config(const pa_config* c) {
   return PA_OK;
 }
 
+// Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) + (#sequences with q_i >= 2).
+int64_t prefill_items(int64_t T, int64_t S, int64_t bq) { return cdiv(T, bq) + std::min<int64_t>(S, T / 2); }
+
+// Prefill work-list area: seq_start [S + 1], list_seq [items], list_qb [items], count.
+uint64_t prefill_ws_bytes(int64_t S, int64_t items) {
+  return align256((uint64_t)(S + 1) * 4) + 2 * align256((uint64_t)items * 4) + 256;
+}
+
 pa_tunables tunables_from_env() {
   pa_tunables t{kWgPerCuDefault, kMinSegDefault, 1};
   if (const char* e = std::getenv("PA_DECODE_HEAD_MAJOR")) t.decode_head_major = std::min(std::max(std::atoi(e), 0), 2);
@@ -167,10 +175,11 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   }
   if (S >= 1 && T >= 2 && max_len >= 2) {
     p->prefill_launch = 1;
-    const int64_t items = cdiv(T, p->block_q) + std::min<int64_t>(S, T / 2);
+    const int64_t items = prefill_items(T, S, p->block_q);
     p->prefill_grid[0] = items * c.num_kv_heads;
     p->prefill_grid[1] = 1;
     p->prefill_grid[2] = 1;
+    ws += prefill_ws_bytes(S, items);
   }
   p->workspace_bytes = ws;
 }
@@ -343,6 +352,10 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
     const uint64_t rows = (uint64_t)std::min(by_len, by_target) * cfg->num_q_heads;
     best += align256(rows * cfg->head_dim * 4) + align256(rows * 2 * 4);
   }
+  if (max_seqs >= 1 && max_tokens >= 2) {
+    const int64_t bq = kBlockM / (cfg->num_q_heads / cfg->num_kv_heads);
+    best += prefill_ws_bytes(max_seqs, prefill_items(max_tokens, max_seqs, bq));
+  }
   *bytes = best;
   return PA_OK;
 }
@@ -508,7 +521,17 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
     pa::PrefillPlan pp;
     pp.block_q = p.block_q;
     pp.work_items = (int32_t)(p.prefill_grid[0] / c.num_kv_heads);
-    hipError_t e = timed_launch(h, PA_KERNEL_PREFILL, st,
+    uint8_t* pw = ws + p.workspace_bytes - prefill_ws_bytes(sh.S, pp.work_items);
+    pp.seq_start = reinterpret_cast<int32_t*>(pw);
+    pw += align256((uint64_t)(sh.S + 1) * 4);
+    pp.list_seq = reinterpret_cast<int32_t*>(pw);
+    pw += align256((uint64_t)pp.work_items * 4);
+    pp.list_qb = reinterpret_cast<int32_t*>(pw);
+    pw += align256((uint64_t)pp.work_items * 4);
+    pp.count = reinterpret_cast<int32_t*>(pw);
+    hipError_t e = pa::launch_prefill_plan(a, pp, st);
+    if (e != hipSuccess) return hip_fail(e, "prefill plan launch");
+    e = timed_launch(h, PA_KERNEL_PREFILL, st,
                                 [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }

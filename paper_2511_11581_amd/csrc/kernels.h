@@ -43,6 +43,10 @@ struct DecodePlan {
 struct PrefillPlan {
   int32_t block_q;     // query tokens per Q-block (BLOCK_M / group)
   int32_t work_items;  // Q-block slots in the grid (upper bound)
+  int32_t* seq_start;  // [num_seqs + 1] prefix sums of Q-blocks per sequence
+  int32_t* list_seq;   // [work_items] sequence of the w-th Q-block (planned order)
+  int32_t* list_qb;    // [work_items] Q-block index inside that sequence
+  int32_t* count;      // [1] number of Q-blocks
 };
 
 struct GatherArgs {
@@ -75,6 +79,7 @@ struct ValidateArgs {
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st);
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st);
+hipError_t launch_prefill_plan(const BatchArgs& a, const PrefillPlan& p, hipStream_t st);
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
