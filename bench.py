@@ -57,6 +57,41 @@ def prefill_flops(w):
     return 4 * w.head_dim * w.num_q_heads * pairs
 
 
+KERNEL_SOURCES = {
+    "decode_kernel": ("decode.hip", "common.hpp", "kernels.h"),
+    "prefill_kernel": ("prefill.hip", "common.hpp", "kernels.h"),
+}
+
+
+def kernel_source_hash(kernel):
+    """sha256 over the source files a kernel is built from."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2511_11581_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs recorded in profiles/traffic.json (each
+    counter scaled by what it reads for a plain device copy of known size),
+    or None when no record exists or the kernel's sources have changed since
+    the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+        k = rec["kernels"][kernel]
+    except (OSError, KeyError, ValueError):
+        return None
+    if k.get("workload") != workload or k.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    cal = rec["calibration"]
+    return (k["fetch_kib"] * 1024 * cal["fetch_scale"] + k["write_kib"] * 1024 * cal["write_scale"])
+
+
 def make_attention(w, profile=False):
     from paper_2511_11581_amd import pa
     return pa.PagedAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size,
@@ -217,14 +252,16 @@ def main():
         dom_ms = h["per_kernel_us"].get("decode", 0) / 1e3
         achieved = decode_bytes(headline_w) / (dom_ms * 1e-3) / 1e9 if dom_ms else None
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS if achieved else None, "traffic": None,
+                "frac": achieved / HBM_PEAK_GBS if achieved else None,
+                "traffic": measured_traffic("decode_kernel", h["name"]),
                 "kernel": "decode_kernel", "kernel_us": dom_ms * 1e3}
     else:
         value, unit = h["TFLOPs"], "TFLOP/s"
         dom_ms = h["per_kernel_us"].get("prefill", 0) / 1e3
         achieved = prefill_flops(headline_w) / (dom_ms * 1e-3) / 1e12 if dom_ms else None
         roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / BF16_PEAK_TFLOPS if achieved else None, "traffic": None,
+                "frac": achieved / BF16_PEAK_TFLOPS if achieved else None,
+                "traffic": measured_traffic("prefill_kernel", h["name"]),
                 "kernel": "prefill_kernel", "kernel_us": dom_ms * 1e3}
 
     cpu = None

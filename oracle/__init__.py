@@ -45,9 +45,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB):
-        build(force=True)
-    lib = ctypes.CDLL(_LIB)
+    path = os.environ.get("PA_ORACLE_LIB")  # a test-built variant (mutation tests)
+    if not path:
+        path = _LIB
+        if not os.path.exists(_LIB):
+            build(force=True)
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     I = ctypes.c_int64
     D = ctypes.c_double

@@ -77,6 +77,23 @@ def sdpa_reference(q, ks, vs, seqs, G, scale, k_scale=1.0, v_scale=1.0):
     return torch.cat(outs, 0).numpy()
 
 
+def lse_reference(q, ks, seqs, G, scale, k_scale=1.0):
+    """Natural-log log-sum-exp of every row's causal scores, [T, Hq] (torch
+    fp64 logsumexp over an explicit dense score matrix)."""
+    outs = []
+    t0 = 0
+    for (c, ql), k in zip(seqs, ks):
+        L = c + ql
+        qq = to_f64(q[t0:t0 + ql]).permute(1, 0, 2)                  # [Hq, ql, d]
+        kk = to_f64(k, k_scale).repeat_interleave(G, dim=1).permute(1, 2, 0)  # [Hq, d, L]
+        s = scale * (qq @ kk)
+        mask = torch.arange(L)[None, :] <= (c + torch.arange(ql))[:, None]
+        s = s.masked_fill(~mask[None], float("-inf"))
+        outs.append(torch.logsumexp(s, dim=-1).permute(1, 0))
+        t0 += ql
+    return torch.cat(outs, 0).numpy()
+
+
 def rand_dense(seqs, Hq, Hkv, d, seed, fp8=False):
     g = torch.Generator().manual_seed(seed)
     T = sum(q for _, q in seqs)
@@ -117,8 +134,11 @@ def test_matches_dense_fp64_sdpa(case):
     scale = 1.0 / math.sqrt(d)
     ksc, vsc = (0.03, 0.02) if fp8 else (1.0, 1.0)
     ref = sdpa_reference(q, ks, vs, seqs, Hq // Hkv, scale, ksc, vsc)
-    out = oracle.forward(q, kc, vc, table, sl, qsl_of(seqs), scale, k_scale=ksc, v_scale=vsc)
+    out, lse = oracle.forward(q, kc, vc, table, sl, qsl_of(seqs), scale, k_scale=ksc, v_scale=vsc,
+                              with_lse=True)
     np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lse_reference(q, ks, seqs, Hq // Hkv, scale, ksc),
+                               rtol=0, atol=1e-12)
 
 
 def test_block_permutation_invariance():
