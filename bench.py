@@ -150,8 +150,8 @@ def measure(k, steps, warmup):
         "us_per_batch": ms * 1e3, "alg_bytes": B, "alg_flops": F,
         "GBps": B / (ms * 1e-3) / 1e9, "TFLOPs": F / (ms * 1e-3) / 1e12,
         "per_kernel_us": {kk: v * 1e3 for kk, v in kms.items() if v > 0},
-        "plan": {kk: plan[kk] for kk in ("segment_len", "max_splits", "block_q",
-                                         "decode_grid", "prefill_grid")},
+        "plan": {kk: plan[kk] for kk in ("decode_step", "decode_workers", "decode_min_steps",
+                                         "block_q", "decode_grid", "prefill_grid")},
     }
     res["frac_hbm"] = res["GBps"] / HBM_PEAK_GBS
     res["frac_mfma"] = res["TFLOPs"] / BF16_PEAK_TFLOPS

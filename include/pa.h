@@ -99,20 +99,36 @@ typedef struct pa_config {
 typedef struct pa_handle pa_handle;
 
 /* Kernel kinds reported by pa_profile_read. */
-enum { PA_KERNEL_DECODE = 0, PA_KERNEL_MERGE = 1, PA_KERNEL_PREFILL = 2, PA_KERNEL_KINDS = 3 };
+enum {
+  PA_KERNEL_DECODE = 0,   /* persistent split-KV decode workers */
+  PA_KERNEL_MERGE = 1,    /* log-sum-exp merge of decode pieces */
+  PA_KERNEL_PREFILL = 2,  /* Q-block kernel (rows with >= 2 query tokens) */
+  PA_KERNEL_PLAN = 3,     /* per-batch work lists built on the device */
+  PA_KERNEL_KINDS = 4
+};
 
 typedef struct pa_profile {
   int64_t launches[PA_KERNEL_KINDS];  /* timed launches since the last reset */
   double total_ms[PA_KERNEL_KINDS];   /* summed event-to-event durations */
 } pa_profile;
 
-/* The launch decisions for one batch shape (host-visible sizes only). */
+/* The launch decisions for one batch shape (host-visible sizes only).
+ *
+ * Decode work (rows with one query token) is split as the parallel tiled
+ * softmax of Sec. 4.5, with the segment boundaries chosen for a static
+ * launch grid (Sec. 4.7): the (sequence, kv head) pairs of the batch, each
+ * ceil(L / decode_step) steps long, are laid end to end and the resulting
+ * step range is cut into equal contiguous shares, one per worker (a wave);
+ * the part of one pair inside one share is a segment ("piece").  The device
+ * activates min(decode_workers, ceil(total steps / decode_min_steps))
+ * workers, so a single pair of 32 steps with decode_min_steps = 8 is cut
+ * into 4 segments of 8 steps (the example of Fig. 4). */
 typedef struct pa_plan_info {
-  int32_t decode_launch;     /* 1 if the decode (q_len == 1) kernel is launched */
-  int32_t decode_tile;       /* keys per wave iteration */
+  int32_t decode_launch;     /* 1 if the decode kernels are launched */
+  int32_t decode_step;       /* keys per decode step (32, 64 or 128) */
   int32_t decode_waves;      /* waves per decode workgroup */
-  int32_t segment_len;       /* keys per split-KV segment (Sec. 4.5) */
-  int32_t max_splits;        /* segments per sequence at most */
+  int32_t decode_workers;    /* waves in the static decode grid */
+  int32_t decode_min_steps;  /* fewest steps per active worker, batch permitting */
   int32_t merge_launch;      /* 1 if the log-sum-exp merge kernel is launched */
   int32_t prefill_launch;    /* 1 if the Q-block (q_len >= 2) kernel is launched */
   int32_t block_m;           /* rows per Q-block (BLOCK_M, Sec. 4.4) */
@@ -123,6 +139,17 @@ typedef struct pa_plan_info {
   int64_t prefill_grid[3];
   uint64_t workspace_bytes;  /* workspace this batch shape needs */
 } pa_plan_info;
+
+/* One segment of the decode partition (see pa_plan_info). */
+typedef struct pa_decode_piece {
+  int32_t seq;        /* sequence index */
+  int32_t kv_head;
+  int32_t worker;     /* worker (wave) that computes it */
+  int32_t first_key;  /* keys [first_key, end_key) of the sequence */
+  int32_t end_key;
+  int32_t slot;       /* -1: the whole row, written to out directly;
+                         0 / 1: partial slot of the worker, merged afterwards */
+} pa_decode_piece;
 
 /* Workspace bytes that suffice for every batch with at most max_seqs
  * sequences, max_tokens query rows and max_blocks_per_seq table entries per
@@ -147,8 +174,9 @@ pa_status pa_create(const pa_config *cfg, pa_handle **out);
  *   out             bf16 [T, Hq, d]; rows [0, query_start_loc[S]) are written
  *                   exactly once, other rows are untouched.
  * All base pointers and all non-unit strides must be 16-byte aligned in
- * bytes.  Sequences with query length 1 run on the split-KV decode kernel
- * (+ merge), the others on the Q-block kernel. */
+ * bytes.  Sequences with query length 1 run on the persistent split-KV
+ * decode kernel (+ merge), the others on the Q-block kernel; a one-workgroup
+ * plan kernel builds both work lists on the device first. */
 pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *v_cache, const pa_tensor *block_table,
                      const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,
@@ -169,6 +197,17 @@ pa_status pa_debug_gather(pa_handle *h, const pa_tensor *k_cache, const pa_tenso
  * then cfg is used. */
 pa_status pa_plan(const pa_handle *h, const pa_config *cfg, int32_t num_cus, int64_t num_tokens,
                   int64_t num_seqs, int64_t max_blocks_per_seq, pa_plan_info *out);
+
+/* The decode partition pa_forward computes on the device, reproduced on
+ * the host for metadata given in HOST memory (seq_lens [num_seqs],
+ * query_start_loc [num_seqs + 1]) and a device with num_cus compute units
+ * (<= 0: the handle's device, or 256).  Writes the first `cap` pieces in
+ * order of workers and sets *count to the total.  For inspection and tests;
+ * no HIP call.  h may be NULL, then cfg is used. */
+pa_status pa_decode_pieces(const pa_handle *h, const pa_config *cfg, int32_t num_cus,
+                           const int32_t *seq_lens, const int32_t *query_start_loc,
+                           int64_t num_seqs, int64_t num_tokens, int64_t max_blocks_per_seq,
+                           pa_decode_piece *pieces, int64_t cap, int64_t *count);
 
 /* Per-kernel durations recorded under PA_FLAG_PROFILE (zeros otherwise).
  * Waits for the recorded events to complete; with reset != 0 the counters

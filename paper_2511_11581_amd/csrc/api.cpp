@@ -3,16 +3,15 @@
 //
 // The planner sees host-visible sizes only (T, S, the block-table width MB,
 // the head configuration and the CU count); it never reads device metadata,
-// so pa_forward neither synchronises nor copies anything to the host.
-//   - Sequences with one query token (decode, Sec. 4.2) go to the split-KV
-//     decode kernel.  The segment length is chosen so that
-//     S * Hkv * max_splits covers about 8 workgroups per CU when every
-//     sequence is as long as the table allows (Sec. 4.5: split the tiles of
-//     long sequences over several program instances when the batch alone
-//     cannot fill the GPU).  Sequences that need more than one segment are
-//     merged by the log-sum-exp kernel.
-//   - Sequences with two or more query tokens go to the Q-block kernel
-//     (Sec. 4.4) with BLOCK_M = 128 rows, i.e. BLOCK_Q = 128 / G tokens.
+// so pa_forward neither synchronises nor copies anything to the host.  Per
+// call it launches, in stream order:
+//   1. the plan kernel (one workgroup): decode list and Q-block work list,
+//      built from the device metadata (Sec. 6.1);
+//   2. the decode kernel: a static grid of persistent waves (Sec. 4.7) that
+//      split the key tiles of all single-token rows evenly (Sec. 4.5);
+//   3. the log-sum-exp merge of pairs that span several workers;
+//   4. the Q-block kernel for rows with two or more query tokens (Sec. 4.4),
+//      BLOCK_M = 128 rows, i.e. BLOCK_Q = 128 / G tokens.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -32,13 +31,11 @@ struct pa_event_ring {
   int used = 0;
 };
 
-// Launch-planner knobs; defaults can be overridden for tuning sweeps with
-// PA_DECODE_WG_PER_CU (1..64) and PA_DECODE_MIN_SEG (128..2^20 keys, rounded
-// to a multiple of 128), read when a handle is created.
+// Launch-planner knob: the fewest decode steps a worker is given when the
+// batch has enough work (PA_DECODE_MIN_STEPS, 1..4096), read when a handle
+// is created.
 struct pa_tunables {
-  int decode_wg_per_cu;
-  int decode_min_seg;
-  int decode_head_major;   // PA_DECODE_HEAD_MAJOR: kv head fastest in the decode grid
+  int decode_min_steps;
 };
 
 struct pa_handle {
@@ -67,16 +64,14 @@ pa_status fail(pa_status st, const char* fmt, ...) {
 }
 
 constexpr int kMaxCus = 256;
-constexpr int kDecodeTile = 32;
-constexpr int kDecodeWaves = 4;
-constexpr int kSegQuantum = kDecodeTile * kDecodeWaves;  // keys per workgroup step
-constexpr int kMinSegDefault = 256;
-constexpr int kMinSegFloor = 128;
-constexpr int kWgPerCuDefault = 32;
-constexpr int kWgPerCuMax = 64;
+constexpr int kDecodeWaves = 4;       // waves per decode workgroup
+constexpr int kDecodeWgPerCu = 2;     // resident decode workgroups per CU (LDS and VGPR bound)
+constexpr int kMaxDecodeWorkers = kMaxCus * kDecodeWgPerCu * kDecodeWaves;
+constexpr int kMinStepsDefault = 8;
 constexpr int kBlockM = 128;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
+constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
@@ -121,21 +116,51 @@ pa_status check_config(const pa_config* c) {
 // Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) + (#sequences with q_i >= 2).
 int64_t prefill_items(int64_t T, int64_t S, int64_t bq) { return cdiv(T, bq) + std::min<int64_t>(S, T / 2); }
 
-// Prefill work-list area: seq_start [S + 1], list_seq [items], list_qb [items], count.
-uint64_t prefill_ws_bytes(int64_t S, int64_t items) {
-  return align256((uint64_t)(S + 1) * 4) + 2 * align256((uint64_t)items * 4) + 256;
+int decode_step_keys(const pa_config& c) {
+  return pa::decode_step_keys(c.head_dim, c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2);
+}
+
+int decode_workers(int cus) {
+  return std::min(std::max(cus, 1), kMaxCus) * kDecodeWgPerCu * kDecodeWaves;
+}
+
+// Workspace layout: validation header, decode-list counters, decode list
+// [S + 1] int4, piece partials [workers, 2, G, d] and [workers, 2, G, 2]
+// fp32, then the Q-block work list (seq_start [S + 1], list_seq, list_qb,
+// count).
+struct WsLayout {
+  uint64_t meta, dec, part_o, part_ml, seq_start, list_seq, list_qb, count, total;
+};
+
+WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
+  const int G = c.num_q_heads / c.num_kv_heads;
+  WsLayout l;
+  uint64_t off = kHeader;
+  l.meta = off;
+  off += kMeta;
+  l.dec = off;
+  off += align256((uint64_t)(S + 1) * 16);
+  l.part_o = off;
+  off += align256((uint64_t)workers * 2 * G * c.head_dim * 4);
+  l.part_ml = off;
+  off += align256((uint64_t)workers * 2 * G * 2 * 4);
+  l.seq_start = off;
+  off += items > 0 ? align256((uint64_t)(S + 1) * 4) : 0;
+  l.list_seq = off;
+  off += align256((uint64_t)items * 4);
+  l.list_qb = off;
+  off += align256((uint64_t)items * 4);
+  l.count = off;
+  off += items > 0 ? 256 : 0;
+  l.total = off;
+  return l;
 }
 
 pa_tunables tunables_from_env() {
-  pa_tunables t{kWgPerCuDefault, kMinSegDefault, 1};
-  if (const char* e = std::getenv("PA_DECODE_HEAD_MAJOR")) t.decode_head_major = std::min(std::max(std::atoi(e), 0), 2);
-  if (const char* e = std::getenv("PA_DECODE_WG_PER_CU")) {
+  pa_tunables t{kMinStepsDefault};
+  if (const char* e = std::getenv("PA_DECODE_MIN_STEPS")) {
     const int v = std::atoi(e);
-    if (v >= 1) t.decode_wg_per_cu = std::min(v, kWgPerCuMax);
-  }
-  if (const char* e = std::getenv("PA_DECODE_MIN_SEG")) {
-    const long v = std::atol(e);
-    if (v >= kMinSegFloor) t.decode_min_seg = (int)(std::min(v, 1L << 20) / 128 * 128);
+    if (v >= 1) t.decode_min_steps = std::min(v, 4096);
   }
   return t;
 }
@@ -143,45 +168,36 @@ pa_tunables tunables_from_env() {
 void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S,
                int64_t MB, pa_plan_info* p) {
   std::memset(p, 0, sizeof *p);
-  cus = std::min(std::max(cus, 1), kMaxCus);
   const int G = c.num_q_heads / c.num_kv_heads;
   const int64_t max_len = MB * c.block_size;
-  p->decode_tile = kDecodeTile;
+  p->decode_step = decode_step_keys(c);
   p->decode_waves = kDecodeWaves;
+  p->decode_workers = decode_workers(cus);
+  p->decode_min_steps = tun.decode_min_steps;
   p->block_m = kBlockM;
   p->block_q = kBlockM / G;
   p->prefill_tile = kPrefillTile;
-  uint64_t ws = kHeader;
+  int64_t items = 0;
   if (S >= 1 && T >= 1 && max_len >= 1) {
     p->decode_launch = 1;
-    const int64_t units = S * c.num_kv_heads;
-    const int64_t want = cdiv((int64_t)tun.decode_wg_per_cu * cus, units);
-    int64_t seg = cdiv(cdiv(max_len, want), kSegQuantum) * kSegQuantum;
-    seg = std::max<int64_t>(seg, tun.decode_min_seg);
-    const int64_t splits = cdiv(max_len, seg);
-    p->segment_len = (int32_t)seg;
-    p->max_splits = (int32_t)splits;
-    p->decode_grid[0] = splits;
-    p->decode_grid[1] = S;
-    p->decode_grid[2] = c.num_kv_heads;
-    if (splits > 1) {
-      p->merge_launch = 1;
-      p->merge_grid[0] = c.num_q_heads;
-      p->merge_grid[1] = S;
-      p->merge_grid[2] = 1;
-      const uint64_t rows = (uint64_t)S * splits * c.num_q_heads;
-      ws += align256(rows * c.head_dim * 4) + align256(rows * 2 * 4);
+    p->decode_grid[0] = p->decode_workers / kDecodeWaves;
+    p->decode_grid[1] = 1;
+    p->decode_grid[2] = 1;
+    p->merge_launch = 1;
+    p->merge_grid[0] = S;
+    p->merge_grid[1] = c.num_kv_heads;
+    p->merge_grid[2] = 1;
+    if (T >= 2 && max_len >= 2) {
+      p->prefill_launch = 1;
+      items = prefill_items(T, S, p->block_q);
+      p->prefill_grid[0] = items * c.num_kv_heads;
+      p->prefill_grid[1] = 1;
+      p->prefill_grid[2] = 1;
     }
+    p->workspace_bytes = ws_layout(c, p->decode_workers, S, items).total;
+  } else {
+    p->workspace_bytes = kHeader;
   }
-  if (S >= 1 && T >= 2 && max_len >= 2) {
-    p->prefill_launch = 1;
-    const int64_t items = prefill_items(T, S, p->block_q);
-    p->prefill_grid[0] = items * c.num_kv_heads;
-    p->prefill_grid[1] = 1;
-    p->prefill_grid[2] = 1;
-    ws += prefill_ws_bytes(S, items);
-  }
-  p->workspace_bytes = ws;
 }
 
 // ---- tensor checks -------------------------------------------------------
@@ -319,8 +335,8 @@ hipError_t timed_launch(pa_handle* h, int kind, hipStream_t st, F&& fn) {
 
 void destroy_events(pa_handle* h) {
   for (auto& r : h->ring) {
-    for (hipEvent_t ev : r.start) hipEventDestroy(ev);
-    for (hipEvent_t ev : r.stop) hipEventDestroy(ev);
+    for (hipEvent_t ev : r.start) (void)hipEventDestroy(ev);
+    for (hipEvent_t ev : r.stop) (void)hipEventDestroy(ev);
     r.start.clear();
     r.stop.clear();
   }
@@ -338,23 +354,13 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   if (!bytes) return fail(PA_ERR_INVALID_ARG, "bytes is NULL");
   if (max_tokens < 0 || max_seqs < 0 || max_blocks_per_seq < 0)
     return fail(PA_ERR_INVALID_ARG, "negative maximum");
-  // The split count grows with the table width and shrinks with the batch;
-  // take the largest requirement over all batch sizes up to max_seqs, with
-  // the fewest CUs the plan can assume (1), so any device is covered.
+  // The layout grows with S and T and the worker count is at most
+  // kMaxDecodeWorkers, so the largest batch on the largest device bounds all.
   uint64_t best = kHeader;
-  const int64_t max_len = max_blocks_per_seq * cfg->block_size;
-  if (max_seqs >= 1 && max_len >= 1) {
-    // splits(S) <= min(ceil(max_len / min_seg), ceil(wg_per_cu * cus / (S * Hkv))); the
-    // product S * splits(S) is bounded by min(S * ceil(max_len / min_seg),
-    // wg_per_cu * cus / Hkv + S), taken at the extreme knob values.
-    const int64_t by_len = max_seqs * cdiv(max_len, kMinSegFloor);
-    const int64_t by_target = (int64_t)kWgPerCuMax * kMaxCus / cfg->num_kv_heads + max_seqs;
-    const uint64_t rows = (uint64_t)std::min(by_len, by_target) * cfg->num_q_heads;
-    best += align256(rows * cfg->head_dim * 4) + align256(rows * 2 * 4);
-  }
-  if (max_seqs >= 1 && max_tokens >= 2) {
+  if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
     const int64_t bq = kBlockM / (cfg->num_q_heads / cfg->num_kv_heads);
-    best += prefill_ws_bytes(max_seqs, prefill_items(max_tokens, max_seqs, bq));
+    const int64_t items = max_tokens >= 2 ? prefill_items(max_tokens, max_seqs, bq) : 0;
+    best = ws_layout(*cfg, kMaxDecodeWorkers, max_seqs, items).total;
   }
   *bytes = best;
   return PA_OK;
@@ -369,6 +375,64 @@ pa_status pa_plan(const pa_handle* h, const pa_config* cfg, int32_t num_cus, int
     return fail(PA_ERR_INVALID_ARG, "negative size");
   int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
   make_plan(*c, h ? h->tun : tunables_from_env(), cus, num_tokens, num_seqs, max_blocks_per_seq, out);
+  return PA_OK;
+}
+
+pa_status pa_decode_pieces(const pa_handle* h, const pa_config* cfg, int32_t num_cus,
+                           const int32_t* seq_lens, const int32_t* query_start_loc, int64_t num_seqs,
+                           int64_t num_tokens, int64_t max_blocks_per_seq, pa_decode_piece* pieces,
+                           int64_t cap, int64_t* count) {
+  const pa_config* c = h ? &h->cfg : cfg;
+  TRY(check_config(c));
+  if (!count) return fail(PA_ERR_INVALID_ARG, "count is NULL");
+  if (num_seqs < 0 || num_tokens < 0 || max_blocks_per_seq < 0 || cap < 0)
+    return fail(PA_ERR_INVALID_ARG, "negative size");
+  if (num_seqs > 0 && (!seq_lens || !query_start_loc))
+    return fail(PA_ERR_INVALID_ARG, "metadata pointer is NULL");
+  if (cap > 0 && !pieces) return fail(PA_ERR_INVALID_ARG, "pieces is NULL");
+  const int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
+  const pa_tunables tun = h ? h->tun : tunables_from_env();
+  const int KS = decode_step_keys(*c), Hkv = c->num_kv_heads;
+  const int64_t cap_keys = max_blocks_per_seq * c->block_size;
+  // The decode list, as the plan kernel builds it.
+  struct Dec { int32_t s, L; int64_t P; };
+  std::vector<Dec> dec;
+  int64_t P = 0;
+  for (int64_t i = 0; i < num_seqs; ++i) {
+    const int64_t t0 = query_start_loc[i], L = std::min<int64_t>(seq_lens[i], cap_keys);
+    if (query_start_loc[i + 1] - t0 == 1 && t0 >= 0 && t0 < num_tokens && L >= 1) {
+      dec.push_back(Dec{(int32_t)i, (int32_t)L, P});
+      P += cdiv(L, KS);
+    }
+  }
+  const int64_t total = (int64_t)Hkv * P;
+  const int W = pa::active_workers(total, tun.decode_min_steps, decode_workers(cus));
+  // Walk every worker's range of the tile space, pair by pair.
+  int64_t n = 0;
+  size_t j = 0;
+  for (int w = 0; w < W; ++w) {
+    int64_t t = pa::worker_begin(w, total, W);
+    const int64_t te = pa::worker_begin(w + 1, total, W);
+    while (t < te) {
+      while (j + 1 < dec.size() && (int64_t)Hkv * dec[j + 1].P <= t) ++j;
+      const int64_t nt = cdiv(dec[j].L, KS);
+      const int64_t off = t - (int64_t)Hkv * dec[j].P;
+      const int64_t g = off / nt, k0 = off % nt, k1 = std::min(nt, k0 + (te - t));
+      const bool head = k0 > 0, tail = k1 < nt;
+      if (n < cap) {
+        pa_decode_piece& pc = pieces[n];
+        pc.seq = dec[j].s;
+        pc.kv_head = (int32_t)g;
+        pc.worker = w;
+        pc.first_key = (int32_t)(k0 * KS);
+        pc.end_key = (int32_t)std::min<int64_t>(k1 * KS, dec[j].L);
+        pc.slot = (!head && !tail) ? -1 : (head ? 0 : 1);
+      }
+      ++n;
+      t += k1 - k0;
+    }
+  }
+  *count = n;
   return PA_OK;
 }
 
@@ -445,6 +509,8 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   if (!(scale > 0.f) || !(scale < 1e30f)) return fail(PA_ERR_INVALID_ARG, "scale must be positive and finite");
   pa_plan_info p;
   make_plan(c, h->tun, h->cus, sh.T, sh.S, sh.MB, &p);
+  if (sh.S * cdiv(sh.MB * c.block_size, p.decode_step) * c.num_kv_heads > INT32_MAX)
+    return fail(PA_ERR_UNSUPPORTED, "batch too large for 32-bit decode step indices");
   if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
     return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
                 (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
@@ -500,39 +566,36 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   a.sl2 = scale * c.k_scale * 1.4426950408889634f;
   a.v_scale = c.v_scale;
 
-  if (p.decode_launch) {
-    pa::DecodePlan dp;
-    dp.seg_len = p.segment_len;
-    dp.max_splits = p.max_splits;
-    dp.head_major = h->tun.decode_head_major;
-    const uint64_t rows = (uint64_t)sh.S * p.max_splits * c.num_q_heads;
-    dp.part_o = reinterpret_cast<float*>(ws + kHeader);
-    dp.part_ml = reinterpret_cast<float*>(ws + kHeader + align256(rows * c.head_dim * 4));
-    hipError_t e = timed_launch(h, PA_KERNEL_DECODE, st,
-                                [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
-    if (e != hipSuccess) return hip_fail(e, "decode launch");
-    if (p.merge_launch) {
-      e = timed_launch(h, PA_KERNEL_MERGE, st,
-                       [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
-      if (e != hipSuccess) return hip_fail(e, "merge launch");
-    }
-  }
+  if (!p.decode_launch) return PA_OK;
+  const int64_t items = p.prefill_launch ? p.prefill_grid[0] / c.num_kv_heads : 0;
+  const WsLayout wl = ws_layout(c, p.decode_workers, sh.S, items);
+  pa::DecodePlan dp;
+  dp.workers = p.decode_workers;
+  dp.step_keys = p.decode_step;
+  dp.min_steps = p.decode_min_steps;
+  dp.meta = reinterpret_cast<int32_t*>(ws + wl.meta);
+  dp.dec = reinterpret_cast<int4*>(ws + wl.dec);
+  dp.part_o = reinterpret_cast<float*>(ws + wl.part_o);
+  dp.part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
+  pa::PrefillPlan pp;
+  pp.block_q = p.block_q;
+  pp.work_items = (int32_t)items;
+  pp.seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
+  pp.list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
+  pp.list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
+  pp.count = reinterpret_cast<int32_t*>(ws + wl.count);
+
+  hipError_t e = timed_launch(h, PA_KERNEL_PLAN, st,
+                              [&] { return pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st); });
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  e = timed_launch(h, PA_KERNEL_DECODE, st,
+                   [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+  if (e != hipSuccess) return hip_fail(e, "merge launch");
   if (p.prefill_launch) {
-    pa::PrefillPlan pp;
-    pp.block_q = p.block_q;
-    pp.work_items = (int32_t)(p.prefill_grid[0] / c.num_kv_heads);
-    uint8_t* pw = ws + p.workspace_bytes - prefill_ws_bytes(sh.S, pp.work_items);
-    pp.seq_start = reinterpret_cast<int32_t*>(pw);
-    pw += align256((uint64_t)(sh.S + 1) * 4);
-    pp.list_seq = reinterpret_cast<int32_t*>(pw);
-    pw += align256((uint64_t)pp.work_items * 4);
-    pp.list_qb = reinterpret_cast<int32_t*>(pw);
-    pw += align256((uint64_t)pp.work_items * 4);
-    pp.count = reinterpret_cast<int32_t*>(pw);
-    hipError_t e = pa::launch_prefill_plan(a, pp, st);
-    if (e != hipSuccess) return hip_fail(e, "prefill plan launch");
     e = timed_launch(h, PA_KERNEL_PREFILL, st,
-                                [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
+                     [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }
   return PA_OK;

@@ -1,29 +1,42 @@
-// Decode attention over a paged KV cache with split-KV segments
-// (arxiv 2511.11581, Sec. 4.4 GQA packing and Sec. 4.5 parallel tiled
-// softmax; Eq. 1-2 for what is computed).
+// Decode attention over a paged KV cache: persistent workers over an even
+// split of the batch's key tiles, plus the log-sum-exp merge
+// (arxiv 2511.11581, Sec. 4.4 GQA packing, Sec. 4.5 parallel tiled softmax,
+// Sec. 4.7 static launch grid; Eq. 1-2 for what is computed).
 //
-// One workgroup = (kv head g, segment k, sequence s), 4 waves.  Only
-// sequences whose query length is 1 are handled here.  All G = Hq/Hkv query
-// heads of kv head g are packed into the columns of one 16-wide MFMA tile,
-// so each K/V row of the segment is read from HBM exactly once.  The segment
-// [k*seg_len, min((k+1)*seg_len, L)) is cut into 32-key tiles dealt to the 4
-// waves round-robin; each wave keeps its own running max / sum / output and
-// the waves are merged through LDS at the end.  A sequence that needs one
-// segment writes bf16 output directly; otherwise the segment stores its
-// unnormalised partials for the log-sum-exp merge kernel.
+// Only sequences whose query length is 1 are handled here.  The plan kernel
+// lists them (j = 0..J-1) with the prefix P(j) of their step counts
+// nt(j) = ceil(L_j / KS) (KS keys per step).  The (sequence, kv head) pairs,
+// sequence-major, lay out a tile space of Hkv * P(J) steps: pair (j, g)
+// occupies [Hkv P(j) + g nt(j), + nt(j)).  Worker w of the W active workers
+// (one wave each, launched as a fixed grid of 4-wave workgroups) takes the
+// contiguous range [worker_begin(w), worker_begin(w + 1)) of that space, so
+// every worker streams the same number of K/V bytes whatever the lengths.
+// The part of one pair inside one worker is a piece, i.e. a segment of the
+// parallel tiled softmax: a piece covering its whole pair writes bf16
+// output; a piece cut at the worker's start (head) or end (tail) stores its
+// unnormalised partials (acc, m, l), and merge_kernel combines the pieces
+// of every pair that spans several workers.  A worker has at most one head
+// and one tail piece, so partial slot (w, 0) holds the head piece and
+// (w, 1) a tail-only piece.
 //
-// Memory path per wave and tile: K and V rows are read with whole-row
-// coalesced loads (16 lanes per row, 4 rows per instruction: lane l reads
-// key 4r + (l & 3), bytes (l >> 2) * LB of the row, r = 0..7), the next
-// tile's loads in flight while the current one is consumed.  Through the
-// wave's private LDS area they are rearranged for the matrix cores:
+// Per wave and step: the G query heads of kv head g are the columns of one
+// 16-wide MFMA tile, so every K/V row is read from HBM once.  K and V rows
+// are read with whole-row coalesced loads (16 lanes per 256-byte row; lane l
+// reads key 4r + (l & 3), bytes (l >> 2) * LB of the row), the next step's
+// loads in flight while the current one is consumed, also across piece
+// boundaries: the next piece's block ids are fetched while the current
+// piece runs.  Through the wave's private LDS area:
 //   K  -> natural bf16 rows, read back as MFMA A operands (key rows),
 //   V  -> V^T rows (one row per d), 16-byte transposing writes,
 //   S^T[16 keys x 16 heads] = K Q^T, P = online softmax (log2 domain),
 //   O^T[d x heads] += V^T P^T      (v_mfma_f32_16x16x32_bf16).
 // MFMA row m of key block kb holds key 16kb + (m >> 2) + 4(m & 3), so the 8
 // keys of one lane's P^T / V^T operand slots are exactly the 8 keys that one
-// loading lane holds (all keys of the tile congruent to l & 3 mod 4).
+// loading lane holds (all keys of the sub-tile congruent to l & 3 mod 4).
+// fp8 and head_dim 64 rows are shorter, so a step covers 2 or 4 sub-tiles
+// of 32 keys to keep the same bytes in flight per wave.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.h"
 
@@ -32,7 +45,7 @@ namespace pa {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kTile = 32;      // keys per wave iteration
+constexpr int kSub = 32;       // keys per sub-tile (one pass of the matrix cores)
 
 // V^T row r (a d index), 16-byte column group cg (8 keys): rows are 64 bytes,
 // 64 bytes of padding follow every 2^PSH rows (PSH = log2 of the d values a
@@ -59,6 +72,15 @@ __device__ __forceinline__ uint32_t dw(const typename LoadT<LB>::T& v, int i) {
   else return v[i];
 }
 
+__device__ __forceinline__ int lane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+
+// A contiguous range of steps of one (sequence, kv head) pair (wave-uniform).
+struct Piece {
+  int j, s, t0, L, g;  // decode-list index, sequence, token row, length, kv head
+  int k0, k1;          // steps [k0, k1) of the pair
+  int head, tail;      // the pair starts before / continues after this worker
+};
+
 template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan p) {
   constexpr int EB = FP8 ? 1 : 2;          // bytes per cached element
@@ -69,60 +91,104 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   constexpr int NSTEP = D / 32;            // MFMA k-steps over d
   constexpr int NDB = D / 16;              // 16-row d blocks of O^T
   constexpr int KRB = 2 * D + 32;          // LDS bytes per K row (bf16 + pad)
-  constexpr int KT = kTile * KRB;          // K tile bytes
-  constexpr int VT = 16 * (4 * D + 4 * (D >> PSH));  // V^T tile bytes
+  constexpr int KT = kSub * KRB;           // K sub-tile bytes
+  constexpr int VT = 16 * (4 * D + 4 * (D >> PSH));  // V^T sub-tile bytes
   constexpr int WB = KT + VT;              // LDS bytes per wave
-  constexpr int RED = D + 2;               // floats per (wave, head) in the merge area
+  constexpr int NSUB = decode_subtiles(D, EB);  // sub-tiles per step
+  constexpr int KS = kSub * NSUB;          // keys per step
+  constexpr int R = 8 * NSUB;              // rows one lane loads per step (K and V each)
+  constexpr int BPS = KS / 16;             // 16-key blocks per step
   typedef typename LoadT<LB>::T LT;
   static_assert(DPL == 8 || DPL == 4, "head_dim 64 or 128");
-  static_assert(kWaves * 16 * RED * 4 <= kWaves * WB, "merge area must fit");
+  constexpr int NWIN = 4;                  // block-id registers per lane (window of 64 NWIN blocks)
+  static_assert(64 % BPS == 0, "steps must not straddle block-id registers");
 
   __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves * WB];
 
   const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
   const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
   const int lq = lane & 3, lc = lane >> 2;     // loading coordinates
-  int g, ks, s;
-  if (p.head_major == 2) {
-    // XCD-grouped: workgroups are dealt round-robin to the 8 XCDs; the j-th
-    // workgroup of XCD x handles head j % Hkv of unit (j / Hkv) * 8 + x, so
-    // the Hkv heads of one (sequence, segment) run together on one XCD.
-    const int i = blockIdx.x, x = i & 7, j = i >> 3;
-    const int u = (j / a.num_kv_heads) * 8 + x;
-    if (u >= a.num_seqs * p.max_splits) return;
-    g = j % a.num_kv_heads;
-    s = u / p.max_splits;
-    ks = u % p.max_splits;
-  } else {
-    g = p.head_major ? blockIdx.x : blockIdx.y;
-    ks = p.head_major ? blockIdx.y : blockIdx.x;
-    s = blockIdx.z;
+  const int Hkv = a.num_kv_heads, G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
+
+  const int J = p.meta[0], Wn = p.meta[1];
+  const int w = blockIdx.x * kWaves + wave;
+  if (w >= Wn || J <= 0) return;
+  const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
+  int64_t t = worker_begin(w, Ttot, Wn);
+  const int64_t t_end = worker_begin(w + 1, Ttot, Wn);
+  if (t >= t_end) return;
+
+  // ---- first pair: largest j with Hkv * P(j) <= t, by a 64-ary search; the
+  //      wave then holds entries base .. base + 63 of the list, one per lane.
+  int lo = 0, hi = J;
+  while (hi - lo > 63) {
+    const int step = (hi - lo + 63) / 64;
+    const int idx = lo + lane * step;
+    const int64_t P = (int64_t)Hkv * p.dec[min(idx, J)].w;
+    const bool ok = idx < hi && P <= t;
+    lo += (63 - __builtin_clzll(__ballot(ok))) * step;
+    hi = min(hi, lo + step);
   }
-
-  const int t0 = a.qsl[s];
-  if (a.qsl[s + 1] - t0 != 1 || t0 < 0 || t0 >= a.num_tokens) return;
-  const int L = min(a.seq_lens[s], a.mb * a.block_size);
-  if (L <= 0) return;
-  const int nsplit = (L + p.seg_len - 1) / p.seg_len;
-  if (ks >= nsplit) return;
-  const int kbeg = ks * p.seg_len;
-  const int kend = min(L, kbeg + p.seg_len);
-  const int ntiles = (kend - kbeg + kTile - 1) / kTile;
-  const int32_t* bt_row = a.bt + (int64_t)s * a.bt_row;
-  const int G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
-
-  // Q^T as MFMA B operands: column c16 = head g*G + c16 (zero if c16 >= G),
-  // k-step st covers d = 32 st + 8 q4 + j.
-  bf16x8 qt[NSTEP];
+  int base = lo;
+  int4 ent = p.dec[min(base + lane, J)];
   {
+    const bool ok = base + lane < hi && (int64_t)Hkv * ent.w <= t;
+    lo = base + (63 - __builtin_clzll(__ballot(ok)));
+  }
+  // Entry jj of the list (jj + 1 - base <= 63 must hold): fields by readlane.
+  auto reload = [&](int jj) {   // rare: the wait below drains everything in flight
+    base = jj;
+    ent = p.dec[min(base + lane, J)];
+    __builtin_amdgcn_s_waitcnt(0);
+  };
+
+  // Block-table entries of the 64 * NWIN 16-key blocks starting at `first`
+  // (register i, lane l: block first + 64 i + l), loaded from clamped
+  // indices; entries past the sequence end are never used for a valid key,
+  // and every entry is clamped into [0, num_blocks) at its use.
+  auto load_window = [&](const Piece& pc, int first, int (&win)[NWIN]) {
+    const int32_t* bt_row = a.bt + (int64_t)pc.s * a.bt_row;
+#pragma unroll
+    for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(((first + 64 * i + lane) * 16) >> bsl, a.mb - 1)];
+  };
+  auto make_piece = [&](int jj, int g, int k0, int64_t budget) {
+    if (jj + 1 - base > 63) reload(jj);
+    Piece pc;
+    jj = uniform(jj);
+    pc.j = jj;
+    pc.s = lane_i(ent.x, jj - base);
+    pc.t0 = lane_i(ent.y, jj - base);
+    pc.L = min(lane_i(ent.z, jj - base), a.mb * a.block_size);
+    const int nt = lane_i(ent.w, jj + 1 - base) - lane_i(ent.w, jj - base);
+    pc.g = uniform(g);
+    pc.k0 = uniform(k0);
+    pc.k1 = uniform((int)min((int64_t)nt, (int64_t)k0 + budget));
+    pc.head = pc.k0 > 0;
+    pc.tail = pc.k1 < nt;
+    return pc;
+  };
+  // Q^T of a piece as MFMA B operands: column c16 = head g*G + c16 (zero if
+  // c16 >= G), k-step st covers d = 32 st + 8 q4 + j.
+  auto load_q = [&](const Piece& pc, bf16x8 (&qt)[NSTEP]) {
     const bool hv = c16 < G;
-    const uint8_t* qrow = a.q + (int64_t)t0 * a.q_tok + (int64_t)(g * G + (hv ? c16 : 0)) * a.q_head;
+    const uint8_t* qrow = a.q + (int64_t)pc.t0 * a.q_tok + (int64_t)(pc.g * G + (hv ? c16 : 0)) * a.q_head;
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) {
-      u32x4 w = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
-      qt[st] = __builtin_bit_cast(bf16x8, w);
+      u32x4 v = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
+      qt[st] = __builtin_bit_cast(bf16x8, v);
     }
+  };
+
+  Piece cur;
+  {
+    const int64_t Pj = lane_i(ent.w, lo - base);
+    const int nt = lane_i(ent.w, lo + 1 - base) - (int)Pj;
+    const int64_t off = t - (int64_t)Hkv * Pj;
+    cur = make_piece(lo, (int)(off / nt), (int)(off % nt), t_end - t);
   }
+  bf16x8 qc[NSTEP];
+  int win[NWIN];
+  int cb = 0;   // first 16-key block of the window held in win
 
   float m_run = kNegInf, l_run = 0.f;
   f32x4 o[NDB];
@@ -130,245 +196,308 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   for (int db = 0; db < NDB; ++db) o[db] = f32x4{0, 0, 0, 0};
   uint8_t* kl = lds + wave * WB;
   uint8_t* vt = kl + KT;
-  const uint8_t* kbase = a.k + (int64_t)g * a.kg.head + lc * LB;
-  const uint8_t* vbase = a.v + (int64_t)g * a.vg.head + lc * LB;
 
-  // This wave's tiles are wave, wave + 4, ...; it holds the physical block
-  // of each of their 16-key blocks in a per-lane page cache (lane j: tile
-  // number cache_base + j/2, half j%2), refilled every 32 tiles.
-  const int nt = wave < ntiles ? (ntiles - wave + kWaves - 1) / kWaves : 0;
-  int cache = 0, cache_base = -1000000;
-  auto refill = [&](int i0) {
-    const int blk16 = (kbeg + (wave + kWaves * (i0 + (lane >> 1))) * kTile) / 16 + (lane & 1);
-    const int key = blk16 * 16;
-    cache = key < kend ? page_of(bt_row, key, bsl, a.num_blocks) : 0;
-    cache_base = i0;
-  };
-  // Issue the loads of the i-th tile of this wave: lane holds keys 4r + lq.
-  auto issue = [&](int i, LT (&kr)[8], LT (&vr)[8]) {
-    if (i - cache_base >= 32) refill(i);
-    const int tb = kbeg + (wave + kWaves * i) * kTile;
-    const int pg0 = __builtin_amdgcn_readlane(cache, 2 * (i - cache_base));
-    int pg1 = __builtin_amdgcn_readlane(cache, 2 * (i - cache_base) + 1);
-    pg1 = (tb + 16 < kend) ? pg1 : pg0;
-    const int sl0 = tb & bsm, sl1 = (tb + 16) & bsm;
+  // Issue the K/V loads of step k of a pair (kv head g, block cache `cache`
+  // starting at 16-key block cb); live = 0 issues harmless loads of one row.
+  // Addresses: a wave-uniform (scalar) base per 4-row group and a fixed
+  // 32-bit per-lane offset (row lq of the group, byte lc * LB of the row).
+  const uint32_t koff = (uint32_t)(lq * a.kg.slot + lc * LB);
+  const uint32_t voff = (uint32_t)(lq * a.vg.slot + lc * LB);
+  // Issue the K (or V) loads of step k of the current piece (block ids from
+  // the window registers; refill() must have made the step's blocks resident).
+  auto issue = [&](const uint8_t* base, const KvGeom& geo, uint32_t off, int k, LT (&rows)[R]) {
+    const int blk0 = uniform(k * BPS - cb);
+    const int kb0 = (k * KS) & bsm;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int kb = r >> 2;
-      const int slot = (kb ? sl1 : sl0) + 4 * (r & 3) + lq;
-      const int64_t pg = kb ? pg1 : pg0;
-      kr[r] = ldn<LB>(kbase + pg * a.kg.blk + (int64_t)slot * a.kg.slot);
-      vr[r] = ldn<LB>(vbase + pg * a.vg.blk + (int64_t)slot * a.vg.slot);
+    for (int b = 0; b < BPS; ++b) {
+      const int bi = blk0 + b;   // never straddles registers: 64 % BPS == 0
+      int pg = lane_i(win[0], bi & 63);
+#pragma unroll
+      for (int i = 1; i < NWIN; ++i) pg = (bi >> 6) == i ? lane_i(win[i], bi & 63) : pg;
+      pg = pg < 0 ? 0 : (pg >= a.num_blocks ? a.num_blocks - 1 : pg);
+      const int sb = (kb0 + 16 * b) & bsm;
+      const uint8_t* bp = base + (int64_t)pg * geo.blk + (int64_t)cur.g * geo.head + (int64_t)sb * geo.slot;
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) rows[4 * b + r4] = ldn<LB>(bp + 4 * r4 * geo.slot + off);
     }
   };
   // bf16 words of one loaded row chunk (DPL values of one key).
-  auto to_bf16 = [&](const LT& v, uint32_t (&w)[NW]) {
+  auto to_bf16 = [&](const LT& v, uint32_t (&wd)[NW]) {
     if constexpr (FP8) {
 #pragma unroll
       for (int q = 0; q < LB / 4; ++q) {
         const u32x2 cv = fp8x4_to_bf16x4(dw<LB>(v, q));
-        w[2 * q] = cv[0];
-        w[2 * q + 1] = cv[1];
+        wd[2 * q] = cv[0];
+        wd[2 * q + 1] = cv[1];
       }
     } else {
 #pragma unroll
-      for (int q = 0; q < NW; ++q) w[q] = dw<LB>(v, q);
+      for (int q = 0; q < NW; ++q) wd[q] = dw<LB>(v, q);
     }
   };
-  // Attention update with the i-th tile of this wave.
-  auto consume = [&](int i, LT (&kr)[8], LT (&vr)[8]) {
-    const int tb = kbeg + (wave + kWaves * i) * kTile;
-    // ---- K rows -> LDS (bf16, natural layout)
+  // Scores and online-softmax update for step k of the current piece; the
+  // probabilities P^T of sub-tile u (as MFMA B operands) go to pt[u].
+  auto consume_k = [&](int k, LT (&kr)[R], bf16x8 (&pt)[NSUB]) {
+    f32x4 sacc[NSUB][2];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      uint32_t w[NW];
-      to_bf16(kr[r], w);
-      uint8_t* dst = kl + (4 * r + lq) * KRB + lc * (2 * DPL);
-      if constexpr (NW == 4) *(u32x4*)dst = u32x4{w[0], w[1], w[2], w[3]};
-      else *(u32x2*)dst = u32x2{w[0], w[1]};
+    for (int u = 0; u < NSUB; ++u) {
+      // ---- K rows -> LDS (bf16, natural layout)
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        uint32_t wd[NW];
+        to_bf16(kr[8 * u + r], wd);
+        uint8_t* dst = kl + (4 * r + lq) * KRB + lc * (2 * DPL);
+        if constexpr (NW == 4) *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
+        else *(u32x2*)dst = u32x2{wd[0], wd[1]};
+      }
+      // ---- S^T = K Q^T; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x4 acc = {0, 0, 0, 0};
+        const uint8_t* kp = kl + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
+#pragma unroll
+        for (int st = 0; st < NSTEP; ++st)
+          acc = mfma16(*(const bf16x8*)(kp + 64 * st), qc[st], acc);
+        sacc[u][kb] = acc;
+      }
     }
-    // ---- S^T = K Q^T; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
-    f32x4 sacc[2];
+    // ---- online softmax (log2 domain); lane holds keys 32u + 16kb + q4 + 4r of head c16
+    const int kend = uniform(cur.L - k * KS);   // keys of this step inside the sequence
+    if (kend < KS) {   // last step of the pair: mask keys >= L (compare with immediates)
+      const int lim = kend - q4;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x4 acc = {0, 0, 0, 0};
-      const uint8_t* kp = kl + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
+      for (int u = 0; u < NSUB; ++u)
 #pragma unroll
-      for (int st = 0; st < NSTEP; ++st)
-        acc = mfma16(*(const bf16x8*)(kp + 64 * st), qt[st], acc);
-      sacc[kb] = acc;
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            sacc[u][kb][r] = kSub * u + 16 * kb + 4 * r < lim ? sacc[u][kb][r] : kNegInf;
     }
-    // ---- online softmax (log2 domain); lane holds keys 16kb + q4 + 4r of head c16
-    float x[2][4];
     float mx = kNegInf;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int u = 0; u < NSUB; ++u)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = tb + 16 * kb + q4 + 4 * r;
-        x[kb][r] = key < kend ? sacc[kb][r] : kNegInf;
-        mx = fmaxf(mx, x[kb][r]);
-      }
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[u][kb][r]);
     mx = xor16_max(mx);
     mx = xor32_max(mx) * a.sl2;
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
     float psum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int u = 0; u < NSUB; ++u) {
+      float x[2][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        x[kb][r] = fast_exp2(__builtin_fmaf(x[kb][r], a.sl2, -m_new));
-        psum += x[kb][r];
-      }
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          x[kb][r] = fast_exp2(__builtin_fmaf(sacc[u][kb][r], a.sl2, -m_new));
+          psum += x[kb][r];
+        }
+      const u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
+                        pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
+      pt[u] = __builtin_bit_cast(bf16x8, pw);
+    }
     l_run = l_run * alpha + psum;
     m_run = m_new;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-    u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
-                pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
-    const bf16x8 pt = __builtin_bit_cast(bf16x8, pw);
+  };
+  // V^T column group of sub-tile u for d value e of this lane's chunk: the
+  // bf16 pairs (row 2jj, row 2jj + 1) for jj = 0..3, taken straight from the
+  // loaded row chunks (v_perm pairs the 16-bit halves, or the fp8 bytes,
+  // which one conversion then widens); with MASK, rows of keys >= kend
+  // (lim = kend - lq) read as zero, as their slots may hold NaN.
+  auto vt_col = [&](LT (&vr)[R], int u, int e, int lim, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    u32x4 col;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int r0 = 8 * u + 2 * jj, r1 = r0 + 1;
+      uint32_t w0, w1;
+      if constexpr (FP8) {
+        w0 = dw<LB>(vr[r0], e >> 2);
+        w1 = dw<LB>(vr[r1], e >> 2);
+      } else {
+        w0 = dw<LB>(vr[r0], e >> 1);
+        w1 = dw<LB>(vr[r1], e >> 1);
+      }
+      if constexpr (MASK) {
+        w0 = kSub * u + 4 * (2 * jj) < lim ? w0 : 0u;
+        w1 = kSub * u + 4 * (2 * jj + 1) < lim ? w1 : 0u;
+      }
+      if constexpr (FP8) {
+        const uint32_t bsel = (uint32_t)(e & 3);
+        const uint32_t pair = __builtin_amdgcn_perm(w1, w0, bsel | ((4u + bsel) << 8) | 0x0C0C0000u);
+        col[jj] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(pair, 1.0f, false));
+      } else {
+        col[jj] = __builtin_amdgcn_perm(w1, w0, (e & 1) ? 0x07060302u : 0x05040100u);
+      }
+    }
+    return col;
+  };
+  // O^T += V^T P^T for step k of the current piece.
+  auto consume_v = [&](int k, LT (&vr)[R], const bf16x8 (&pt)[NSUB]) {
+    const int kend = uniform(cur.L - k * KS);
+    const int lim = kend - lq;
+#pragma unroll
+    for (int u = 0; u < NSUB; ++u) {
+      // ---- V -> V^T: this lane's 8 keys (4r + lq, r = 0..7) are the 8
+      //      consecutive positions of column group lq.
+      if (kend < KS) {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e)
+          *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = vt_col(vr, u, e, lim, std::true_type{});
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e)
+          *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = vt_col(vr, u, e, lim, std::false_type{});
+      }
+      // ---- O^T += V^T P^T
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const u32x4 va = *(const u32x4*)(vt + vt_off<PSH>(16 * db + c16, q4));
+        o[db] = mfma16(__builtin_bit_cast(bf16x8, va), pt[u], o[db]);
+      }
+    }
+  };
+  // End of a piece: bf16 output if the piece is its whole pair, else partials.
+  auto finalize = [&]() {
+    float l_tot = xor16_sum(l_run);
+    l_tot = xor32_sum(l_tot);
+    if (c16 < G) {
+      if (!cur.head && !cur.tail) {
+        const float inv = a.v_scale / l_tot;
+        uint8_t* orow = a.out + (int64_t)cur.t0 * a.o_tok + (int64_t)(cur.g * G + c16) * a.o_head;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const u32x2 v2 = {pack_bf16(o[db][0] * inv, o[db][1] * inv), pack_bf16(o[db][2] * inv, o[db][3] * inv)};
+          *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
+        }
+      } else {
+        const int64_t row = ((int64_t)w * 2 + (cur.head ? 0 : 1)) * G + c16;
+        float* po = p.part_o + row * D;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[db];
+        if (q4 == 0) *(f32x2*)(p.part_ml + row * 2) = f32x2{m_run, l_tot};
+      }
+    }
+    m_run = kNegInf;
+    l_run = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db] = f32x4{0, 0, 0, 0};
+  };
 
-    // ---- V -> V^T: this lane's 8 keys (4r + lq, r = 0..7) are the 8
-    //      consecutive positions of column group lq; keys past the segment end
-    //      are zeroed (their slots may hold NaN).
-    uint32_t vw[8][NW];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      to_bf16(vr[r], vw[r]);
-      if (tb + 4 * r + lq >= kend) {
-#pragma unroll
-        for (int q = 0; q < NW; ++q) vw[r][q] = 0u;
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) {
-      const int wi = e >> 1;
-      u32x4 col;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = vw[2 * j][wi], hi = vw[2 * j + 1][wi];
-        col[j] = (e & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = col;
-    }
-    // ---- O^T += V^T P^T
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const u32x4 va = *(const u32x4*)(vt + vt_off<PSH>(16 * db + c16, q4));
-      o[db] = mfma16(__builtin_bit_cast(bf16x8, va), pt, o[db]);
+  // Software pipeline over the worker's steps (two register sets, loop
+  // unrolled by two).  Every half issues the loads of the next step (of the
+  // current piece, else the first step of the next piece) unconditionally,
+  // so that each wait covers only the older set; sched_barrier keeps the
+  // compiler from hoisting the consumer's first instructions above them.
+  // Make the blocks of step k resident in the window registers (a new window
+  // starts at the step's first block; the load is waited for at its use).
+  auto refill = [&](int k) {
+    if (k * BPS >= cb + 64 * NWIN) {   // rare: drains the loads in flight
+      cb = uniform(k * BPS);
+      load_window(cur, cb, win);
+      __builtin_amdgcn_s_waitcnt(0);
     }
   };
 
-  // Software pipeline: the loads of tile i+1 are in flight while tile i is
-  // consumed (two register sets, loop unrolled by two).  The steady-state
-  // body issues unconditionally so that each wait covers only the older set;
-  // sched_barrier keeps the compiler from hoisting the consumer's first
-  // instructions above the new loads (which would force a full wait).
-  LT krA[8], vrA[8], krB[8], vrB[8];
-  int i = 0;
-  if (nt > 0) issue(0, krA, vrA);
-  for (; i + 2 < nt; i += 2) {
-    issue(i + 1, krB, vrB);
-    __builtin_amdgcn_sched_barrier(0);
-    consume(i, krA, vrA);
-    issue(i + 2, krA, vrA);
-    __builtin_amdgcn_sched_barrier(0);
-    consume(i + 1, krB, vrB);
-  }
-  if (i + 1 < nt) {
-    issue(i + 1, krB, vrB);
-    __builtin_amdgcn_sched_barrier(0);
-    consume(i, krA, vrA);
-    consume(i + 1, krB, vrB);
-  } else if (i < nt) {
-    consume(i, krA, vrA);
-  }
-
-  // ---- merge the 4 waves through LDS
-  float l_tot = xor16_sum(l_run);
-  l_tot = xor32_sum(l_tot);
-  __syncthreads();
-  float* red = (float*)lds;
-  {
-    float* rw = red + (wave * 16 + c16) * RED;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) rw[16 * db + 4 * q4 + i] = o[db][i];
-    if (q4 == 0) {
-      rw[D] = m_run;
-      rw[D + 1] = l_tot;
+  // Per piece: block ids and query rows, then a software pipeline over its
+  // steps, skewed by half a step: the K loads of the next step are issued
+  // before the current step's scores, its V loads before the current step's
+  // P V product, so that the current step's K registers are free before the
+  // next step's V registers fill.  Two register sets, loop unrolled by two;
+  // the steady-state body issues unconditionally so that each wait covers
+  // only the older set, and sched_barrier keeps the compiler from hoisting
+  // the consumers above the new loads.
+  LT krA[R], vrA[R], krB[R], vrB[R];
+  auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&ky)[R], LT (&vy)[R]) {
+    bf16x8 pt[NSUB];
+    if (more) {
+      refill(k + 1);
+      issue(a.k, a.kg, koff, k + 1, ky);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  }
-  __syncthreads();
-  const int hq = a.num_q_heads;
-  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
-    const int hh = idx / D, dd = idx % D;
-    float M = kNegInf;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red[(w * 16 + hh) * RED + D]);
-    float num = 0.f, den = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float* rw = red + (w * 16 + hh) * RED;
-      const float sc = fast_exp2(rw[D] - M);
-      num += sc * rw[dd];
-      den += sc * rw[D + 1];
+    consume_k(k, kx, pt);
+    if (more) {
+      __builtin_amdgcn_sched_barrier(0);
+      issue(a.v, a.vg, voff, k + 1, vy);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    const int h = g * G + hh;
-    if (nsplit == 1) {
-      __bf16 r = (__bf16)(num / den * a.v_scale);
-      *(__bf16*)(a.out + (int64_t)t0 * a.o_tok + (int64_t)h * a.o_head + 2 * dd) = r;
+    consume_v(k, vx, pt);
+  };
+  for (;;) {
+    cb = uniform(cur.k0 * BPS);
+    load_window(cur, cb, win);
+    load_q(cur, qc);
+    __builtin_amdgcn_s_waitcnt(0);
+    int k = cur.k0;
+    issue(a.k, a.kg, koff, k, krA);
+    issue(a.v, a.vg, voff, k, vrA);
+    for (; k + 2 < cur.k1; k += 2) {
+      step(k, true, krA, vrA, krB, vrB);
+      step(k + 1, true, krB, vrB, krA, vrA);
+    }
+    if (k + 1 < cur.k1) {
+      step(k, true, krA, vrA, krB, vrB);
+      step(k + 1, false, krB, vrB, krA, vrA);
     } else {
-      const int64_t row = ((int64_t)s * p.max_splits + ks) * hq + h;
-      p.part_o[row * D + dd] = num;
-      if (dd == 0) {
-        p.part_ml[row * 2] = M;
-        p.part_ml[row * 2 + 1] = den;
-      }
+      step(k, false, krA, vrA, krB, vrB);
     }
+    finalize();
+    t += cur.k1 - cur.k0;
+    if (t >= t_end) break;
+    const int jj = cur.g + 1 < Hkv ? cur.j : cur.j + 1;
+    const int g = cur.g + 1 < Hkv ? cur.g + 1 : 0;
+    cur = make_piece(jj, g, 0, t_end - t);
   }
 }
 
-// Log-sum-exp merge of the segment partials of one (sequence, query head):
-// M = max_k m_k, out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k.
-// One thread per output element d; m_k and l_k are uniform per workgroup.
+// Log-sum-exp merge of the pieces of every (sequence, kv head) pair that
+// spans several workers: M = max_k m_k, out = sum_k 2^(m_k - M) acc_k /
+// sum_k 2^(m_k - M) l_k (Sec. 4.5).  One workgroup per pair; the pair's
+// first worker holds its piece in slot 1, later workers in slot 0.
 template <int D>
-__global__ __launch_bounds__(D) void merge_kernel(BatchArgs a, DecodePlan p) {
-  const int h = blockIdx.x, s = blockIdx.y;
-  const int t0 = a.qsl[s];
-  if (a.qsl[s + 1] - t0 != 1 || t0 < 0 || t0 >= a.num_tokens) return;
-  const int L = min(a.seq_lens[s], a.mb * a.block_size);
-  if (L <= 0) return;
-  const int nsplit = min((L + p.seg_len - 1) / p.seg_len, p.max_splits);
-  if (nsplit <= 1) return;
-  const int hq = a.num_q_heads, dd = threadIdx.x;
-  const int64_t row0 = (int64_t)s * p.max_splits * hq + h;
-  float M = kNegInf;
-  for (int k = 0; k < nsplit; ++k) M = fmaxf(M, p.part_ml[(row0 + (int64_t)k * hq) * 2]);
-  float num = 0.f, den = 0.f;
-  for (int k = 0; k < nsplit; ++k) {
-    const int64_t row = row0 + (int64_t)k * hq;
-    const float sc = fast_exp2(p.part_ml[row * 2] - M);
-    num += sc * p.part_o[row * D + dd];
-    den += sc * p.part_ml[row * 2 + 1];
+__global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
+  const int jj = blockIdx.x, g = blockIdx.y;
+  const int J = p.meta[0], Wn = p.meta[1];
+  if (jj >= J) return;
+  const int Hkv = a.num_kv_heads, G = a.group;
+  const int4 e = p.dec[jj];
+  const int nt = p.dec[jj + 1].w - e.w;
+  const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
+  const int64_t ta = (int64_t)Hkv * e.w + (int64_t)g * nt;
+  const int w0 = worker_of(ta, Ttot, Wn), w1 = worker_of(ta + nt - 1, Ttot, Wn);
+  if (w0 == w1) return;
+  const int n = w1 - w0 + 1;
+  auto row_of = [&](int k, int hh) {
+    return ((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * G + hh;
+  };
+  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
+    const int hh = idx / D, dd = idx % D;
+    float M = kNegInf;
+    for (int k = 0; k < n; ++k) M = fmaxf(M, p.part_ml[row_of(k, hh) * 2]);
+    float num = 0.f, den = 0.f;
+    for (int k = 0; k < n; ++k) {
+      const int64_t row = row_of(k, hh);
+      const f32x2 ml = *(const f32x2*)(p.part_ml + row * 2);
+      const float sc = fast_exp2(ml[0] - M);
+      num += sc * p.part_o[row * D + dd];
+      den += sc * ml[1];
+    }
+    const int h = g * G + hh;
+    __bf16 r = (__bf16)(num / den * a.v_scale);
+    *(__bf16*)(a.out + (int64_t)e.y * a.o_tok + (int64_t)h * a.o_head + 2 * dd) = r;
   }
-  __bf16 r = (__bf16)(num / den * a.v_scale);
-  *(__bf16*)(a.out + (int64_t)t0 * a.o_tok + (int64_t)h * a.o_head + 2 * dd) = r;
 }
 
 }  // namespace
 
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st) {
-  // kv head fastest: the workgroups reading the same cache blocks run together
-  dim3 grid(p.head_major ? a.num_kv_heads : p.max_splits,
-            p.head_major ? p.max_splits : a.num_kv_heads, a.num_seqs), block(256);
-  if (p.head_major == 2) {
-    const int64_t units = (int64_t)a.num_seqs * p.max_splits;
-    grid = dim3((unsigned)(((units + 7) / 8) * 8 * a.num_kv_heads), 1, 1);
-  }
+  const dim3 grid((unsigned)((p.workers + kWaves - 1) / kWaves)), block(64 * kWaves);
   if (head_dim == 128) {
     if (fp8) decode_kernel<128, true><<<grid, block, 0, st>>>(a, p);
     else decode_kernel<128, false><<<grid, block, 0, st>>>(a, p);
@@ -382,9 +511,9 @@ hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, 
 }
 
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st) {
-  dim3 grid(a.num_q_heads, a.num_seqs);
-  if (head_dim == 128) merge_kernel<128><<<grid, dim3(128), 0, st>>>(a, p);
-  else if (head_dim == 64) merge_kernel<64><<<grid, dim3(64), 0, st>>>(a, p);
+  const dim3 grid(a.num_seqs, a.num_kv_heads), block(256);
+  if (head_dim == 128) merge_kernel<128><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64) merge_kernel<64><<<grid, block, 0, st>>>(a, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

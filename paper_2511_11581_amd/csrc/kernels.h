@@ -6,6 +6,8 @@
 
 namespace pa {
 
+constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernel
+
 struct KvGeom {
   int64_t blk;   // bytes between physical blocks
   int64_t slot;  // bytes between token slots of one block
@@ -33,12 +35,41 @@ struct BatchArgs {
 };
 
 struct DecodePlan {
-  int32_t seg_len;     // keys per segment (multiple of 128)
-  int32_t max_splits;  // segments per sequence at most
-  int32_t head_major;  // grid order: kv head fastest (1) or segment fastest (0)
-  float* part_o;       // [num_seqs, max_splits, Hq, head_dim] unnormalised
-  float* part_ml;      // [num_seqs, max_splits, Hq, 2] (max in log2 units, sum)
+  int32_t workers;     // decode waves in the static grid (workgroups of 4 waves)
+  int32_t step_keys;   // keys per decode step (KS)
+  int32_t min_steps;   // fewest steps per active worker when the batch allows
+  int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
+  int4* dec;           // [J + 1] {sequence, token row, length, prefix P(j) of step counts}
+  float* part_o;       // [workers, 2, G, head_dim] unnormalised piece results
+  float* part_ml;      // [workers, 2, G, 2] (max in log2 units, sum)
 };
+
+// Keys per decode step: one lane loads LB = head_dim * elem_bytes / 16 bytes
+// of 8 rows per 32-key sub-tile; a step takes 16 / LB sub-tiles (at most 2)
+// to keep the bytes in flight per wave up.
+__host__ __device__ constexpr int decode_subtiles(int head_dim, int elem_bytes) {
+  return head_dim * elem_bytes / 16 >= 8 ? 16 / (head_dim * elem_bytes / 16) : 2;
+}
+__host__ __device__ constexpr int decode_step_keys(int head_dim, int elem_bytes) {
+  return 32 * decode_subtiles(head_dim, elem_bytes);
+}
+
+// Even split of the decode tile space (total steps over all (sequence, kv
+// head) pairs) over W workers: worker w takes [worker_begin(w), worker_begin(w + 1)).
+__host__ __device__ inline int64_t worker_begin(int64_t w, int64_t total, int64_t W) {
+  return w * total / W;
+}
+// The worker whose range holds step t (0 <= t < total).
+__host__ __device__ inline int worker_of(int64_t t, int64_t total, int64_t W) {
+  return (int)(((t + 1) * W - 1) / total);
+}
+// Workers given work: every worker gets at least min_steps steps when the
+// batch has that many, at most W, none for an empty batch.
+__host__ __device__ inline int active_workers(int64_t total, int64_t min_steps, int64_t W) {
+  if (total <= 0) return 0;
+  const int64_t want = (total + min_steps - 1) / min_steps;
+  return (int)(want < W ? want : W);
+}
 
 struct PrefillPlan {
   int32_t block_q;     // query tokens per Q-block (BLOCK_M / group)
@@ -79,7 +110,8 @@ struct ValidateArgs {
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st);
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st);
-hipError_t launch_prefill_plan(const BatchArgs& a, const PrefillPlan& p, hipStream_t st);
+hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
+                       bool with_prefill, hipStream_t st);
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);

@@ -27,132 +27,8 @@ namespace pa {
 
 namespace {
 
-constexpr int kTileN = 64;     // keys per tile
+constexpr int kTileN = kPrefillTileKeys;  // keys per tile
 constexpr int kThreads = 256;
-
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanSortCap = 8192;   // larger work lists keep the natural order
-constexpr int kPlanBuckets = 2048;   // key-tile counts are clamped to this
-
-// Number of Q-blocks of sequence i (0 for single-token or empty rows, and
-// for rows whose metadata is out of range).
-__device__ __forceinline__ int nqb_of(const BatchArgs& a, int i, int bq) {
-  const int t0 = a.qsl[i], q = a.qsl[i + 1] - t0;
-  if (q < 2 || t0 < 0 || t0 + q > a.num_tokens) return 0;
-  const int L = min(a.seq_lens[i], a.mb * a.block_size);
-  if (L < q) return 0;
-  return (q + bq - 1) / bq;
-}
-
-// Block-wide exclusive scan of one value per thread (kPlanThreads threads).
-__device__ int block_exclusive_scan(int v, int& total) {
-  __shared__ int wsum[kPlanThreads / 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  if (w == 0) {
-    int t = lane < kPlanThreads / 64 ? wsum[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(t, o);
-      if (lane >= o) t += y;
-    }
-    if (lane < kPlanThreads / 64) wsum[lane] = t;
-  }
-  __syncthreads();
-  const int before = (w > 0 ? wsum[w - 1] : 0) + x - v;
-  total = wsum[kPlanThreads / 64 - 1];
-  __syncthreads();
-  return before;
-}
-
-// Work list of the Q-block kernel, built on the device so the host never
-// reads the batch metadata (one workgroup).  Q-blocks are ordered by
-// decreasing number of key tiles (longest first), which evens out the
-// causal triangle's very unequal work items across the CUs.
-__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(BatchArgs a, PrefillPlan pp) {
-  __shared__ int hist[kPlanBuckets];
-  __shared__ int keys[kPlanSortCap];
-  const int tid = threadIdx.x, S = a.num_seqs, bq = pp.block_q;
-  // 1. prefix sums of Q-blocks per sequence
-  int carry = 0;
-  for (int base = 0; base < S; base += kPlanThreads) {
-    const int i = base + tid;
-    const int n = i < S ? nqb_of(a, i, bq) : 0;
-    int tot;
-    const int ex = block_exclusive_scan(n, tot);
-    if (i < S) pp.seq_start[i] = carry + ex;
-    carry += tot;
-  }
-  const int N = min(carry, pp.work_items);
-  if (tid == 0) {
-    pp.seq_start[S] = carry;
-    pp.count[0] = N;
-  }
-  __threadfence();
-  __syncthreads();
-  // item -> (sequence, Q-block index): binary search in seq_start (device-
-  // coherent loads: the array was just written by other threads)
-  auto start_of = [&](int i) {
-    return __hip_atomic_load(pp.seq_start + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  };
-  auto locate = [&](int idx, int& seq, int& qb) {
-    int lo = 0, hi = S - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (start_of(mid) <= idx) lo = mid; else hi = mid - 1;
-    }
-    seq = lo;
-    qb = idx - start_of(lo);
-  };
-  if (N > kPlanSortCap) {
-    for (int idx = tid; idx < N; idx += kPlanThreads) {
-      int seq, qb;
-      locate(idx, seq, qb);
-      pp.list_seq[idx] = seq;
-      pp.list_qb[idx] = qb;
-    }
-    return;
-  }
-  // 2. counting sort by decreasing key-tile count
-  for (int k = tid; k < kPlanBuckets; k += kPlanThreads) hist[k] = 0;
-  __syncthreads();
-  for (int idx = tid; idx < N; idx += kPlanThreads) {
-    int seq, qb;
-    locate(idx, seq, qb);
-    const int t0 = a.qsl[seq], q = a.qsl[seq + 1] - t0;
-    const int L = min(a.seq_lens[seq], a.mb * a.block_size);
-    const int kv = (L - q) + min((qb + 1) * bq, q);
-    const int key = min((kv + kTileN - 1) / kTileN, kPlanBuckets - 1);
-    keys[idx] = key;
-    atomicAdd(&hist[key], 1);
-  }
-  __syncthreads();
-  // exclusive scan of the histogram in decreasing key order: bucket offsets
-  int hcarry = 0;
-  for (int base = 0; base < kPlanBuckets; base += kPlanThreads) {
-    const int b = kPlanBuckets - 1 - (base + tid);
-    const int n = hist[b];
-    int tot;
-    const int ex = block_exclusive_scan(n, tot);
-    hist[b] = hcarry + ex;  // bucket b is read and written by this thread only
-    hcarry += tot;
-  }
-  __syncthreads();
-  for (int idx = tid; idx < N; idx += kPlanThreads) {
-    int seq, qb;
-    locate(idx, seq, qb);
-    const int pos = atomicAdd(&hist[keys[idx]], 1);
-    pp.list_seq[pos] = seq;
-    pp.list_qb[pos] = qb;
-  }
-}
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, PrefillPlan pp) {
@@ -456,11 +332,6 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 
 }  // namespace
 
-hipError_t launch_prefill_plan(const BatchArgs& a, const PrefillPlan& p, hipStream_t st) {
-  if (a.num_seqs <= 0) return hipSuccess;
-  prefill_plan_kernel<<<dim3(1), dim3(kPlanThreads), 0, st>>>(a, p);
-  return hipGetLastError();
-}
 
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st) {

@@ -36,13 +36,13 @@ PA_DTYPE_I32 = 2
 PA_DTYPE_F32 = 3
 PA_FLAG_VALIDATE = 1
 PA_FLAG_PROFILE = 2
-PA_KERNEL_KINDS = 3
-KERNEL_NAMES = ("decode", "merge", "prefill")
+PA_KERNEL_KINDS = 4
+KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
 
 # Every function declared in include/pa.h.
 EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
-           "pa_profile_read", "pa_destroy", "pa_last_error")
+           "pa_decode_pieces", "pa_profile_read", "pa_destroy", "pa_last_error")
 
 
 class pa_tensor(ctypes.Structure):
@@ -59,9 +59,9 @@ class pa_config(ctypes.Structure):
 
 
 class pa_plan_info(ctypes.Structure):
-    _fields_ = [("decode_launch", ctypes.c_int32), ("decode_tile", ctypes.c_int32),
-                ("decode_waves", ctypes.c_int32), ("segment_len", ctypes.c_int32),
-                ("max_splits", ctypes.c_int32), ("merge_launch", ctypes.c_int32),
+    _fields_ = [("decode_launch", ctypes.c_int32), ("decode_step", ctypes.c_int32),
+                ("decode_waves", ctypes.c_int32), ("decode_workers", ctypes.c_int32),
+                ("decode_min_steps", ctypes.c_int32), ("merge_launch", ctypes.c_int32),
                 ("prefill_launch", ctypes.c_int32), ("block_m", ctypes.c_int32),
                 ("block_q", ctypes.c_int32), ("prefill_tile", ctypes.c_int32),
                 ("decode_grid", ctypes.c_int64 * 3), ("merge_grid", ctypes.c_int64 * 3),
@@ -73,6 +73,11 @@ class pa_plan_info(ctypes.Structure):
             v = getattr(self, name)
             d[name] = list(v) if hasattr(v, "__len__") else int(v)
         return d
+
+
+class pa_decode_piece(ctypes.Structure):
+    _fields_ = [("seq", ctypes.c_int32), ("kv_head", ctypes.c_int32), ("worker", ctypes.c_int32),
+                ("first_key", ctypes.c_int32), ("end_key", ctypes.c_int32), ("slot", ctypes.c_int32)]
 
 
 class pa_profile(ctypes.Structure):
@@ -107,13 +112,18 @@ def load_library(path: str = LIB_PATH):
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, T, P]
     lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                             ctypes.POINTER(pa_plan_info)]
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    lib.pa_decode_pieces.argtypes = [P, C, ctypes.c_int32, I32P, I32P, ctypes.c_int64,
+                                     ctypes.c_int64, ctypes.c_int64,
+                                     ctypes.POINTER(pa_decode_piece), ctypes.c_int64,
+                                     ctypes.POINTER(ctypes.c_int64)]
     lib.pa_profile_read.argtypes = [P, ctypes.POINTER(pa_profile), ctypes.c_int]
     lib.pa_destroy.argtypes = [P]
     lib.pa_destroy.restype = None
     lib.pa_last_error.argtypes = []
     lib.pa_last_error.restype = ctypes.c_char_p
     for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
-                 "pa_profile_read"):
+                 "pa_decode_pieces", "pa_profile_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -184,6 +194,23 @@ def pa_plan(h=None, cfg: Optional[pa_config] = None, num_cus: int = 0, num_token
     _check(load_library().pa_plan(h, ctypes.byref(cfg) if cfg is not None else None, num_cus,
                                   num_tokens, num_seqs, max_blocks_per_seq, ctypes.byref(info)))
     return info.as_dict()
+
+
+def pa_decode_pieces(h=None, cfg: Optional[pa_config] = None, num_cus: int = 0, seq_lens=(),
+                     query_start_loc=(), num_tokens: int = 0, max_blocks_per_seq: int = 0) -> list:
+    """The decode partition of a batch whose metadata is given on the host:
+    a list of dicts {seq, kv_head, worker, first_key, end_key, slot}."""
+    lib = load_library()
+    sl = (ctypes.c_int32 * max(1, len(seq_lens)))(*[int(x) for x in seq_lens])
+    qsl = (ctypes.c_int32 * max(1, len(query_start_loc)))(*[int(x) for x in query_start_loc])
+    cfgp = ctypes.byref(cfg) if cfg is not None else None
+    n = ctypes.c_int64()
+    _check(lib.pa_decode_pieces(h, cfgp, num_cus, sl, qsl, len(seq_lens), num_tokens,
+                                max_blocks_per_seq, None, 0, ctypes.byref(n)))
+    buf = (pa_decode_piece * max(1, n.value))()
+    _check(lib.pa_decode_pieces(h, cfgp, num_cus, sl, qsl, len(seq_lens), num_tokens,
+                                max_blocks_per_seq, buf, n.value, ctypes.byref(n)))
+    return [{k: int(getattr(buf[i], k)) for k, _ in pa_decode_piece._fields_} for i in range(n.value)]
 
 
 def pa_profile_read(h, reset: bool = True) -> dict:

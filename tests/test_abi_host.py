@@ -63,49 +63,107 @@ def plan(c, cus=256, T=1, S=1, MB=1):
     return pa.pa_plan(None, c, cus, T, S, MB)
 
 
-def segment_ranges(n_keys, seg_len, tile):
-    """The decode kernel's partition of one row: segment k covers keys
-    [k * seg_len, min((k + 1) * seg_len, n_keys)), returned in tiles."""
-    out = []
-    k = 0
-    while k * seg_len < n_keys:
-        a, b = k * seg_len, min((k + 1) * seg_len, n_keys)
-        out.append((a // tile, -(-b // tile)))
-        k += 1
-    return out
-
-
-def test_plan_reproduces_the_papers_partition_example():
-    # Fig. 4 (Sec. 4.5): 32 tiles distributed over 4 segments of 8 tiles.
+def fig4_example():
     line = [x for x in open(os.path.join(GOLDEN, "fig4_segments.txt")).read().splitlines()
             if x and not x.startswith("#")][0]
     head, tail = line.split("|")
     n_tiles, tps = (int(x) for x in head.split())
-    expect = [tuple(int(x) for x in part.split()) for part in tail.split(";")]
-    p = plan(cfg(), cus=256, T=64, S=64, MB=n_tiles * 32 // 16)
-    assert p["decode_tile"] == 32
-    assert p["segment_len"] == tps * p["decode_tile"]
-    assert p["max_splits"] == len(expect)
-    assert segment_ranges(n_tiles * p["decode_tile"], p["segment_len"], p["decode_tile"]) == expect
+    return n_tiles, tps, [tuple(int(x) for x in part.split()) for part in tail.split(";")]
 
 
-def test_plan_decode_splits_fill_the_gpu():
-    # Llama-3-8B decode shape: 64 sequences up to 8193 tokens.
-    p = plan(cfg(), cus=256, T=64, S=64, MB=513)
-    assert p["decode_launch"] == 1 and p["merge_launch"] == 1
-    assert p["segment_len"] % (p["decode_tile"] * p["decode_waves"]) == 0
-    assert p["max_splits"] * p["segment_len"] >= 513 * 16
-    assert 64 * 8 * p["max_splits"] >= 8 * 256 * 0.9
-    assert p["decode_grid"] == [p["max_splits"], 64, 8]
-    # 70B-style long decode: 16 sequences, 8 kv heads, up to 131088 tokens.
-    p = plan(cfg(64, 8), cus=256, T=16, S=16, MB=8193)
-    assert p["max_splits"] >= 16 and p["segment_len"] >= 256
+def test_plan_reproduces_the_papers_partition_example():
+    # Fig. 4 (Sec. 4.5): the tiles of one long decode row are distributed over
+    # segments of 8 tiles, here 32 tiles over 4 segments.
+    n_tiles, tps, expect = fig4_example()
+    c = cfg(4, 1, 128)
+    p = plan(c, cus=256, T=1, S=1, MB=n_tiles * 2)
+    assert p["decode_step"] == 32 and p["decode_min_steps"] == tps
+    L = n_tiles * p["decode_step"]
+    pcs = pa.pa_decode_pieces(None, c, 256, [L], [0, 1], 1, n_tiles * 2)
+    got = [(x["first_key"] // 32, x["end_key"] // 32) for x in pcs]
+    assert got == expect
+    assert len({x["worker"] for x in pcs}) == len(expect)
+    # the first segment continues on the next worker (tail slot), the others
+    # start inside the row (head slot); all of them are merged
+    assert [x["slot"] for x in pcs] == [1] + [0] * (len(expect) - 1)
 
 
-def test_plan_short_batches_do_not_split():
-    p = plan(cfg(8, 2, 64), cus=256, T=4, S=4, MB=16)
-    assert p["max_splits"] == 1 and p["merge_launch"] == 0
-    assert p["workspace_bytes"] < 4096  # no split partials; header + prefill work list only
+def check_partition(c, cus, seq_lens, qsl, T, MB):
+    """Every decode row's keys are covered once, in order, by pieces of
+    consecutive workers; the workers' step counts differ by at most one."""
+    p = plan(c, cus=cus, T=T, S=len(seq_lens), MB=MB)
+    KS = p["decode_step"]
+    pcs = pa.pa_decode_pieces(None, c, cus, seq_lens, qsl, T, MB)
+    cap = MB * c.block_size
+    rows = {}
+    for x in pcs:
+        rows.setdefault((x["seq"], x["kv_head"]), []).append(x)
+    decode = [i for i in range(len(seq_lens))
+              if qsl[i + 1] - qsl[i] == 1 and 0 <= qsl[i] < T and min(seq_lens[i], cap) >= 1]
+    assert sorted(rows) == sorted((i, g) for i in decode for g in range(c.num_kv_heads))
+    for (i, g), lst in rows.items():
+        L = min(seq_lens[i], cap)
+        assert lst[0]["first_key"] == 0 and lst[-1]["end_key"] == L
+        for x, y in zip(lst, lst[1:]):
+            assert x["end_key"] == y["first_key"] and y["worker"] == x["worker"] + 1
+            assert x["end_key"] % KS == 0
+        if len(lst) == 1:
+            assert lst[0]["slot"] == -1
+        else:
+            assert lst[0]["slot"] == 1 and all(x["slot"] == 0 for x in lst[1:])
+    steps = {}
+    for x in pcs:
+        steps[x["worker"]] = steps.get(x["worker"], 0) + -(-(x["end_key"] - x["first_key"]) // KS)
+        # a worker holds at most one piece per partial slot
+    for w in steps:
+        slots = [x["slot"] for x in pcs if x["worker"] == w and x["slot"] >= 0]
+        assert len(slots) == len(set(slots))
+    if steps:
+        assert sorted(steps) == list(range(len(steps)))
+        assert max(steps.values()) - min(steps.values()) <= 1
+        total = sum(steps.values())
+        W = len(steps)
+        assert W == min(p["decode_workers"], -(-total // p["decode_min_steps"]))
+    return pcs
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_decode_partition_covers_every_key_once(seed):
+    g = torch.Generator().manual_seed(seed)
+    S = int(torch.randint(1, 200, (1,), generator=g))
+    MB = int(torch.randint(1, 300, (1,), generator=g))
+    bs = [16, 32, 64][seed % 3]
+    q = torch.randint(0, 3, (S,), generator=g)
+    q[torch.rand(S, generator=g) < 0.7] = 1
+    L = torch.minimum(torch.randint(1, MB * bs + 1, (S,), generator=g) + q, torch.tensor(MB * bs))
+    L = torch.maximum(L, q)
+    qsl = [0] + torch.cumsum(q, 0).tolist()
+    T = qsl[-1] + 3
+    for Hq, Hkv, d, kv in [(32, 8, 128, pa.PA_DTYPE_BF16), (64, 8, 128, pa.PA_DTYPE_FP8_E4M3),
+                           (8, 2, 64, pa.PA_DTYPE_BF16)]:
+        check_partition(cfg(Hq, Hkv, d, bs, kv), [1, 80, 256][seed % 3], L.tolist(), qsl, T, MB)
+
+
+def test_decode_partition_of_the_benchmark_decode_batch():
+    # 64 decode rows up to 8193 keys: all 2048 workers busy, one step apart
+    from paper_2511_11581_amd import workloads as W
+    w = W.make_config(2, device="cpu", poison=False)
+    c = cfg(32, 8, 128)
+    pcs = check_partition(c, 256, w.seq_lens.tolist(), w.query_start_loc.tolist(), w.num_tokens,
+                          int(w.block_table.shape[1]))
+    assert len({x["worker"] for x in pcs}) == 2048
+
+
+def test_plan_decode_grid_is_static():
+    for S, MB in [(1, 1), (64, 513), (16, 8193)]:
+        p = plan(cfg(), cus=256, T=S, S=S, MB=MB)
+        assert p["decode_launch"] == 1 and p["merge_launch"] == 1
+        assert p["decode_workers"] == 256 * 8
+        assert p["decode_grid"] == [p["decode_workers"] // p["decode_waves"], 1, 1]
+    assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 8
+    assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64
+    assert plan(cfg(8, 2, 64))["decode_step"] == 64
+    assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64  # sub-tiles capped at 2
 
 
 def test_plan_prefill_grid_bounds_the_q_blocks():
@@ -144,11 +202,11 @@ def test_workspace_bound_covers_every_plan():
         c = cfg(Hq, Hkv, d)
         for S_max, MB_max in [(1, 1), (4, 16), (64, 513), (16, 8193), (128, 1025), (300, 40)]:
             bound = pa.pa_workspace_bytes(c, 10 * S_max, S_max, MB_max)
-            for S, MB, cus in itertools.product(sorted({1, 2, 3, S_max // 2 or 1, S_max}),
-                                                sorted({1, MB_max // 3 or 1, MB_max}),
-                                                (1, 80, 256)):
-                p = plan(c, cus=cus, T=S, S=S, MB=MB)
-                assert p["workspace_bytes"] <= bound, (Hq, Hkv, d, S, MB, cus)
+            for S, MB, cus, T in itertools.product(sorted({1, 2, 3, S_max // 2 or 1, S_max}),
+                                                   sorted({1, MB_max // 3 or 1, MB_max}),
+                                                   (1, 80, 256), (1, 2, 10)):
+                p = plan(c, cus=cus, T=T * S, S=S, MB=MB)
+                assert p["workspace_bytes"] <= bound, (Hq, Hkv, d, S, MB, cus, T)
 
 
 def test_create_without_a_gpu_reports_a_device_error():

@@ -95,8 +95,9 @@ def test_invalid_arguments_are_reported_before_launch(bad):
 
 
 def test_workspace_too_small():
-    w = W.make_batch([(3000, 1), (2000, 1)], 8, 2, 128, seed=4).to("cuda")
-    att = attention_for(w, max_blocks=2)  # sized for short sequences only
+    # a batch with 600 prefill rows on a workspace sized for decode only
+    w = W.make_batch([(30, 600), (20, 1)], 8, 2, 128, seed=4).to("cuda")
+    att = attention_for(w, max_tokens=1)
     with pytest.raises(pa.PaError) as ei:
         _call(att, w)
     assert ei.value.status == pa.PA_ERR_WORKSPACE
