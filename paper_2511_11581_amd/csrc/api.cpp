@@ -185,8 +185,8 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
     p->decode_grid[2] = 1;
     p->merge_launch = 1;
     p->merge_grid[0] = S;
-    p->merge_grid[1] = c.num_kv_heads;
-    p->merge_grid[2] = 1;
+    p->merge_grid[1] = (G + 3) / 4;
+    p->merge_grid[2] = c.num_kv_heads;
     if (T >= 2 && max_len >= 2) {
       p->prefill_launch = 1;
       items = prefill_items(T, S, p->block_q);

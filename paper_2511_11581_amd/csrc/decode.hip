@@ -457,14 +457,20 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
 
 // Log-sum-exp merge of the pieces of every (sequence, kv head) pair that
 // spans several workers: M = max_k m_k, out = sum_k 2^(m_k - M) acc_k /
-// sum_k 2^(m_k - M) l_k (Sec. 4.5).  One workgroup per pair; the pair's
-// first worker holds its piece in slot 1, later workers in slot 0.
+// sum_k 2^(m_k - M) l_k (Sec. 4.5).  One wave per (pair, query head of the
+// group), lanes over d; the pair's first worker holds its piece in slot 1,
+// later workers in slot 0.  The pieces' (m, l) are read one per lane, 64 at
+// a time, and their weights reach the lanes by readlane.
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
-  const int jj = blockIdx.x, g = blockIdx.y;
+  constexpr int DPT = D / 64;   // d values per lane
+  const int lane = threadIdx.x & 63;
+  const int jj = blockIdx.x, G = a.group;
+  const int hh = uniform(blockIdx.y * 4 + (threadIdx.x >> 6));   // head within the group
+  const int g = blockIdx.z;
   const int J = p.meta[0], Wn = p.meta[1];
-  if (jj >= J) return;
-  const int Hkv = a.num_kv_heads, G = a.group;
+  if (jj >= J || hh >= G) return;
+  const int Hkv = a.num_kv_heads;
   const int4 e = p.dec[jj];
   const int nt = p.dec[jj + 1].w - e.w;
   const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
@@ -472,25 +478,55 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
   const int w0 = worker_of(ta, Ttot, Wn), w1 = worker_of(ta + nt - 1, Ttot, Wn);
   if (w0 == w1) return;
   const int n = w1 - w0 + 1;
-  auto row_of = [&](int k, int hh) {
-    return ((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * G + hh;
-  };
-  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
-    const int hh = idx / D, dd = idx % D;
-    float M = kNegInf;
-    for (int k = 0; k < n; ++k) M = fmaxf(M, p.part_ml[row_of(k, hh) * 2]);
-    float num = 0.f, den = 0.f;
-    for (int k = 0; k < n; ++k) {
-      const int64_t row = row_of(k, hh);
-      const f32x2 ml = *(const f32x2*)(p.part_ml + row * 2);
-      const float sc = fast_exp2(ml[0] - M);
-      num += sc * p.part_o[row * D + dd];
-      den += sc * ml[1];
-    }
-    const int h = g * G + hh;
-    __bf16 r = (__bf16)(num / den * a.v_scale);
-    *(__bf16*)(a.out + (int64_t)e.y * a.o_tok + (int64_t)h * a.o_head + 2 * dd) = r;
+  auto row_of = [&](int k) { return ((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * G + hh; };
+  float M = kNegInf;
+  for (int k0 = 0; k0 < n; k0 += 64) {
+    const int k = k0 + lane;
+    const float m = k < n ? p.part_ml[row_of(k) * 2] : kNegInf;
+    M = fmaxf(M, m);
   }
+  M = xor16_max(M);
+  M = xor32_max(M);
+  M = fmaxf(M, __shfl_xor(M, 8));
+  M = fmaxf(M, __shfl_xor(M, 4));
+  M = fmaxf(M, __shfl_xor(M, 2));
+  M = fmaxf(M, __shfl_xor(M, 1));
+  float num[DPT] = {}, den = 0.f;
+  for (int k0 = 0; k0 < n; k0 += 64) {
+    const int k = k0 + lane;
+    f32x2 ml = {kNegInf, 0.f};
+    if (k < n) ml = *(const f32x2*)(p.part_ml + row_of(k) * 2);
+    const float wk = k < n ? fast_exp2(ml[0] - M) : 0.f;
+    den += wk * ml[1];
+    const int kn = min(64, n - k0);
+    // 8 pieces per round: their loads are independent and in flight together
+    for (int i0 = 0; i0 < kn; i0 += 8) {
+      float v[8][DPT];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int kk = min(i0 + i, kn - 1);
+        const float* po = p.part_o + row_of(k0 + kk) * D + lane * DPT;
+#pragma unroll
+        for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float wi = i0 + i < kn ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk), i0 + i)) : 0.f;
+#pragma unroll
+        for (int x = 0; x < DPT; ++x) num[x] += wi * v[i][x];
+      }
+    }
+  }
+  den = xor16_sum(den);
+  den = xor32_sum(den);
+  den += __shfl_xor(den, 8);
+  den += __shfl_xor(den, 4);
+  den += __shfl_xor(den, 2);
+  den += __shfl_xor(den, 1);
+  const float inv = a.v_scale / den;
+  uint8_t* orow = a.out + (int64_t)e.y * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
+  if constexpr (DPT == 2) *(uint32_t*)orow = pack_bf16(num[0] * inv, num[1] * inv);
+  else *(__bf16*)orow = (__bf16)(num[0] * inv);
 }
 
 }  // namespace
@@ -511,7 +547,7 @@ hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, 
 }
 
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st) {
-  const dim3 grid(a.num_seqs, a.num_kv_heads), block(256);
+  const dim3 grid(a.num_seqs, (a.group + 3) / 4, a.num_kv_heads), block(256);
   if (head_dim == 128) merge_kernel<128><<<grid, block, 0, st>>>(a, p);
   else if (head_dim == 64) merge_kernel<64><<<grid, block, 0, st>>>(a, p);
   else return hipErrorInvalidValue;

@@ -45,10 +45,11 @@ struct DecodePlan {
 };
 
 // Keys per decode step: one lane loads LB = head_dim * elem_bytes / 16 bytes
-// of 8 rows per 32-key sub-tile; a step takes 16 / LB sub-tiles (at most 2)
-// to keep the bytes in flight per wave up.
+// of 8 rows per 32-key sub-tile.  A step is one sub-tile, or two when rows
+// are as short as 64 bytes (LB = 4), to keep the bytes in flight per wave up
+// without exceeding the register budget.
 __host__ __device__ constexpr int decode_subtiles(int head_dim, int elem_bytes) {
-  return head_dim * elem_bytes / 16 >= 8 ? 16 / (head_dim * elem_bytes / 16) : 2;
+  return head_dim * elem_bytes / 16 >= 8 ? 1 : 2;
 }
 __host__ __device__ constexpr int decode_step_keys(int head_dim, int elem_bytes) {
   return 32 * decode_subtiles(head_dim, elem_bytes);

@@ -23,102 +23,107 @@ constexpr int kPlanThreads = 1024;
 constexpr int kPlanSortCap = 8192;   // larger Q-block lists keep the natural order
 constexpr int kPlanBuckets = 2048;   // key-tile counts are clamped to this
 
-// Number of Q-blocks of sequence i (0 for single-token or empty rows, and
-// for rows whose metadata is out of range).
-__device__ __forceinline__ int nqb_of(const BatchArgs& a, int i, int bq) {
-  const int t0 = a.qsl[i], q = a.qsl[i + 1] - t0;
-  if (q < 2 || t0 < 0 || t0 + q > a.num_tokens) return 0;
-  const int L = min(a.seq_lens[i], a.mb * a.block_size);
-  if (L < q) return 0;
-  return (q + bq - 1) / bq;
-}
 
-// Block-wide exclusive scan of one value per thread (kPlanThreads threads).
-__device__ int block_exclusive_scan(int v, int& total) {
-  __shared__ int wsum[kPlanThreads / 64];
+// Block-wide exclusive scan of NV values per thread (kPlanThreads threads),
+// all in one pass; tot[] receives the block totals.
+template <int NV>
+__device__ void block_scan(const int (&v)[NV], int (&ex)[NV], int (&tot)[NV]) {
+  __shared__ int wsum[NV][kPlanThreads / 64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x = v;
+  int x[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) x[i] = v[i];
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int y = __shfl_up(x[i], o);
+      if (lane >= o) x[i] += y;
+    }
   }
-  if (lane == 63) wsum[w] = x;
+  if (lane == 63)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) wsum[i][w] = x[i];
   __syncthreads();
   if (w == 0) {
-    int t = lane < kPlanThreads / 64 ? wsum[lane] : 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(t, o);
-      if (lane >= o) t += y;
+    for (int i = 0; i < NV; ++i) {
+      int t = lane < kPlanThreads / 64 ? wsum[i][lane] : 0;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(t, o);
+        if (lane >= o) t += y;
+      }
+      if (lane < kPlanThreads / 64) wsum[i][lane] = t;
     }
-    if (lane < kPlanThreads / 64) wsum[lane] = t;
   }
   __syncthreads();
-  const int before = (w > 0 ? wsum[w - 1] : 0) + x - v;
-  total = wsum[kPlanThreads / 64 - 1];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    ex[i] = (w > 0 ? wsum[i][w - 1] : 0) + x[i] - v[i];
+    tot[i] = wsum[i][kPlanThreads / 64 - 1];
+  }
   __syncthreads();
-  return before;
 }
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodePlan dp, PrefillPlan pp,
                                                             int with_prefill) {
   __shared__ int hist[kPlanBuckets];
   __shared__ int keys[kPlanSortCap];
+  __shared__ int start_l[kPlanSortCap + 1];   // seq_start when S < kPlanSortCap
   const int tid = threadIdx.x, S = a.num_seqs;
   const int cap = a.mb * a.block_size;
-
-  // ---- decode list
-  {
-    int njs = 0, nsteps = 0;
-    for (int base = 0; base < S; base += kPlanThreads) {
-      const int i = base + tid;
-      int is_dec = 0, nt = 0, t0 = 0, L = 0;
-      if (i < S) {
-        t0 = a.qsl[i];
-        L = min(a.seq_lens[i], cap);
-        if (a.qsl[i + 1] - t0 == 1 && t0 >= 0 && t0 < a.num_tokens && L >= 1) {
-          is_dec = 1;
-          nt = (L + dp.step_keys - 1) / dp.step_keys;
-        }
-      }
-      int tot_j, tot_s;
-      const int ej = block_exclusive_scan(is_dec, tot_j);
-      const int es = block_exclusive_scan(nt, tot_s);
-      if (is_dec) dp.dec[njs + ej] = make_int4(i, t0, L, nsteps + es);
-      njs += tot_j;
-      nsteps += tot_s;
-    }
-    if (tid == 0) {
-      dp.dec[njs] = make_int4(0, 0, 0, nsteps);
-      dp.meta[0] = njs;
-      dp.meta[1] = active_workers((int64_t)a.num_kv_heads * nsteps, dp.min_steps, dp.workers);
-    }
-  }
-  if (!with_prefill) return;
-
-  // ---- Q-block list: 1. prefix sums of Q-blocks per sequence
   const int bq = pp.block_q;
-  int carry = 0;
+  const bool local = S < kPlanSortCap;
+
+  // ---- one pass over the sequences: decode flag, decode steps, Q-blocks
+  int njs = 0, nsteps = 0, nqb = 0;
   for (int base = 0; base < S; base += kPlanThreads) {
     const int i = base + tid;
-    const int n = i < S ? nqb_of(a, i, bq) : 0;
-    int tot;
-    const int ex = block_exclusive_scan(n, tot);
-    if (i < S) pp.seq_start[i] = carry + ex;
-    carry += tot;
+    int v[3] = {0, 0, 0};
+    int t0 = 0, L = 0;
+    if (i < S) {
+      t0 = a.qsl[i];
+      const int q = a.qsl[i + 1] - t0;
+      L = min(a.seq_lens[i], cap);
+      if (q == 1 && t0 >= 0 && t0 < a.num_tokens && L >= 1) {
+        v[0] = 1;
+        v[1] = (L + dp.step_keys - 1) / dp.step_keys;
+      } else if (with_prefill && q >= 2 && t0 >= 0 && t0 + q <= a.num_tokens && L >= q) {
+        v[2] = (q + bq - 1) / bq;
+      }
+    }
+    int ex[3], tot[3];
+    block_scan<3>(v, ex, tot);
+    if (v[0]) dp.dec[njs + ex[0]] = make_int4(i, t0, L, nsteps + ex[1]);
+    if (with_prefill && i < S) {
+      pp.seq_start[i] = nqb + ex[2];
+      if (local) start_l[i] = nqb + ex[2];
+    }
+    njs += tot[0];
+    nsteps += tot[1];
+    nqb += tot[2];
   }
-  const int N = min(carry, pp.work_items);
   if (tid == 0) {
-    pp.seq_start[S] = carry;
-    pp.count[0] = N;
+    dp.dec[njs] = make_int4(0, 0, 0, nsteps);
+    dp.meta[0] = njs;
+    dp.meta[1] = active_workers((int64_t)a.num_kv_heads * nsteps, dp.min_steps, dp.workers);
+    if (with_prefill) {
+      pp.seq_start[S] = nqb;
+      pp.count[0] = min(nqb, pp.work_items);
+    }
   }
-  __threadfence();
+  if (!with_prefill || nqb == 0) return;
+
+  // ---- Q-block list: item -> (sequence, Q-block index) by binary search
+  //      in the prefix sums (from LDS, or device-coherent global loads)
+  if (local && tid == 0) start_l[S] = nqb;
+  const int N = min(nqb, pp.work_items);
+  if (!local) __threadfence();
   __syncthreads();
-  // item -> (sequence, Q-block index): binary search in seq_start (device-
-  // coherent loads: the array was just written by other threads)
   auto start_of = [&](int i) {
-    return __hip_atomic_load(pp.seq_start + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return local ? start_l[i]
+                 : __hip_atomic_load(pp.seq_start + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
   auto locate = [&](int idx, int& seq, int& qb) {
     int lo = 0, hi = S - 1;
@@ -138,7 +143,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     }
     return;
   }
-  // 2. counting sort by decreasing key-tile count
+  // counting sort by decreasing key-tile count
   for (int k = tid; k < kPlanBuckets; k += kPlanThreads) hist[k] = 0;
   __syncthreads();
   for (int idx = tid; idx < N; idx += kPlanThreads) {
@@ -156,11 +161,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
   int hcarry = 0;
   for (int base = 0; base < kPlanBuckets; base += kPlanThreads) {
     const int b = kPlanBuckets - 1 - (base + tid);
-    const int n = hist[b];
-    int tot;
-    const int ex = block_exclusive_scan(n, tot);
-    hist[b] = hcarry + ex;  // bucket b is read and written by this thread only
-    hcarry += tot;
+    const int v[1] = {hist[b]};
+    int ex[1], tot[1];
+    block_scan<1>(v, ex, tot);
+    hist[b] = hcarry + ex[0];  // bucket b is read and written by this thread only
+    hcarry += tot[0];
   }
   __syncthreads();
   for (int idx = tid; idx < N; idx += kPlanThreads) {

@@ -161,9 +161,9 @@ def test_plan_decode_grid_is_static():
         assert p["decode_workers"] == 256 * 8
         assert p["decode_grid"] == [p["decode_workers"] // p["decode_waves"], 1, 1]
     assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 8
-    assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64
-    assert plan(cfg(8, 2, 64))["decode_step"] == 64
-    assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64  # sub-tiles capped at 2
+    assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 32
+    assert plan(cfg(8, 2, 64))["decode_step"] == 32
+    assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64  # 64-byte rows: two sub-tiles
 
 
 def test_plan_prefill_grid_bounds_the_q_blocks():
