@@ -64,9 +64,6 @@ pa_status fail(pa_status st, const char* fmt, ...) {
 }
 
 constexpr int kMaxCus = 256;
-constexpr int kDecodeWaves = 4;       // waves per decode workgroup
-constexpr int kDecodeWgPerCu = 2;     // resident decode workgroups per CU (LDS and VGPR bound)
-constexpr int kMaxDecodeWorkers = kMaxCus * kDecodeWgPerCu * kDecodeWaves;
 constexpr int kMinStepsDefault = 8;
 constexpr int kBlockM = 128;
 constexpr int kPrefillTile = 64;
@@ -120,9 +117,7 @@ int decode_step_keys(const pa_config& c) {
   return pa::decode_step_keys(c.head_dim, c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2);
 }
 
-int decode_workers(int cus) {
-  return std::min(std::max(cus, 1), kMaxCus) * kDecodeWgPerCu * kDecodeWaves;
-}
+int decode_workers(int cus) { return std::min(std::max(cus, 1), kMaxCus) * pa::kDecodeWaves; }
 
 // Workspace layout: validation header, decode-list counters, decode list
 // [S + 1] int4, piece partials [workers, 2, G, d] and [workers, 2, G, 2]
@@ -171,7 +166,7 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   const int G = c.num_q_heads / c.num_kv_heads;
   const int64_t max_len = MB * c.block_size;
   p->decode_step = decode_step_keys(c);
-  p->decode_waves = kDecodeWaves;
+  p->decode_waves = pa::kDecodeWaves;
   p->decode_workers = decode_workers(cus);
   p->decode_min_steps = tun.decode_min_steps;
   p->block_m = kBlockM;
@@ -180,7 +175,7 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   int64_t items = 0;
   if (S >= 1 && T >= 1 && max_len >= 1) {
     p->decode_launch = 1;
-    p->decode_grid[0] = p->decode_workers / kDecodeWaves;
+    p->decode_grid[0] = p->decode_workers / p->decode_waves;
     p->decode_grid[1] = 1;
     p->decode_grid[2] = 1;
     p->merge_launch = 1;
@@ -354,13 +349,13 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   if (!bytes) return fail(PA_ERR_INVALID_ARG, "bytes is NULL");
   if (max_tokens < 0 || max_seqs < 0 || max_blocks_per_seq < 0)
     return fail(PA_ERR_INVALID_ARG, "negative maximum");
-  // The layout grows with S and T and the worker count is at most
-  // kMaxDecodeWorkers, so the largest batch on the largest device bounds all.
+  // The layout grows with S and T and with the worker count, which is
+  // largest on the largest device, so that batch and device bound all.
   uint64_t best = kHeader;
   if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
     const int64_t bq = kBlockM / (cfg->num_q_heads / cfg->num_kv_heads);
     const int64_t items = max_tokens >= 2 ? prefill_items(max_tokens, max_seqs, bq) : 0;
-    best = ws_layout(*cfg, kMaxDecodeWorkers, max_seqs, items).total;
+    best = ws_layout(*cfg, decode_workers(kMaxCus), max_seqs, items).total;
   }
   *bytes = best;
   return PA_OK;

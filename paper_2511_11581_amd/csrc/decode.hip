@@ -8,7 +8,8 @@
 // nt(j) = ceil(L_j / KS) (KS keys per step).  The (sequence, kv head) pairs,
 // sequence-major, lay out a tile space of Hkv * P(J) steps: pair (j, g)
 // occupies [Hkv P(j) + g nt(j), + nt(j)).  Worker w of the W active workers
-// (one wave each, launched as a fixed grid of 4-wave workgroups) takes the
+// (one wave each, launched as a fixed grid of 4-wave workgroups, one or two per
+// CU) takes the
 // contiguous range [worker_begin(w), worker_begin(w + 1)) of that space, so
 // every worker streams the same number of K/V bytes whatever the lengths.
 // The part of one pair inside one worker is a piece, i.e. a segment of the
@@ -22,10 +23,8 @@
 // Per wave and step: the G query heads of kv head g are the columns of one
 // 16-wide MFMA tile, so every K/V row is read from HBM once.  K and V rows
 // are read with whole-row coalesced loads (16 lanes per 256-byte row; lane l
-// reads key 4r + (l & 3), bytes (l >> 2) * LB of the row), the next step's
-// loads in flight while the current one is consumed, also across piece
-// boundaries: the next piece's block ids are fetched while the current
-// piece runs.  Through the wave's private LDS area:
+// reads key 4r + (l & 3), bytes (l >> 2) * LB of the row), the next one or
+// two steps' loads in flight while the current one is consumed.  Through the wave's private LDS area:
 //   K  -> natural bf16 rows, read back as MFMA A operands (key rows),
 //   V  -> V^T rows (one row per d), 16-byte transposing writes,
 //   S^T[16 keys x 16 heads] = K Q^T, P = online softmax (log2 domain),
@@ -44,7 +43,6 @@ namespace pa {
 
 namespace {
 
-constexpr int kWaves = 4;
 constexpr int kSub = 32;       // keys per sub-tile (one pass of the matrix cores)
 
 // V^T row r (a d index), 16-byte column group cg (8 keys): rows are 64 bytes,
@@ -82,7 +80,7 @@ struct Piece {
 };
 
 template <int D, bool FP8>
-__global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan p) {
+__global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs a, DecodePlan p) {
   constexpr int EB = FP8 ? 1 : 2;          // bytes per cached element
   constexpr int LB = D * EB / 16;          // bytes one lane loads per row
   constexpr int DPL = LB / EB;             // d values one lane loads per row
@@ -103,7 +101,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   constexpr int NWIN = 4;                  // block-id registers per lane (window of 64 NWIN blocks)
   static_assert(64 % BPS == 0, "steps must not straddle block-id registers");
 
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves * WB];
+  // LDS sized so that one workgroup fills a CU (a second would not fit).
+  constexpr int kLdsBytes = kDecodeWaves * WB > 80 * 1024 + 1024 ? kDecodeWaves * WB : 80 * 1024 + 1024;
+  static_assert(kLdsBytes <= 160 * 1024 && 2 * kLdsBytes > 160 * 1024, "one workgroup per CU");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
 
   const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
   const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   const int Hkv = a.num_kv_heads, G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
 
   const int J = p.meta[0], Wn = p.meta[1];
-  const int w = blockIdx.x * kWaves + wave;
+  const int w = blockIdx.x * kDecodeWaves + wave;
   if (w >= Wn || J <= 0) return;
   const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
   int64_t t = worker_begin(w, Ttot, Wn);
@@ -405,25 +406,25 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
   };
 
   // Per piece: block ids and query rows, then a software pipeline over its
-  // steps, skewed by half a step: the K loads of the next step are issued
-  // before the current step's scores, its V loads before the current step's
-  // P V product, so that the current step's K registers are free before the
-  // next step's V registers fill.  Two register sets, loop unrolled by two;
-  // the steady-state body issues unconditionally so that each wait covers
-  // only the older set, and sched_barrier keeps the compiler from hoisting
-  // the consumers above the new loads.
+  // steps with one step in flight, skewed by half a step: while step k is
+  // consumed, the K loads of step k + 1 are issued before its scores and the
+  // V loads before its P V product, so that step k's K registers are free
+  // before step k + 1's V registers fill.  Two register sets, loop unrolled
+  // by two with an exact tail; every issue in the loop body is
+  // unconditional so that each wait covers only the older set, and
+  // sched_barrier keeps the compiler from hoisting consumers above the loads.
   LT krA[R], vrA[R], krB[R], vrB[R];
-  auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&ky)[R], LT (&vy)[R]) {
+  auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&kz)[R], LT (&vz)[R]) {
     bf16x8 pt[NSUB];
     if (more) {
       refill(k + 1);
-      issue(a.k, a.kg, koff, k + 1, ky);
+      issue(a.k, a.kg, koff, k + 1, kz);
       __builtin_amdgcn_sched_barrier(0);
     }
     consume_k(k, kx, pt);
     if (more) {
       __builtin_amdgcn_sched_barrier(0);
-      issue(a.v, a.vg, voff, k + 1, vy);
+      issue(a.v, a.vg, voff, k + 1, vz);
       __builtin_amdgcn_sched_barrier(0);
     }
     consume_v(k, vx, pt);
@@ -434,17 +435,18 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(BatchArgs a, DecodePlan 
     load_q(cur, qc);
     __builtin_amdgcn_s_waitcnt(0);
     int k = cur.k0;
+    const int k1 = cur.k1;
     issue(a.k, a.kg, koff, k, krA);
     issue(a.v, a.vg, voff, k, vrA);
-    for (; k + 2 < cur.k1; k += 2) {
+    for (; k + 2 < k1; k += 2) {   // A holds step k
       step(k, true, krA, vrA, krB, vrB);
       step(k + 1, true, krB, vrB, krA, vrA);
     }
-    if (k + 1 < cur.k1) {
+    if (k + 1 < k1) {
       step(k, true, krA, vrA, krB, vrB);
-      step(k + 1, false, krB, vrB, krA, vrA);
+      step(k + 1, false, krB, vrB, krB, vrB);
     } else {
-      step(k, false, krA, vrA, krB, vrB);
+      step(k, false, krA, vrA, krA, vrA);
     }
     finalize();
     t += cur.k1 - cur.k0;
@@ -533,7 +535,7 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
 
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st) {
-  const dim3 grid((unsigned)((p.workers + kWaves - 1) / kWaves)), block(64 * kWaves);
+  const dim3 grid((unsigned)((p.workers + kDecodeWaves - 1) / kDecodeWaves)), block(64 * kDecodeWaves);
   if (head_dim == 128) {
     if (fp8) decode_kernel<128, true><<<grid, block, 0, st>>>(a, p);
     else decode_kernel<128, false><<<grid, block, 0, st>>>(a, p);

@@ -7,6 +7,13 @@
 namespace pa {
 
 constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernel
+// Decode workgroup: 4 waves, one workgroup per CU (its LDS use keeps a
+// second one out), so one wave per SIMD.  With two waves on a SIMD the
+// memory system serves the first wave slot first and the second finishes
+// ~1.5x later, which a static split of the steps cannot absorb; deeper
+// per-wave pipelines (three register sets) and two workgroups per CU
+// measured no faster than one wave per SIMD with one step in flight.
+constexpr int kDecodeWaves = 4;
 
 struct KvGeom {
   int64_t blk;   // bytes between physical blocks
@@ -35,7 +42,7 @@ struct BatchArgs {
 };
 
 struct DecodePlan {
-  int32_t workers;     // decode waves in the static grid (workgroups of 4 waves)
+  int32_t workers;     // decode waves in the static grid
   int32_t step_keys;   // keys per decode step (KS)
   int32_t min_steps;   // fewest steps per active worker when the batch allows
   int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
@@ -45,11 +52,11 @@ struct DecodePlan {
 };
 
 // Keys per decode step: one lane loads LB = head_dim * elem_bytes / 16 bytes
-// of 8 rows per 32-key sub-tile.  A step is one sub-tile, or two when rows
-// are as short as 64 bytes (LB = 4), to keep the bytes in flight per wave up
-// without exceeding the register budget.
+// of 8 rows per 32-key sub-tile.  A step is one sub-tile; bf16 rows shorter
+// than 256 bytes and fp8 rows of 64 bytes take two, so that a step moves
+// 8-16 KB per wave within the register budget of the workgroup shape.
 __host__ __device__ constexpr int decode_subtiles(int head_dim, int elem_bytes) {
-  return head_dim * elem_bytes / 16 >= 8 ? 1 : 2;
+  return head_dim * elem_bytes / 16 >= (elem_bytes == 1 ? 8 : 16) ? 1 : 2;
 }
 __host__ __device__ constexpr int decode_step_keys(int head_dim, int elem_bytes) {
   return 32 * decode_subtiles(head_dim, elem_bytes);

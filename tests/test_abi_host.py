@@ -145,24 +145,25 @@ def test_decode_partition_covers_every_key_once(seed):
 
 
 def test_decode_partition_of_the_benchmark_decode_batch():
-    # 64 decode rows up to 8193 keys: all 2048 workers busy, one step apart
+    # 64 decode rows up to 8193 keys: all 1024 workers busy, one step apart
     from paper_2511_11581_amd import workloads as W
     w = W.make_config(2, device="cpu", poison=False)
     c = cfg(32, 8, 128)
     pcs = check_partition(c, 256, w.seq_lens.tolist(), w.query_start_loc.tolist(), w.num_tokens,
                           int(w.block_table.shape[1]))
-    assert len({x["worker"] for x in pcs}) == 2048
+    assert len({x["worker"] for x in pcs}) == 1024
 
 
 def test_plan_decode_grid_is_static():
     for S, MB in [(1, 1), (64, 513), (16, 8193)]:
         p = plan(cfg(), cus=256, T=S, S=S, MB=MB)
         assert p["decode_launch"] == 1 and p["merge_launch"] == 1
-        assert p["decode_workers"] == 256 * 8
+        assert p["decode_workers"] == 256 * 4
         assert p["decode_grid"] == [p["decode_workers"] // p["decode_waves"], 1, 1]
-    assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 8
+    assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 4
     assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 32
-    assert plan(cfg(8, 2, 64))["decode_step"] == 32
+    assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_workers"] == 256 * 4
+    assert plan(cfg(8, 2, 64))["decode_step"] == 64
     assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64  # 64-byte rows: two sub-tiles
 
 
