@@ -8,9 +8,8 @@
 // nt(j) = ceil(L_j / KS) (KS keys per step).  The (sequence, kv head) pairs,
 // sequence-major, lay out a tile space of Hkv * P(J) steps: pair (j, g)
 // occupies [Hkv P(j) + g nt(j), + nt(j)).  Worker w of the W active workers
-// (one wave each, launched as a fixed grid of 4-wave workgroups, one or two per
-// CU) takes the
-// contiguous range [worker_begin(w), worker_begin(w + 1)) of that space, so
+// (one wave each, launched as a fixed grid of 4-wave workgroups, one per CU)
+// takes the contiguous range [worker_begin(w), worker_begin(w + 1)) of that space, so
 // every worker streams the same number of K/V bytes whatever the lengths.
 // The part of one pair inside one worker is a piece, i.e. a segment of the
 // parallel tiled softmax: a piece covering its whole pair writes bf16
@@ -23,8 +22,9 @@
 // Per wave and step: the G query heads of kv head g are the columns of one
 // 16-wide MFMA tile, so every K/V row is read from HBM once.  K and V rows
 // are read with whole-row coalesced loads (16 lanes per 256-byte row; lane l
-// reads key 4r + (l & 3), bytes (l >> 2) * LB of the row), the next one or
-// two steps' loads in flight while the current one is consumed.  Through the wave's private LDS area:
+// reads key 4r + (l & 3), bytes (l >> 2) * LB of the row), the next step's
+// loads in flight while the current one is consumed.  Through the wave's
+// private LDS area:
 //   K  -> natural bf16 rows, read back as MFMA A operands (key rows),
 //   V  -> V^T rows (one row per d), 16-byte transposing writes,
 //   S^T[16 keys x 16 heads] = K Q^T, P = online softmax (log2 domain),
@@ -32,8 +32,8 @@
 // MFMA row m of key block kb holds key 16kb + (m >> 2) + 4(m & 3), so the 8
 // keys of one lane's P^T / V^T operand slots are exactly the 8 keys that one
 // loading lane holds (all keys of the sub-tile congruent to l & 3 mod 4).
-// fp8 and head_dim 64 rows are shorter, so a step covers 2 or 4 sub-tiles
-// of 32 keys to keep the same bytes in flight per wave.
+// A step is one sub-tile of 32 keys, or two for head_dim 64 (shorter rows:
+// more keys per step keep the bytes in flight per wave up).
 #include <type_traits>
 
 #include "common.hpp"
