@@ -65,7 +65,6 @@ pa_status fail(pa_status st, const char* fmt, ...) {
 
 constexpr int kMaxCus = 256;
 constexpr int kMinStepsDefault = 8;
-constexpr int kBlockM = 128;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
 constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel
@@ -92,7 +91,7 @@ pa_status check_config(const pa_config* c) {
     return fail(PA_ERR_INVALID_ARG, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)",
                 c->num_q_heads, c->num_kv_heads);
   const int G = c->num_q_heads / c->num_kv_heads;
-  if (G > 16 || (kBlockM % G) != 0)
+  if (G > 16 || (128 % G) != 0)
     return fail(PA_ERR_UNSUPPORTED, "query heads per kv head must be 1, 2, 4, 8 or 16 (got %d)", G);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
@@ -116,6 +115,8 @@ int64_t prefill_items(int64_t T, int64_t S, int64_t bq) { return cdiv(T, bq) + s
 int decode_step_keys(const pa_config& c) {
   return pa::decode_step_keys(c.head_dim, c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2);
 }
+
+int block_m(const pa_config& c) { return pa::prefill_block_m(c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2); }
 
 int decode_workers(int cus) { return std::min(std::max(cus, 1), kMaxCus) * pa::kDecodeWaves; }
 
@@ -169,8 +170,8 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   p->decode_waves = pa::kDecodeWaves;
   p->decode_workers = decode_workers(cus);
   p->decode_min_steps = tun.decode_min_steps;
-  p->block_m = kBlockM;
-  p->block_q = kBlockM / G;
+  p->block_m = block_m(c);
+  p->block_q = block_m(c) / G;
   p->prefill_tile = kPrefillTile;
   int64_t items = 0;
   if (S >= 1 && T >= 1 && max_len >= 1) {
@@ -353,7 +354,7 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   // largest on the largest device, so that batch and device bound all.
   uint64_t best = kHeader;
   if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
-    const int64_t bq = kBlockM / (cfg->num_q_heads / cfg->num_kv_heads);
+    const int64_t bq = block_m(*cfg) / (cfg->num_q_heads / cfg->num_kv_heads);
     const int64_t items = max_tokens >= 2 ? prefill_items(max_tokens, max_seqs, bq) : 0;
     best = ws_layout(*cfg, decode_workers(kMaxCus), max_seqs, items).total;
   }

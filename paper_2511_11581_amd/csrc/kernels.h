@@ -6,7 +6,16 @@
 
 namespace pa {
 
-constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernel
+constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernels
+// Q-block kernels: bf16 caches use 8 waves x 32 rows (BLOCK_M = 256, two
+// waves per SIMD working in alternating phases) with tiles loaded straight
+// into LDS; fp8 caches 4 waves x 32 rows (BLOCK_M = 128) with tiles
+// converted to bf16 on their way into LDS.
+constexpr int kQblockWaves = 8;
+constexpr int kQblockWaveRows = 32;
+__host__ __device__ constexpr int prefill_block_m(int elem_bytes) {
+  return elem_bytes == 1 ? 128 : kQblockWaveRows * kQblockWaves;
+}
 // Decode workgroup: 4 waves, one workgroup per CU (its LDS use keeps a
 // second one out), so one wave per SIMD.  With two waves on a SIMD the
 // memory system serves the first wave slot first and the second finishes
@@ -122,6 +131,7 @@ hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPl
                        bool with_prefill, hipStream_t st);
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st);
+hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t st);
 

@@ -335,18 +335,13 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st) {
+  if (!fp8) return launch_qblock(a, p, head_dim, st);
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   dim3 grid((unsigned)blocks), block(kThreads);
-  if (head_dim == 128) {
-    if (fp8) prefill_kernel<128, true><<<grid, block, 0, st>>>(a, p);
-    else prefill_kernel<128, false><<<grid, block, 0, st>>>(a, p);
-  } else if (head_dim == 64) {
-    if (fp8) prefill_kernel<64, true><<<grid, block, 0, st>>>(a, p);
-    else prefill_kernel<64, false><<<grid, block, 0, st>>>(a, p);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  if (head_dim == 128) prefill_kernel<128, true><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64) prefill_kernel<64, true><<<grid, block, 0, st>>>(a, p);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

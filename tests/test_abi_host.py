@@ -170,11 +170,13 @@ def test_plan_decode_grid_is_static():
 def test_plan_prefill_grid_bounds_the_q_blocks():
     p = plan(cfg(), cus=256, T=6589, S=4, MB=188)
     assert p["prefill_launch"] == 1
-    assert p["block_m"] == 128 and p["block_q"] == 32
+    assert p["block_m"] == 256 and p["block_q"] == 64   # bf16 caches: 8 waves x 32 rows
     # sum ceil(q_i / BLOCK_Q) <= ceil(T / BLOCK_Q) + S
     qs = [2048, 1024, 3000, 517]
-    need = sum(-(-q // 32) for q in qs)
+    need = sum(-(-q // 64) for q in qs)
     assert p["prefill_grid"][0] >= need * 8
+    pf = plan(cfg(32, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3), cus=256, T=6589, S=4, MB=188)
+    assert pf["block_m"] == 128 and pf["block_q"] == 32
     p1 = plan(cfg(), T=1, S=1, MB=4)
     assert p1["prefill_launch"] == 0
 
