@@ -116,19 +116,24 @@ typedef struct pa_profile {
  *
  * Decode work (rows with one query token) is split as the parallel tiled
  * softmax of Sec. 4.5, with the segment boundaries chosen for a static
- * launch grid (Sec. 4.7): the (sequence, kv head) pairs of the batch, each
- * ceil(L / decode_step) steps long, are laid end to end and the resulting
- * step range is cut into equal contiguous shares, one per worker (a wave);
- * the part of one pair inside one share is a segment ("piece").  The device
- * activates min(decode_workers, ceil(total steps / decode_min_steps))
- * workers, so a single pair of 32 steps with decode_min_steps = 8 is cut
- * into 4 segments of 8 steps (the example of Fig. 4). */
+ * launch grid (Sec. 4.7).  The kv heads are grouped in units of
+ * decode_unit_heads (HU) adjacent heads, so that a unit's cache rows of one
+ * token form a run of at least 256 bytes; the (sequence, unit) pairs of the
+ * batch, each ceil(L / decode_step) steps long, are laid end to end and the
+ * resulting step range is cut into equal contiguous shares, one per worker
+ * group of HU waves, wave i of a group taking kv head HU u + i of every unit
+ * u in its share.  The part of one (sequence, kv head) pair inside one
+ * share is a segment ("piece").  The device activates
+ * min(decode_workers / HU, ceil(total steps / decode_min_steps)) groups, so
+ * a single pair of 32 steps with decode_min_steps = 8 is cut into 4
+ * segments of 8 steps (the example of Fig. 4). */
 typedef struct pa_plan_info {
   int32_t decode_launch;     /* 1 if the decode kernels are launched */
   int32_t decode_step;       /* keys per decode step (32, 64 or 128) */
   int32_t decode_waves;      /* waves per decode workgroup */
   int32_t decode_workers;    /* waves in the static decode grid */
-  int32_t decode_min_steps;  /* fewest steps per active worker, batch permitting */
+  int32_t decode_min_steps;  /* fewest steps per active worker group, batch permitting */
+  int32_t decode_unit_heads; /* kv heads per decode unit (HU, see above) */
   int32_t merge_launch;      /* 1 if the log-sum-exp merge kernel is launched */
   int32_t prefill_launch;    /* 1 if the Q-block (q_len >= 2) kernel is launched */
   int32_t block_m;           /* rows per Q-block (BLOCK_M, Sec. 4.4) */

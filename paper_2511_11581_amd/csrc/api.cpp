@@ -112,24 +112,37 @@ pa_status check_config(const pa_config* c) {
 // Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) + (#sequences with q_i >= 2).
 int64_t prefill_items(int64_t T, int64_t S, int64_t bq) { return cdiv(T, bq) + std::min<int64_t>(S, T / 2); }
 
+int decode_unit_heads(const pa_config& c);
 int decode_step_keys(const pa_config& c) {
-  return pa::decode_step_keys(c.head_dim, c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2);
+  const int eb = c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2;
+  return pa::decode_step_keys(decode_unit_heads(c) * c.head_dim * eb, eb);
 }
 
 int block_m(const pa_config& c) { return pa::prefill_block_m(c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2); }
 
 int decode_workers(int cus) { return std::min(std::max(cus, 1), kMaxCus) * pa::kDecodeWaves; }
 
+// kv heads one decode worker computes together: the most adjacent heads (a
+// power of two dividing Hkv) whose rows of one token stay within 256 bytes,
+// so that the worker's reads per token form one run of 256 bytes when rows
+// are shorter.
+int decode_unit_heads(const pa_config& c) {
+  const int row = c.head_dim * (c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2);
+  int hu = 1;
+  while (hu * 2 * row <= 256 && c.num_kv_heads % (hu * 2) == 0) hu *= 2;
+  return hu;
+}
+
 // Workspace layout: validation header, decode-list counters, decode list
-// [S + 1] int4, piece partials [workers, 2, G, d] and [workers, 2, G, 2]
-// fp32, then the Q-block work list (seq_start [S + 1], list_seq, list_qb,
-// count).
+// [S + 1] int4, piece partials [workers, 2, HU, G, d] and
+// [workers, 2, HU, G, 2] fp32, then the Q-block work list (seq_start
+// [S + 1], list_seq, list_qb, count).
 struct WsLayout {
   uint64_t meta, dec, part_o, part_ml, seq_start, list_seq, list_qb, count, total;
 };
 
 WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
-  const int G = c.num_q_heads / c.num_kv_heads;
+  const int G = c.num_q_heads / c.num_kv_heads * decode_unit_heads(c);   // partial rows per slot
   WsLayout l;
   uint64_t off = kHeader;
   l.meta = off;
@@ -170,6 +183,7 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   p->decode_waves = pa::kDecodeWaves;
   p->decode_workers = decode_workers(cus);
   p->decode_min_steps = tun.decode_min_steps;
+  p->decode_unit_heads = decode_unit_heads(c);
   p->block_m = block_m(c);
   p->block_q = block_m(c) / G;
   p->prefill_tile = kPrefillTile;
@@ -388,7 +402,7 @@ pa_status pa_decode_pieces(const pa_handle* h, const pa_config* cfg, int32_t num
   if (cap > 0 && !pieces) return fail(PA_ERR_INVALID_ARG, "pieces is NULL");
   const int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
   const pa_tunables tun = h ? h->tun : tunables_from_env();
-  const int KS = decode_step_keys(*c), Hkv = c->num_kv_heads;
+  const int KS = decode_step_keys(*c), HU = decode_unit_heads(*c), Hu = c->num_kv_heads / HU;
   const int64_t cap_keys = max_blocks_per_seq * c->block_size;
   // The decode list, as the plan kernel builds it.
   struct Dec { int32_t s, L; int64_t P; };
@@ -401,30 +415,31 @@ pa_status pa_decode_pieces(const pa_handle* h, const pa_config* cfg, int32_t num
       P += cdiv(L, KS);
     }
   }
-  const int64_t total = (int64_t)Hkv * P;
+  const int64_t total = (int64_t)Hu * P;
   const int W = pa::active_workers(total, tun.decode_min_steps, decode_workers(cus));
-  // Walk every worker's range of the tile space, pair by pair.
+  // Walk every worker's range of the unit step space, unit by unit; a unit
+  // piece is one piece per head of the unit.
   int64_t n = 0;
   size_t j = 0;
   for (int w = 0; w < W; ++w) {
     int64_t t = pa::worker_begin(w, total, W);
     const int64_t te = pa::worker_begin(w + 1, total, W);
     while (t < te) {
-      while (j + 1 < dec.size() && (int64_t)Hkv * dec[j + 1].P <= t) ++j;
+      while (j + 1 < dec.size() && (int64_t)Hu * dec[j + 1].P <= t) ++j;
       const int64_t nt = cdiv(dec[j].L, KS);
-      const int64_t off = t - (int64_t)Hkv * dec[j].P;
-      const int64_t g = off / nt, k0 = off % nt, k1 = std::min(nt, k0 + (te - t));
+      const int64_t off = t - (int64_t)Hu * dec[j].P;
+      const int64_t gu = off / nt, k0 = off % nt, k1 = std::min(nt, k0 + (te - t));
       const bool head = k0 > 0, tail = k1 < nt;
-      if (n < cap) {
+      for (int hu = 0; hu < HU; ++hu, ++n) {
+        if (n >= cap) continue;
         pa_decode_piece& pc = pieces[n];
         pc.seq = dec[j].s;
-        pc.kv_head = (int32_t)g;
+        pc.kv_head = (int32_t)(gu * HU + hu);
         pc.worker = w;
         pc.first_key = (int32_t)(k0 * KS);
         pc.end_key = (int32_t)std::min<int64_t>(k1 * KS, dec[j].L);
         pc.slot = (!head && !tail) ? -1 : (head ? 0 : 1);
       }
-      ++n;
       t += k1 - k0;
     }
   }
@@ -569,6 +584,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   dp.workers = p.decode_workers;
   dp.step_keys = p.decode_step;
   dp.min_steps = p.decode_min_steps;
+  dp.unit_heads = p.decode_unit_heads;
   dp.meta = reinterpret_cast<int32_t*>(ws + wl.meta);
   dp.dec = reinterpret_cast<int4*>(ws + wl.dec);
   dp.part_o = reinterpret_cast<float*>(ws + wl.part_o);

@@ -5,19 +5,25 @@
 //
 // Only sequences whose query length is 1 are handled here.  The plan kernel
 // lists them (j = 0..J-1) with the prefix P(j) of their step counts
-// nt(j) = ceil(L_j / KS) (KS keys per step).  The (sequence, kv head) pairs,
-// sequence-major, lay out a tile space of Hkv * P(J) steps: pair (j, g)
-// occupies [Hkv P(j) + g nt(j), + nt(j)).  Worker w of the W active workers
-// (one wave each, launched as a fixed grid of 4-wave workgroups, one per CU)
-// takes the contiguous range [worker_begin(w), worker_begin(w + 1)) of that space, so
-// every worker streams the same number of K/V bytes whatever the lengths.
-// The part of one pair inside one worker is a piece, i.e. a segment of the
-// parallel tiled softmax: a piece covering its whole pair writes bf16
-// output; a piece cut at the worker's start (head) or end (tail) stores its
-// unnormalised partials (acc, m, l), and merge_kernel combines the pieces
-// of every pair that spans several workers.  A worker has at most one head
-// and one tail piece, so partial slot (w, 0) holds the head piece and
-// (w, 1) a tail-only piece.
+// nt(j) = ceil(L_j / KS) (KS keys per step).  The kv heads are taken in
+// units of HU adjacent heads (HU = 1 for 256-byte cache rows, 2 for 128-byte
+// rows, 4 for 64-byte rows, as Hkv allows) that one wave computes together,
+// so that its loads of one token cover a contiguous run of 256 bytes: HBM
+// serves 128-byte rows at a 1 KB stride at little more than half the rate
+// of 256-byte runs, even when two waves read the two halves at the same
+// time.  The (sequence, unit) pairs, sequence-major, lay out a space of
+// (Hkv / HU) P(J) steps: pair (j, gu) occupies
+// [(Hkv / HU) P(j) + gu nt(j), + nt(j)).  Worker w of the W active workers
+// (one wave each, launched as a fixed grid of 4-wave workgroups, one per
+// CU) takes the contiguous range [worker_begin(w), worker_begin(w + 1)) of
+// that space, so every worker streams the same number of K/V bytes
+// whatever the lengths.  The part of one (sequence, kv head) pair inside one
+// worker is a piece, i.e. a segment of the parallel tiled softmax: a piece
+// covering its whole pair writes bf16 output; a piece cut at the worker's
+// start (head) or end (tail) stores its unnormalised partials (acc, m, l),
+// and merge_kernel combines the pieces of every pair that spans several
+// workers.  A worker has at most one head and one tail unit piece, so
+// partial slot (w, 0) holds the head pieces and (w, 1) tail-only pieces.
 //
 // Per wave and step: the G query heads of kv head g are the columns of one
 // 16-wide MFMA tile, so every K/V row is read from HBM once.  K and V rows
@@ -72,32 +78,37 @@ __device__ __forceinline__ uint32_t dw(const typename LoadT<LB>::T& v, int i) {
 
 __device__ __forceinline__ int lane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
-// A contiguous range of steps of one (sequence, kv head) pair (wave-uniform).
+// A contiguous range of steps of one (sequence, unit) pair (wave-uniform).
 struct Piece {
-  int j, s, t0, L, g;  // decode-list index, sequence, token row, length, kv head
+  int j, s, t0, L, g;  // decode-list index, sequence, token row, length, first kv head
+  int gu;              // unit (its heads are g = HU gu .. HU gu + HU - 1)
   int k0, k1;          // steps [k0, k1) of the pair
   int head, tail;      // the pair starts before / continues after this worker
 };
 
-template <int D, bool FP8>
+template <int D, bool FP8, int HU>
 __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs a, DecodePlan p) {
   constexpr int EB = FP8 ? 1 : 2;          // bytes per cached element
-  constexpr int LB = D * EB / 16;          // bytes one lane loads per row
+  constexpr int UB = HU * D * EB;          // bytes of one token's unit row (HU heads)
+  constexpr int LB = UB / 16;              // bytes one lane loads per unit row
+  constexpr int LPH = 16 / HU;             // lanes per head row
   constexpr int DPL = LB / EB;             // d values one lane loads per row
-  constexpr int PSH = DPL == 8 ? 3 : 2;    // log2(DPL)
+  constexpr int PSH = DPL == 16 ? 4 : (DPL == 8 ? 3 : 2);   // log2(DPL)
   constexpr int NW = DPL / 2;              // bf16 dwords per lane per row
   constexpr int NSTEP = D / 32;            // MFMA k-steps over d
   constexpr int NDB = D / 16;              // 16-row d blocks of O^T
   constexpr int KRB = 2 * D + 32;          // LDS bytes per K row (bf16 + pad)
   constexpr int KT = kSub * KRB;           // K sub-tile bytes
   constexpr int VT = 16 * (4 * D + 4 * (D >> PSH));  // V^T sub-tile bytes
-  constexpr int WB = KT + VT;              // LDS bytes per wave
-  constexpr int NSUB = decode_subtiles(D, EB);  // sub-tiles per step
+  constexpr int HT = KT + VT;              // LDS bytes per head of the unit
+  constexpr int WB = HU * HT;              // LDS bytes per wave
+  constexpr int NSUB = decode_subtiles(UB, EB);  // sub-tiles per step
   constexpr int KS = kSub * NSUB;          // keys per step
   constexpr int R = 8 * NSUB;              // rows one lane loads per step (K and V each)
   constexpr int BPS = KS / 16;             // 16-key blocks per step
   typedef typename LoadT<LB>::T LT;
-  static_assert(DPL == 8 || DPL == 4, "head_dim 64 or 128");
+  static_assert(DPL == 16 || DPL == 8 || DPL == 4, "head_dim 64 or 128");
+  static_assert(LPH * DPL == D, "lanes of one head row cover it");
   constexpr int NWIN = 4;                  // block-id registers per lane (window of 64 NWIN blocks)
   static_assert(64 % BPS == 0, "steps must not straddle block-id registers");
 
@@ -109,23 +120,25 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
   const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
   const int lq = lane & 3, lc = lane >> 2;     // loading coordinates
+  const int hl = lc / LPH, ci = lc % LPH;      // head of the unit and chunk of its row this lane loads
   const int Hkv = a.num_kv_heads, G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
 
   const int J = p.meta[0], Wn = p.meta[1];
   const int w = blockIdx.x * kDecodeWaves + wave;
+  const int Hu = Hkv / HU;                     // units per sequence
   if (w >= Wn || J <= 0) return;
-  const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
+  const int64_t Ttot = (int64_t)Hu * p.dec[J].w;
   int64_t t = worker_begin(w, Ttot, Wn);
   const int64_t t_end = worker_begin(w + 1, Ttot, Wn);
   if (t >= t_end) return;
 
-  // ---- first pair: largest j with Hkv * P(j) <= t, by a 64-ary search; the
+  // ---- first unit: largest j with Hu * P(j) <= t, by a 64-ary search; the
   //      wave then holds entries base .. base + 63 of the list, one per lane.
   int lo = 0, hi = J;
   while (hi - lo > 63) {
     const int step = (hi - lo + 63) / 64;
     const int idx = lo + lane * step;
-    const int64_t P = (int64_t)Hkv * p.dec[min(idx, J)].w;
+    const int64_t P = (int64_t)Hu * p.dec[min(idx, J)].w;
     const bool ok = idx < hi && P <= t;
     lo += (63 - __builtin_clzll(__ballot(ok))) * step;
     hi = min(hi, lo + step);
@@ -133,7 +146,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   int base = lo;
   int4 ent = p.dec[min(base + lane, J)];
   {
-    const bool ok = base + lane < hi && (int64_t)Hkv * ent.w <= t;
+    const bool ok = base + lane < hi && (int64_t)Hu * ent.w <= t;
     lo = base + (63 - __builtin_clzll(__ballot(ok)));
   }
   // Entry jj of the list (jj + 1 - base <= 63 must hold): fields by readlane.
@@ -152,31 +165,36 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
 #pragma unroll
     for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(((first + 64 * i + lane) * 16) >> bsl, a.mb - 1)];
   };
-  auto make_piece = [&](int jj, int g, int k0, int64_t budget) {
+  auto make_piece = [&](int jj, int gu, int k0, int64_t budget) {
     if (jj + 1 - base > 63) reload(jj);
     Piece pc;
     jj = uniform(jj);
     pc.j = jj;
+    pc.gu = uniform(gu);
     pc.s = lane_i(ent.x, jj - base);
     pc.t0 = lane_i(ent.y, jj - base);
     pc.L = min(lane_i(ent.z, jj - base), a.mb * a.block_size);
     const int nt = lane_i(ent.w, jj + 1 - base) - lane_i(ent.w, jj - base);
-    pc.g = uniform(g);
+    pc.g = uniform(gu * HU);
     pc.k0 = uniform(k0);
     pc.k1 = uniform((int)min((int64_t)nt, (int64_t)k0 + budget));
     pc.head = pc.k0 > 0;
     pc.tail = pc.k1 < nt;
     return pc;
   };
-  // Q^T of a piece as MFMA B operands: column c16 = head g*G + c16 (zero if
-  // c16 >= G), k-step st covers d = 32 st + 8 q4 + j.
-  auto load_q = [&](const Piece& pc, bf16x8 (&qt)[NSTEP]) {
+  // Q^T of a piece as MFMA B operands, per head hu of the unit: column c16
+  // = query head (g + hu) G + c16 (zero if c16 >= G), k-step st covers
+  // d = 32 st + 8 q4 + j.
+  auto load_q = [&](const Piece& pc, bf16x8 (&qt)[HU][NSTEP]) {
     const bool hv = c16 < G;
-    const uint8_t* qrow = a.q + (int64_t)pc.t0 * a.q_tok + (int64_t)(pc.g * G + (hv ? c16 : 0)) * a.q_head;
 #pragma unroll
-    for (int st = 0; st < NSTEP; ++st) {
-      u32x4 v = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
-      qt[st] = __builtin_bit_cast(bf16x8, v);
+    for (int hu = 0; hu < HU; ++hu) {
+      const uint8_t* qrow = a.q + (int64_t)pc.t0 * a.q_tok + (int64_t)((pc.g + hu) * G + (hv ? c16 : 0)) * a.q_head;
+#pragma unroll
+      for (int st = 0; st < NSTEP; ++st) {
+        u32x4 v = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
+        qt[hu][st] = __builtin_bit_cast(bf16x8, v);
+      }
     }
   };
 
@@ -184,26 +202,34 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   {
     const int64_t Pj = lane_i(ent.w, lo - base);
     const int nt = lane_i(ent.w, lo + 1 - base) - (int)Pj;
-    const int64_t off = t - (int64_t)Hkv * Pj;
+    const int64_t off = t - (int64_t)Hu * Pj;
     cur = make_piece(lo, (int)(off / nt), (int)(off % nt), t_end - t);
   }
-  bf16x8 qc[NSTEP];
+  bf16x8 qc[HU][NSTEP];
   int win[NWIN];
   int cb = 0;   // first 16-key block of the window held in win
 
-  float m_run = kNegInf, l_run = 0.f;
-  f32x4 o[NDB];
+  float m_run[HU], l_run[HU];
+  f32x4 o[HU][NDB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) o[db] = f32x4{0, 0, 0, 0};
-  uint8_t* kl = lds + wave * WB;
-  uint8_t* vt = kl + KT;
+  for (int hu = 0; hu < HU; ++hu) {
+    m_run[hu] = kNegInf;
+    l_run[hu] = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[hu][db] = f32x4{0, 0, 0, 0};
+  }
+  // Per head of the unit: a K tile (natural rows) and a V^T tile.
+  uint8_t* const wl = lds + wave * WB;
+  auto kl = [&](int hu) { return wl + hu * HT; };
+  auto vt = [&](int hu) { return wl + hu * HT + KT; };
 
   // Issue the K/V loads of step k of a pair (kv head g, block cache `cache`
   // starting at 16-key block cb); live = 0 issues harmless loads of one row.
   // Addresses: a wave-uniform (scalar) base per 4-row group and a fixed
-  // 32-bit per-lane offset (row lq of the group, byte lc * LB of the row).
-  const uint32_t koff = (uint32_t)(lq * a.kg.slot + lc * LB);
-  const uint32_t voff = (uint32_t)(lq * a.vg.slot + lc * LB);
+  // 32-bit per-lane offset (row lq of the group, head hl of the unit, chunk
+  // ci of that head's row).
+  const uint32_t koff = (uint32_t)(lq * a.kg.slot + hl * a.kg.head + ci * LB);
+  const uint32_t voff = (uint32_t)(lq * a.vg.slot + hl * a.vg.head + ci * LB);
   // Issue the K (or V) loads of step k of the current piece (block ids from
   // the window registers; refill() must have made the step's blocks resident).
   auto issue = [&](const uint8_t* base, const KvGeom& geo, uint32_t off, int k, LT (&rows)[R]) {
@@ -238,72 +264,93 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   };
   // Scores and online-softmax update for step k of the current piece; the
   // probabilities P^T of sub-tile u (as MFMA B operands) go to pt[u].
-  auto consume_k = [&](int k, LT (&kr)[R], bf16x8 (&pt)[NSUB]) {
-    f32x4 sacc[NSUB][2];
+  auto consume_k = [&](int k, LT (&kr)[R], bf16x8 (&pt)[HU][NSUB]) {
+    f32x4 sacc[HU][NSUB][2];
 #pragma unroll
     for (int u = 0; u < NSUB; ++u) {
-      // ---- K rows -> LDS (bf16, natural layout)
+      // ---- K rows -> LDS (bf16, natural layout), into the tile of head hl
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
         uint32_t wd[NW];
         to_bf16(kr[8 * u + r], wd);
-        uint8_t* dst = kl + (4 * r + lq) * KRB + lc * (2 * DPL);
-        if constexpr (NW == 4) *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
-        else *(u32x2*)dst = u32x2{wd[0], wd[1]};
+        uint8_t* dst = kl(hl) + (4 * r + lq) * KRB + ci * (2 * DPL);
+        if constexpr (NW == 8) {
+          *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
+          *(u32x4*)(dst + 16) = u32x4{wd[4], wd[5], wd[6], wd[7]};
+        } else if constexpr (NW == 4) {
+          *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
+        } else {
+          *(u32x2*)dst = u32x2{wd[0], wd[1]};
+        }
       }
-      // ---- S^T = K Q^T; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
+      // ---- S^T = K Q^T per head; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x4 acc = {0, 0, 0, 0};
-        const uint8_t* kp = kl + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
+      for (int hu = 0; hu < HU; ++hu)
 #pragma unroll
-        for (int st = 0; st < NSTEP; ++st)
-          acc = mfma16(*(const bf16x8*)(kp + 64 * st), qc[st], acc);
-        sacc[u][kb] = acc;
-      }
+        for (int kb = 0; kb < 2; ++kb) {
+          f32x4 acc = {0, 0, 0, 0};
+          const uint8_t* kp = kl(hu) + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
+#pragma unroll
+          for (int st = 0; st < NSTEP; ++st)
+            acc = mfma16(*(const bf16x8*)(kp + 64 * st), qc[hu][st], acc);
+          sacc[hu][u][kb] = acc;
+        }
     }
     // ---- online softmax (log2 domain); lane holds keys 32u + 16kb + q4 + 4r of head c16
     const int kend = uniform(cur.L - k * KS);   // keys of this step inside the sequence
     if (kend < KS) {   // last step of the pair: mask keys >= L (compare with immediates)
       const int lim = kend - q4;
 #pragma unroll
+      for (int hu = 0; hu < HU; ++hu)
+#pragma unroll
+        for (int u = 0; u < NSUB; ++u)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              sacc[hu][u][kb][r] = kSub * u + 16 * kb + 4 * r < lim ? sacc[hu][u][kb][r] : kNegInf;
+    }
+#pragma unroll
+    for (int hu = 0; hu < HU; ++hu) {
+      float mx = kNegInf;
+#pragma unroll
       for (int u = 0; u < NSUB; ++u)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            sacc[u][kb][r] = kSub * u + 16 * kb + 4 * r < lim ? sacc[u][kb][r] : kNegInf;
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[hu][u][kb][r]);
+      mx = xor16_max(mx);
+      mx = xor32_max(mx) * a.sl2;
+      // The reference max m_run is only raised when some query head's step
+      // max exceeds it by more than 8 (log2 units): the weights then stay
+      // below 2^8, and l, O and the stored partials all use the same
+      // reference, so the result is unchanged while O is rescaled on few
+      // steps only.
+      if (__ballot(mx > m_run[hu] + 8.f)) {
+        const float m_new = fmaxf(m_run[hu], mx);
+        const float alpha = fast_exp2(m_run[hu] - m_new);
+        m_run[hu] = m_new;
+        l_run[hu] *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[hu][db] *= alpha;
+      }
+      float psum = 0.f;
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        float x[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[kb][r] = fast_exp2(__builtin_fmaf(sacc[hu][u][kb][r], a.sl2, -m_run[hu]));
+            psum += x[kb][r];
+          }
+        const u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
+                          pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
+        pt[hu][u] = __builtin_bit_cast(bf16x8, pw);
+      }
+      l_run[hu] += psum;
     }
-    float mx = kNegInf;
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[u][kb][r]);
-    mx = xor16_max(mx);
-    mx = xor32_max(mx) * a.sl2;
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = fast_exp2(m_run - m_new);
-    float psum = 0.f;
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      float x[2][4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          x[kb][r] = fast_exp2(__builtin_fmaf(sacc[u][kb][r], a.sl2, -m_new));
-          psum += x[kb][r];
-        }
-      const u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
-                        pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
-      pt[u] = __builtin_bit_cast(bf16x8, pw);
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db] *= alpha;
   };
   // V^T column group of sub-tile u for d value e of this lane's chunk: the
   // bf16 pairs (row 2jj, row 2jj + 1) for jj = 0..3, taken straight from the
@@ -339,7 +386,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
     return col;
   };
   // O^T += V^T P^T for step k of the current piece.
-  auto consume_v = [&](int k, LT (&vr)[R], const bf16x8 (&pt)[NSUB]) {
+  auto consume_v = [&](int k, LT (&vr)[R], const bf16x8 (&pt)[HU][NSUB]) {
     const int kend = uniform(cur.L - k * KS);
     const int lim = kend - lq;
 #pragma unroll
@@ -349,45 +396,52 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
       if (kend < KS) {
 #pragma unroll
         for (int e = 0; e < DPL; ++e)
-          *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = vt_col(vr, u, e, lim, std::true_type{});
+          *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::true_type{});
       } else {
 #pragma unroll
         for (int e = 0; e < DPL; ++e)
-          *(u32x4*)(vt + vt_off<PSH>(lc * DPL + e, lq)) = vt_col(vr, u, e, lim, std::false_type{});
+          *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::false_type{});
       }
-      // ---- O^T += V^T P^T
+      // ---- O^T += V^T P^T per head
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const u32x4 va = *(const u32x4*)(vt + vt_off<PSH>(16 * db + c16, q4));
-        o[db] = mfma16(__builtin_bit_cast(bf16x8, va), pt[u], o[db]);
-      }
-    }
-  };
-  // End of a piece: bf16 output if the piece is its whole pair, else partials.
-  auto finalize = [&]() {
-    float l_tot = xor16_sum(l_run);
-    l_tot = xor32_sum(l_tot);
-    if (c16 < G) {
-      if (!cur.head && !cur.tail) {
-        const float inv = a.v_scale / l_tot;
-        uint8_t* orow = a.out + (int64_t)cur.t0 * a.o_tok + (int64_t)(cur.g * G + c16) * a.o_head;
+      for (int hu = 0; hu < HU; ++hu)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const u32x2 v2 = {pack_bf16(o[db][0] * inv, o[db][1] * inv), pack_bf16(o[db][2] * inv, o[db][3] * inv)};
-          *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
+          const u32x4 va = *(const u32x4*)(vt(hu) + vt_off<PSH>(16 * db + c16, q4));
+          o[hu][db] = mfma16(__builtin_bit_cast(bf16x8, va), pt[hu][u], o[hu][db]);
         }
-      } else {
-        const int64_t row = ((int64_t)w * 2 + (cur.head ? 0 : 1)) * G + c16;
-        float* po = p.part_o + row * D;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[db];
-        if (q4 == 0) *(f32x2*)(p.part_ml + row * 2) = f32x2{m_run, l_tot};
-      }
     }
-    m_run = kNegInf;
-    l_run = 0.f;
+  };
+  // End of a piece: bf16 output if the piece is its whole pair, else
+  // partials (rows [wave, slot, head of the unit, query head]).
+  auto finalize = [&]() {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db] = f32x4{0, 0, 0, 0};
+    for (int hu = 0; hu < HU; ++hu) {
+      float l_tot = xor16_sum(l_run[hu]);
+      l_tot = xor32_sum(l_tot);
+      if (c16 < G) {
+        if (!cur.head && !cur.tail) {
+          const float inv = a.v_scale / l_tot;
+          uint8_t* orow = a.out + (int64_t)cur.t0 * a.o_tok + (int64_t)((cur.g + hu) * G + c16) * a.o_head;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const u32x2 v2 = {pack_bf16(o[hu][db][0] * inv, o[hu][db][1] * inv),
+                              pack_bf16(o[hu][db][2] * inv, o[hu][db][3] * inv)};
+            *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
+          }
+        } else {
+          const int64_t row = (((int64_t)w * 2 + (cur.head ? 0 : 1)) * HU + hu) * G + c16;
+          float* po = p.part_o + row * D;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[hu][db];
+          if (q4 == 0) *(f32x2*)(p.part_ml + row * 2) = f32x2{m_run[hu], l_tot};
+        }
+      }
+      m_run[hu] = kNegInf;
+      l_run[hu] = 0.f;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[hu][db] = f32x4{0, 0, 0, 0};
+    }
   };
 
   // Software pipeline over the worker's steps (two register sets, loop
@@ -415,7 +469,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   // sched_barrier keeps the compiler from hoisting consumers above the loads.
   LT krA[R], vrA[R], krB[R], vrB[R];
   auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&kz)[R], LT (&vz)[R]) {
-    bf16x8 pt[NSUB];
+    bf16x8 pt[HU][NSUB];
     if (more) {
       refill(k + 1);
       issue(a.k, a.kg, koff, k + 1, kz);
@@ -451,9 +505,9 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
     finalize();
     t += cur.k1 - cur.k0;
     if (t >= t_end) break;
-    const int jj = cur.g + 1 < Hkv ? cur.j : cur.j + 1;
-    const int g = cur.g + 1 < Hkv ? cur.g + 1 : 0;
-    cur = make_piece(jj, g, 0, t_end - t);
+    const int jj = cur.gu + 1 < Hu ? cur.j : cur.j + 1;
+    const int gu = cur.gu + 1 < Hu ? cur.gu + 1 : 0;
+    cur = make_piece(jj, gu, 0, t_end - t);
   }
 }
 
@@ -472,15 +526,17 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
   const int g = blockIdx.z;
   const int J = p.meta[0], Wn = p.meta[1];
   if (jj >= J || hh >= G) return;
-  const int Hkv = a.num_kv_heads;
+  const int HU = p.unit_heads, Hu = a.num_kv_heads / HU;
+  const int gu = g / HU, hu = g - gu * HU;
   const int4 e = p.dec[jj];
   const int nt = p.dec[jj + 1].w - e.w;
-  const int64_t Ttot = (int64_t)Hkv * p.dec[J].w;
-  const int64_t ta = (int64_t)Hkv * e.w + (int64_t)g * nt;
+  const int64_t Ttot = (int64_t)Hu * p.dec[J].w;
+  const int64_t ta = (int64_t)Hu * e.w + (int64_t)gu * nt;
   const int w0 = worker_of(ta, Ttot, Wn), w1 = worker_of(ta + nt - 1, Ttot, Wn);
   if (w0 == w1) return;
   const int n = w1 - w0 + 1;
-  auto row_of = [&](int k) { return ((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * G + hh; };
+  // piece k of the pair sits with wave w0 + k, head hu of its unit
+  auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
   float M = kNegInf;
   for (int k0 = 0; k0 < n; k0 += 64) {
     const int k = k0 + lane;
@@ -536,15 +592,16 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
                          hipStream_t st) {
   const dim3 grid((unsigned)((p.workers + kDecodeWaves - 1) / kDecodeWaves)), block(64 * kDecodeWaves);
-  if (head_dim == 128) {
-    if (fp8) decode_kernel<128, true><<<grid, block, 0, st>>>(a, p);
-    else decode_kernel<128, false><<<grid, block, 0, st>>>(a, p);
-  } else if (head_dim == 64) {
-    if (fp8) decode_kernel<64, true><<<grid, block, 0, st>>>(a, p);
-    else decode_kernel<64, false><<<grid, block, 0, st>>>(a, p);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  const int hu = p.unit_heads;
+  if (head_dim == 128 && !fp8 && hu == 1) decode_kernel<128, false, 1><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128 && fp8 && hu == 2) decode_kernel<128, true, 2><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128 && fp8 && hu == 1) decode_kernel<128, true, 1><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !fp8 && hu == 2) decode_kernel<64, false, 2><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !fp8 && hu == 1) decode_kernel<64, false, 1><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 4) decode_kernel<64, true, 4><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 2) decode_kernel<64, true, 2><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 1) decode_kernel<64, true, 1><<<grid, block, 0, st>>>(a, p);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

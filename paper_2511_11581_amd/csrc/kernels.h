@@ -54,21 +54,23 @@ struct DecodePlan {
   int32_t workers;     // decode waves in the static grid
   int32_t step_keys;   // keys per decode step (KS)
   int32_t min_steps;   // fewest steps per active worker when the batch allows
+  int32_t unit_heads;  // HU: adjacent kv heads one worker computes together
   int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
   int4* dec;           // [J + 1] {sequence, token row, length, prefix P(j) of step counts}
-  float* part_o;       // [workers, 2, G, head_dim] unnormalised piece results
-  float* part_ml;      // [workers, 2, G, 2] (max in log2 units, sum)
+  float* part_o;       // [workers, 2, HU, G, head_dim] unnormalised piece results
+  float* part_ml;      // [workers, 2, HU, G, 2] (max in log2 units, sum)
 };
 
-// Keys per decode step: one lane loads LB = head_dim * elem_bytes / 16 bytes
-// of 8 rows per 32-key sub-tile.  A step is one sub-tile; bf16 rows shorter
-// than 256 bytes and fp8 rows of 64 bytes take two, so that a step moves
-// 8-16 KB per wave within the register budget of the workgroup shape.
-__host__ __device__ constexpr int decode_subtiles(int head_dim, int elem_bytes) {
-  return head_dim * elem_bytes / 16 >= (elem_bytes == 1 ? 8 : 16) ? 1 : 2;
+// Keys per decode step, for units whose rows of one token are unit_bytes
+// long (HU heads x head_dim x elem_bytes): one lane loads unit_bytes / 16
+// bytes of 8 rows per 32-key sub-tile.  A step is one sub-tile when a lane
+// loads 16 bytes (or 8 bytes of fp8), else two, so that a step moves 8-16 KB
+// per wave within the register budget of the workgroup shape.
+__host__ __device__ constexpr int decode_subtiles(int unit_bytes, int elem_bytes) {
+  return unit_bytes / 16 >= (elem_bytes == 1 ? 8 : 16) ? 1 : 2;
 }
-__host__ __device__ constexpr int decode_step_keys(int head_dim, int elem_bytes) {
-  return 32 * decode_subtiles(head_dim, elem_bytes);
+__host__ __device__ constexpr int decode_step_keys(int unit_bytes, int elem_bytes) {
+  return 32 * decode_subtiles(unit_bytes, elem_bytes);
 }
 
 // Even split of the decode tile space (total steps over all (sequence, kv

@@ -5,8 +5,8 @@
 //
 // Decode list: the sequences with one query token, in batch order, with the
 // prefix P(j) of their step counts ceil(L_j / KS) and the number of decode
-// workers given work (every worker streams at least min_steps steps when the
-// batch has that many).
+// workers given work (every worker streams at least min_steps steps of its
+// units when the batch has that many).
 //
 // Q-block list: prefix sums of ceil(q_i / BLOCK_Q) over sequences with two or
 // more query tokens, and the list of (sequence, Q-block) items ordered by
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
   if (tid == 0) {
     dp.dec[njs] = make_int4(0, 0, 0, nsteps);
     dp.meta[0] = njs;
-    dp.meta[1] = active_workers((int64_t)a.num_kv_heads * nsteps, dp.min_steps, dp.workers);
+    dp.meta[1] = active_workers((int64_t)(a.num_kv_heads / dp.unit_heads) * nsteps, dp.min_steps, dp.workers);
     if (with_prefill) {
       pp.seq_start[S] = nqb;
       pp.count[0] = min(nqb, pp.work_items);

@@ -90,9 +90,12 @@ def test_plan_reproduces_the_papers_partition_example():
 
 def check_partition(c, cus, seq_lens, qsl, T, MB):
     """Every decode row's keys are covered once, in order, by pieces of
-    consecutive workers; the workers' step counts differ by at most one."""
+    consecutive workers; a worker computes the HU adjacent kv heads of a unit
+    together (the same keys for each); the workers' unit step counts differ
+    by at most one."""
     p = plan(c, cus=cus, T=T, S=len(seq_lens), MB=MB)
     KS = p["decode_step"]
+    HU = p["decode_unit_heads"]
     pcs = pa.pa_decode_pieces(None, c, cus, seq_lens, qsl, T, MB)
     cap = MB * c.block_size
     rows = {}
@@ -111,17 +114,26 @@ def check_partition(c, cus, seq_lens, qsl, T, MB):
             assert lst[0]["slot"] == -1
         else:
             assert lst[0]["slot"] == 1 and all(x["slot"] == 0 for x in lst[1:])
+    # unit pieces: HU consecutive entries, heads HU u .. HU u + HU - 1, same keys
+    assert len(pcs) % HU == 0
+    for i in range(0, len(pcs), HU):
+        grp = pcs[i:i + HU]
+        assert [x["kv_head"] for x in grp] == list(range(grp[0]["kv_head"], grp[0]["kv_head"] + HU))
+        assert grp[0]["kv_head"] % HU == 0
+        assert all((x["seq"], x["worker"], x["first_key"], x["end_key"], x["slot"]) ==
+                   (grp[0]["seq"], grp[0]["worker"], grp[0]["first_key"], grp[0]["end_key"], grp[0]["slot"])
+                   for x in grp)
     steps = {}
-    for x in pcs:
+    for x in pcs[::HU]:
         steps[x["worker"]] = steps.get(x["worker"], 0) + -(-(x["end_key"] - x["first_key"]) // KS)
         # a worker holds at most one piece per partial slot
-    for w in steps:
-        slots = [x["slot"] for x in pcs if x["worker"] == w and x["slot"] >= 0]
+    for w in steps:   # per unit piece (its HU heads share the slot, one row each)
+        slots = [x["slot"] for x in pcs[::HU] if x["worker"] == w and x["slot"] >= 0]
         assert len(slots) == len(set(slots))
     if steps:
         assert sorted(steps) == list(range(len(steps)))
         assert max(steps.values()) - min(steps.values()) <= 1
-        total = sum(steps.values())
+        total = sum(steps.values())   # steps of the unit space
         W = len(steps)
         assert W == min(p["decode_workers"], -(-total // p["decode_min_steps"]))
     return pcs
@@ -163,8 +175,31 @@ def test_plan_decode_grid_is_static():
     assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 4
     assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 32
     assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_workers"] == 256 * 4
-    assert plan(cfg(8, 2, 64))["decode_step"] == 64
-    assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 64  # 64-byte rows: two sub-tiles
+    assert plan(cfg(8, 2, 64))["decode_step"] == 32   # two heads per unit: 256-byte runs
+    assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 32  # two 64-byte heads per unit: 128-byte runs of fp8
+
+
+def test_decode_unit_heads_make_runs_of_256_bytes():
+    F8 = pa.PA_DTYPE_FP8_E4M3
+    assert plan(cfg(32, 8, 128))["decode_unit_heads"] == 1          # 256-byte bf16 rows
+    assert plan(cfg(64, 8, 128, 16, F8))["decode_unit_heads"] == 2  # 128-byte fp8 rows
+    assert plan(cfg(8, 2, 64))["decode_unit_heads"] == 2            # 128-byte bf16 rows
+    assert plan(cfg(32, 8, 64, 16, F8))["decode_unit_heads"] == 4   # 64-byte fp8 rows
+    assert plan(cfg(8, 2, 64, 16, F8))["decode_unit_heads"] == 2    # limited by Hkv
+    assert plan(cfg(8, 1, 128, 16, F8))["decode_unit_heads"] == 1
+    assert plan(cfg(12, 3, 128, 16, F8))["decode_unit_heads"] == 1  # Hkv odd
+
+
+@pytest.mark.parametrize("kv,d,hkv", [("fp8", 128, 8), ("bf16", 64, 2), ("fp8", 64, 8)])
+def test_decode_partition_with_head_units(kv, d, hkv):
+    g = torch.Generator().manual_seed(d + hkv)
+    S = 37
+    L = torch.randint(1, 3000, (S,), generator=g).tolist()
+    qsl = list(range(S + 1))
+    dt = pa.PA_DTYPE_FP8_E4M3 if kv == "fp8" else pa.PA_DTYPE_BF16
+    c = cfg(4 * hkv, hkv, d, 16, dt)
+    assert plan(c)["decode_unit_heads"] > 1
+    check_partition(c, 80, L, qsl, S, 200)
 
 
 def test_plan_prefill_grid_bounds_the_q_blocks():
