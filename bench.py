@@ -59,7 +59,7 @@ def prefill_flops(w):
 
 KERNEL_SOURCES = {
     "decode_kernel": ("decode.hip", "common.hpp", "kernels.h"),
-    "prefill_kernel": ("prefill.hip", "common.hpp", "kernels.h"),
+    "qblock_kernel": ("qblock.hip", "common.hpp", "kernels.h"),
 }
 
 
@@ -261,8 +261,8 @@ def main():
         achieved = prefill_flops(headline_w) / (dom_ms * 1e-3) / 1e12 if dom_ms else None
         roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / BF16_PEAK_TFLOPS if achieved else None,
-                "traffic": measured_traffic("prefill_kernel", h["name"]),
-                "kernel": "prefill_kernel", "kernel_us": dom_ms * 1e3}
+                "traffic": measured_traffic("qblock_kernel", h["name"]),
+                "kernel": "qblock_kernel", "kernel_us": dom_ms * 1e3}
 
     cpu = None
     if not args.no_cpu_baseline:
