@@ -361,9 +361,9 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 
   // ---- tile periods.  First half: group 0 matrix cores (tile t + 1 scores,
   //      tile t products), group 1 VALU (tile t weights); second half: the
-  //      reverse.  Loads of tile t + 3 go out after the first barrier, into
-  //      the stage of tile t - 1, which both groups finished in the
-  //      previous period.  The groups run separate loops with the same
+  //      reverse.  Loads of tile t + 3 go into the stage of tile t - 1,
+  //      which both groups finished in the previous period.  The groups run
+  //      separate loops with the same
   //      barriers (a barrier counts waves, not code addresses), so that
   //      neither loop merges the other's register state.
   auto sync = [&](int t) {
@@ -371,8 +371,11 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     if (t + 1 == ntiles - 1) zero_tail(t + 1);
     wait_vm_lds<2 * NLD>();
     __builtin_amdgcn_s_barrier();
-    issue(min(t + 3, ntiles - 1), (t + 3) & (kStages - 1));
   };
+  // Loads of tile t + 3 (into the stage of tile t - 1, free in period t).
+  // Each group issues them in its VALU half, next to the short softmax
+  // work, so that the issue stalls stay out of the matrix-core phases.
+  auto load_next = [&](int t) { issue(min(t + 3, ntiles - 1), (t + 3) & (kStages - 1)); };
   auto half = [&]() {
     __builtin_amdgcn_s_waitcnt(0xc07f);   // this half's LDS reads done (vmcnt untouched)
     __builtin_amdgcn_s_barrier();
@@ -389,24 +392,29 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       mfma_phase(t, kFull);
       half();
       valu_phase(t + 1);
+      load_next(t);
     }
     sync(t);
     mfma_phase(t, kPvOnly);
     half();
+    load_next(t);
   } else {
     for (; t + 1 < nact; ++t) {
       sync(t);
+      load_next(t);
       valu_phase(t);
       half();
       mfma_phase(t, kFull);
     }
     sync(t);
+    load_next(t);
     valu_phase(t);
     half();
     mfma_phase(t, kPvOnly);
   }
   for (++t; t < ntiles; ++t) {
     sync(t);
+    load_next(t);
     half();
   }
   // Clamped re-loads of the last tile may still be in flight: they must
