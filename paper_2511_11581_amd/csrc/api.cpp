@@ -283,6 +283,9 @@ pa_status check_batch(const pa_config& c, const pa_tensor* q, const pa_tensor* k
     if ((int64_t)c.block_size * kv->stride[1] * elem_bytes(kv->dtype) >= INT32_MAX ||
         kv->stride[2] * elem_bytes(kv->dtype) >= INT32_MAX)
       return fail(PA_ERR_UNSUPPORTED, "cache slot/head strides too large for 32-bit in-block offsets");
+  for (const pa_tensor* kv : {k, v})
+    if (kv->stride[0] * elem_bytes(kv->dtype) >= ((int64_t)1 << 32))
+      return fail(PA_ERR_UNSUPPORTED, "cache block stride must be below 4 GiB");
   TRY(check_aligned16(q, "q"));
   TRY(check_aligned16(k, "k_cache"));
   TRY(check_aligned16(v, "v_cache"));

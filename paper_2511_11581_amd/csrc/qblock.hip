@@ -56,10 +56,17 @@ constexpr int kWaves = kQblockWaves;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kTile = kPrefillTileKeys;
 constexpr int kStages = 4;
-constexpr int kNWin = 4;   // block-id registers per lane (a window of 256 blocks)
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16v2 __attribute__((ext_vector_type(2)));
 #define LDS_AS __attribute__((address_space(3)))
+
+constexpr uint32_t kOnesBf16x2 = 0x3f803f80u;   // bf16 pair (1, 1)
+
+// c + lo(a) lo(b) + hi(a) hi(b) for bf16 pairs, accumulated in fp32.
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16v2, a), __builtin_bit_cast(bf16v2, b), c, false);
+}
 
 // s_waitcnt with the vector-memory count bounded by N and every LDS
 // operation drained (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4],
@@ -128,81 +135,85 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
     for (int t = 0; t < NT; ++t)
       qt[t] = __builtin_bit_cast(bf16x8, ld16_cached(qrow + 2 * (16 * t + 8 * hf)));
+    // Scores come out in log2 units: Q times scale * log2(e), rounded to
+    // bf16 (a relative change below 2^-9 per element).
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      u32x4 w = __builtin_bit_cast(u32x4, qt[t]);
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        w[h] = pack_bf16(__uint_as_float(w[h] << 16) * a.sl2, __uint_as_float(w[h] & 0xffff0000u) * a.sl2);
+      qt[t] = __builtin_bit_cast(bf16x8, w);
+    }
   }
 
-  // ---- loader geometry: instruction k of this wave covers tile rows
-  //      r0 .. r0 + RPI - 1 (one cache block); lane i takes row r0 + i / CPR
-  //      and LDS slot i % CPR, i.e. logical chunk (i % CPR) ^ f(row).
+  // ---- loader geometry.  A wave loads kTile / kWaves = 8 consecutive rows
+  //      of every tile, which lie in one cache block (block_size >= 16):
+  //      instruction k covers rows wrow + RPI k .. + RPI - 1, lane i takes
+  //      row wrow + RPI k + i / CPR and LDS slot i % CPR, i.e. logical chunk
+  //      (i % CPR) ^ f(row).
+  constexpr int kWaveRows = kTile / kWaves;
+  static_assert(kWaveRows * kWaves == kTile && kWaveRows <= 16, "a wave's rows of a tile stay in one block");
+  const int wrow = kWaveRows * wave;
   auto fK = [](int r) { return (r / KRW) & (CPR - 1); };
   auto fV = [](int r) { return (CPR / 4) * (r & 3) + (CPR / 8) * ((r >> 2) & 1); };
   int koff[NLD], voff[NLD];
 #pragma unroll
   for (int k = 0; k < NLD; ++k) {
-    const int r = RPI * (wave * NLD + k) + lane / CPR, s = lane % CPR;
-    koff[k] = (r & bsm) * (int)a.kg.slot + 16 * (s ^ fK(r));
-    voff[k] = (r & bsm) * (int)a.vg.slot + 16 * (s ^ fV(r));
+    const int rr = RPI * k + lane / CPR, r = wrow + rr, s = lane % CPR;
+    koff[k] = rr * (int)a.kg.slot + 16 * (s ^ fK(r));
+    voff[k] = rr * (int)a.vg.slot + 16 * (s ^ fV(r));
   }
   const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
   const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
+  const uint32_t kblk = (uint32_t)a.kg.blk, vblk = (uint32_t)a.vg.blk;   // < 2^32 (host check)
 
-  // Block ids of blocks wb .. wb + 64 kNWin - 1, one per lane and register.
-  int win[kNWin];
-  int wb = 0;
-  auto load_window = [&](int first) {
-#pragma unroll
-    for (int q = 0; q < kNWin; ++q) win[q] = bt_row[min(first + 64 * q + lane, a.mb - 1)];
+  // Page of this wave's rows in tile tb + j, lane j (tiles tb .. tb + 63),
+  // clamped into the cache so that a corrupt table cannot address outside it.
+  int twin;
+  int tb = 0;
+  auto load_twin = [&](int first) {
+    const int p = bt_row[min((kTile * (first + lane) + wrow) >> bsl, last_blk)];
+    twin = p < 0 ? 0 : (p >= a.num_blocks ? a.num_blocks - 1 : p);
   };
-  load_window(0);
+  load_twin(0);
   __builtin_amdgcn_s_waitcnt(0);   // Q and the window; nothing else in flight
 
-  // Issue the loads of tile t into ring stage st.  Callers clamp t to the
-  // last tile but keep st = (unclamped tile) % kStages, so a clamped re-load
-  // never lands in the stage that holds the real last tile.
-  // issue_part(t, st, j): instruction j of this wave's 2 NLD for the tile
-  // (row group j / 2, K if j is even, else V).
-  auto issue_part = [&](int t, int st, int j) {
-    const int tsl = (t * kTile) & bsm;   // tile start inside its block (block_size > 64)
-    const int k = j >> 1;
-    {
-      const int r0 = RPI * (wave * NLD + k);
-      const int bi = min((t * kTile + r0) >> bsl, last_blk);
-      const int rel = bi - wb;   // inside the window (ensure_window ran for t)
-      int pg = __builtin_amdgcn_readlane(win[0], rel & 63);
-#pragma unroll
-      for (int q = 1; q < kNWin; ++q) {
-        const int c = __builtin_amdgcn_readlane(win[q], rel & 63);
-        pg = (rel >> 6) == q ? c : pg;
-      }
-      pg = pg < 0 ? 0 : (pg >= a.num_blocks ? a.num_blocks - 1 : pg);
-      const int ldo = (wave * NLD + k) * 1024;
-      // (the source is passed as void*: a const pointer here makes the host
-      // pass drop the kernel's launch stub without a diagnostic)
-      if ((j & 1) == 0) {
-        const uint8_t* kp = kbase + (int64_t)pg * a.kg.blk + (int64_t)tsl * a.kg.slot;
-        __builtin_amdgcn_global_load_lds((void*)(kp + koff[k]), (LDS_AS void*)(lds + st * TB + ldo), 16, 0, 0);
-      } else {
-        const uint8_t* vp = vbase + (int64_t)pg * a.vg.blk + (int64_t)tsl * a.vg.slot;
-        __builtin_amdgcn_global_load_lds((void*)(vp + voff[k]), (LDS_AS void*)(lds + VBASE + st * TB + ldo),
-                                         16, 0, 0);
-      }
-    }
-  };
+  // Loads of tile t into ring stage st, in two parts so that the address
+  // work can sit between matrix-core products: issue_prep(t) finds the
+  // wave's page (rare: moves the window, draining the loads in flight),
+  // issue_part(j) sends instruction j of ND (K if j is even, else V).
+  // Callers clamp t to the last tile but keep st = (unclamped tile) %
+  // kStages, so a clamped re-load never lands in the stage that holds the
+  // real last tile.
   constexpr int ND = 2 * NLD;   // load instructions per wave and tile
-  // Make the window hold every block id tile t's loads need (tiles are
-  // loaded in increasing order; the window moves to the tile's first block).
-  // Rare: drains the loads in flight.
-  auto ensure_window = [&](int t) {
-    const int bl = min((t * kTile + kTile - 1) >> bsl, last_blk);
-    if (bl >= wb + 64 * kNWin) {
-      wb = uniform(min((t * kTile) >> bsl, last_blk));
-      load_window(wb);
+  const uint8_t* kp = kbase;
+  const uint8_t* vp = vbase;
+  auto issue_prep = [&](int t) {
+    if (t - tb >= 64) {
+      tb = uniform(t);
+      load_twin(tb);
       __builtin_amdgcn_s_waitcnt(0);
     }
+    const uint32_t pg = (uint32_t)__builtin_amdgcn_readlane(twin, t - tb);
+    const int rb = (kTile * t + wrow) & bsm;   // first row inside the block
+    kp = kbase + (uint64_t)pg * kblk + (uint32_t)(rb * (int)a.kg.slot);
+    vp = vbase + (uint64_t)pg * vblk + (uint32_t)(rb * (int)a.vg.slot);
+  };
+  auto issue_part = [&](int st, int j) {
+    const int k = j >> 1;
+    const int ldo = (wave * NLD + k) * 1024;
+    // (the source is passed as void*: a const pointer here makes the host
+    // pass drop the kernel's launch stub without a diagnostic)
+    if ((j & 1) == 0)
+      __builtin_amdgcn_global_load_lds((void*)(kp + koff[k]), (LDS_AS void*)(lds + st * TB + ldo), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((void*)(vp + voff[k]), (LDS_AS void*)(lds + VBASE + st * TB + ldo), 16, 0, 0);
   };
   auto issue = [&](int t, int st) {
-    ensure_window(t);
+    issue_prep(t);
 #pragma unroll
-    for (int j = 0; j < ND; ++j) issue_part(t, st, j);
+    for (int j = 0; j < ND; ++j) issue_part(st, j);
   };
   // V rows at or past kv_len (last tile only) may hold anything, NaN
   // included, and would poison P V even with zero weights: each lane zeroes
@@ -233,24 +244,117 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   }
 
   f32x16 o[NDB];     // O^T accumulators
-  f32x16 s[2];       // S^T of one tile (two 32-key halves)
+  f32x16 s[2];       // S^T of one tile (two 32-key halves), relative to m_run
+  f32x16 nm;         // -m_run in every element: the score products start from it
   bf16x8 pb[4];      // P^T operands (four 16-key steps)
-  float m_run = kNegInf, l_run = 0.f;
+  float m_run = 0.f, l_run = 0.f;
+  float psum = 0.f;                   // row sum of the tile in progress
+  float alpha = 1.f;                  // O rescale owed before the next products
+  uint64_t resc = 0;                  // (wave-uniform) some lane's alpha != 1
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
 
-  // Matrix-core phase of period t: scores of tile t + 1 (if this wave needs
-  // it) and O^T += V^T P^T of tile t (if this wave attends to it), as one
-  // fixed sequence of products whose LDS operands are read kAhead products
-  // ahead into a small register ring (a scheduling fence after every
-  // product keeps the compiler from hoisting all reads at once).
+  // ---- softmax pieces.  Q carries the factor scale * log2(e), so a score
+  //      product started from nm = -m_run leaves s = S scale log2(e) - m_run
+  //      and the weight is 2^s with no further arithmetic.  Element e is
+  //      s[e / 16][e % 16], key 8(e % 16 / 4) + 4 hf + e % 4 + 32 (e / 16) of
+  //      the tile.  Causal mask of tile t (tiles crossing a diagonal only):
+  auto mask = [&](int t) {
+    const int lim = pos - t * kTile - 4 * hf;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        s[kb][i] = (32 * kb + 8 * (i >> 2) + (i & 3)) <= lim ? s[kb][i] : kNegInf;
+  };
+  // Weights of elements 8u .. 8u + 7, 2^(s - d), to the bf16 operand pb[u];
+  // the row sum adds the rounded weights (the ones the products use) with
+  // dot2.  (Used where the reference moves; the products' schedule splits
+  // the d = 0 case into exp_pair and pack_group below.)
+  auto group = [&](int u, float d) {
+    const int kb = u >> 1, i0 = 8 * (u & 1);
+    u32x4 pw;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      pw[h] = pack_bf16(fast_exp2(s[kb][i0 + 2 * h] - d), fast_exp2(s[kb][i0 + 2 * h + 1] - d));
+    pb[u] = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
+  };
+  // The same split for the products' schedule: exp_pair(u, h) computes the
+  // weights of elements 8u + 2h, 8u + 2h + 1 into ex[], pack_group(u)
+  // writes pb[u] and the row sum.
+  float ex[8];
+  auto exp_pair = [&](int u, int h) {
+    const int kb = u >> 1, i0 = 8 * (u & 1);
+    ex[2 * h] = fast_exp2(s[kb][i0 + 2 * h]);
+    ex[2 * h + 1] = fast_exp2(s[kb][i0 + 2 * h + 1]);
+  };
+  auto pack_group = [&](int u) {
+    u32x4 pw;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) pw[h] = pack_bf16(ex[2 * h], ex[2 * h + 1]);
+    pb[u] = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
+  };
+  // Row max of the tile (relative to m_run), across the lane pair.
+  auto tile_max = [&]() {
+    float mA = kNegInf, mB = kNegInf;
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+      mA = fmaxf(fmaxf(mA, s[0][i]), s[0][i + 1]);
+      mB = fmaxf(fmaxf(mB, s[1][i]), s[1][i + 1]);
+    }
+    return xor32_max(fmaxf(mA, mB));
+  };
+  // End of a tile's softmax.  The reference is kept while every weight of
+  // the row stays below 2^12 (the lane's 32-key sum tells); otherwise it
+  // moves up to the row max and the weights are recomputed, and O and l
+  // owe the factor 2^-d.  m_run thus stays within 12 of the running max
+  // and never above it.
+  auto finish = [&]() {
+    if (__ballot(psum > 4096.f)) {
+      const float d = fmaxf(tile_max(), 0.f);
+      m_run += d;
+      alpha = fast_exp2(-d);
+      resc = 1;
+      l_run *= alpha;
+      psum = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) group(u, d);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) nm[i] = -m_run;
+    }
+    l_run += psum;
+    psum = 0.f;
+  };
+  // Softmax work placed after product step p of the P V sequence (NP steps;
+  // operand pb[u] is read by steps NDB u .. NDB u + NDB - 1, so its next
+  // value may only be written after them).  group(3) and finish() follow
+  // the sequence.
   constexpr int NS = 2 * NT;       // score products: (k-step tt, key half kb)
   constexpr int NP = 4 * NDB;      // PV products: (16-key step u, d block db)
+  // Group u's weights are computed over the NDB steps that read pb[u] and
+  // packed after the last of them; group 3 is packed after the sequence.
+  auto valu_step = [&](int p) {
+    const int u = p / NDB, q = p % NDB;
+#pragma unroll
+    for (int h = q * (4 / NDB); h < (q + 1) * (4 / NDB); ++h) exp_pair(u, h);
+    if (q == NDB - 1 && u < 3) pack_group(u);
+  };
+
+  // Products of period t as one fixed sequence: scores of tile t + 1 (if
+  // this wave needs it) over the K stage, then O^T += V^T P^T of tile t over
+  // the V stage with the softmax of tile t + 1 spread between its steps.
+  // LDS operands are read kAhead products ahead into a small register ring;
+  // a scheduling fence after every product keeps each step's work in place.
   constexpr int kAhead = 4;
-  // mfma_phase(t, full): full = scores of tile t + 1 as well (else PV only).
-  auto mfma_phase = [&](int t, auto full_tag) {
+  static_assert(2 + 3 * ND <= NS + 1, "tile loads fit between the score products");
+  auto period = [&](int t, auto full_tag) {
+    constexpr bool kFullP = decltype(full_tag)::value;
     const uint8_t* ks = lds + ((t + 1) & (kStages - 1)) * TB;
     uint8_t* vs = lds + (t & (kStages - 1)) * TB;
     auto rd = [&](int i) -> bf16x8 {   // operand of product i (i < NS: K, else V^T)
@@ -263,82 +367,37 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       const u32x4 vw = {l2[0], l2[1], h2[0], h2[1]};
       return __builtin_bit_cast(bf16x8, vw);
     };
-    auto run = [&](auto first_tag) {
-      constexpr int I0 = decltype(first_tag)::value;   // 0: scores and PV, NS: PV only
-      bf16x8 ring[kAhead];
+    constexpr int I0 = kFullP ? 0 : NS;
+    bf16x8 ring[kAhead];
 #pragma unroll
-      for (int i = 0; i < kAhead; ++i) ring[i] = rd(I0 + i);
+    for (int i = 0; i < kAhead; ++i) ring[i] = rd(I0 + i);
 #pragma unroll
-      for (int i = I0; i < NS + NP; ++i) {
-        const bf16x8 op = ring[(i - I0) % kAhead];
-        if (i < NS) {
-          s[i & 1] = mfma32(op, qt[i >> 1], s[i & 1]);
-        } else {
-          const int u = (i - NS) / NDB, db = (i - NS) % NDB;
-          o[db] = mfma32(op, pb[u], o[db]);
-        }
-        if (i + kAhead < NS + NP) ring[(i - I0) % kAhead] = rd(i + kAhead);
-        __builtin_amdgcn_sched_barrier(0);
+    for (int i = I0; i < NS + NP; ++i) {
+      const bf16x8 op = ring[(i - I0) % kAhead];
+      if (i < NS) {
+        s[i & 1] = mfma32(op, qt[i >> 1], (i >> 1) == 0 ? nm : s[i & 1]);
+      } else {
+        const int p = i - NS;
+        o[p % NDB] = mfma32(op, pb[p / NDB], o[p % NDB]);
       }
-    };
-    if constexpr (decltype(full_tag)::value) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
-      run(std::integral_constant<int, 0>{});
-    } else {
-      run(std::integral_constant<int, NS>{});
-    }
-  };
-  // VALU phase for tile t: causal mask (tiles crossing a diagonal), row max,
-  // rescale of O when the max rises, weights packed to P^T operands.
-  auto valu_phase = [&](int t) {
-    if (t >= nfull) {
-      const int lim = pos - t * kTile - 4 * hf;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          s[kb][i] = (32 * kb + 8 * (i >> 2) + (i & 3)) <= lim ? s[kb][i] : kNegInf;
-    }
-    float m = kNegInf;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) m = fmaxf(m, s[kb][i]);
-    const float mx = xor32_max(m) * a.sl2;
-    if (__ballot(mx > m_run + 8.f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = fast_exp2(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
-    }
-    float psum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = fast_exp2(__builtin_fmaf(s[kb][i], a.sl2, -m_run));
-        s[kb][i] = p;
-        psum += p;
+      if (i + kAhead < NS + NP) ring[(i - I0) % kAhead] = rd(i + kAhead);
+      if constexpr (kFullP) {
+        // loads of tile t + 3 between the score products
+        if (i == 1) issue_prep(min(t + 3, ntiles - 1));
+        if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) issue_part((t + 3) & (kStages - 1), (i - 2) / 3);
+        if (i == NS - 1 && t + 1 >= nfull) mask(t + 1);
+        if (i >= NS) valu_step(i - NS);
       }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r0 = 8 * h;
-        const u32x4 pw = {pack_bf16(s[kb][r0 + 0], s[kb][r0 + 1]), pack_bf16(s[kb][r0 + 2], s[kb][r0 + 3]),
-                          pack_bf16(s[kb][r0 + 4], s[kb][r0 + 5]), pack_bf16(s[kb][r0 + 6], s[kb][r0 + 7])};
-        pb[2 * kb + h] = __builtin_bit_cast(bf16x8, pw);
-      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    l_run += psum;
+    if constexpr (kFullP) {
+      pack_group(3);
+      finish();
+    }
   };
 
-  // ---- prologue: tiles 0, 1, 2 in flight; scores of tile 0 for all waves,
-  //      weights of tile 0 for group 0 (group 1 takes them in its first
-  //      VALU half)
+  // ---- prologue: tiles 0, 1, 2 in flight; scores and weights of tile 0,
+  //      whose row max becomes the first reference
   issue(0, 0);
   issue(min(1, ntiles - 1), 1);
   issue(min(2, ntiles - 1), 2);
@@ -349,73 +408,53 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   {
     const uint8_t* ks = lds;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
-#pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
-      s[0] = mfma32(*(const bf16x8*)(ks + kaddr[tt]), qt[tt], s[0]);
-      s[1] = mfma32(*(const bf16x8*)(ks + kaddr[tt] + 32 * RB), qt[tt], s[1]);
+      s[0] = mfma32(*(const bf16x8*)(ks + kaddr[tt]), qt[tt], tt == 0 ? f32x16{} : s[0]);
+      s[1] = mfma32(*(const bf16x8*)(ks + kaddr[tt] + 32 * RB), qt[tt], tt == 0 ? f32x16{} : s[1]);
     }
   }
+  if (0 >= nfull) mask(0);
+  m_run = tile_max();   // finite: key 0 is never masked
+#pragma unroll
+  for (int u = 0; u < 4; ++u) group(u, m_run);
+  l_run = psum;
+  psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) nm[i] = -m_run;
 
-  // ---- tile periods.  First half: group 0 matrix cores (tile t + 1 scores,
-  //      tile t products), group 1 VALU (tile t weights); second half: the
-  //      reverse.  Loads of tile t + 3 go into the stage of tile t - 1,
-  //      which both groups finished in the previous period.  The groups run
-  //      separate loops with the same
-  //      barriers (a barrier counts waves, not code addresses), so that
-  //      neither loop merges the other's register state.
+  // ---- tile periods.  sync(t): tile t + 1 has landed for every wave and
+  //      every wave has finished period t - 1, so the stage of tile t - 1
+  //      takes the loads of tile t + 3.  The O rescale owed by the softmax
+  //      of tile t is applied before the products of tile t.
   auto sync = [&](int t) {
     wait_vm_lds<2 * NLD>();   // this wave's loads of tile t + 1 have landed
     if (t + 1 == ntiles - 1) zero_tail(t + 1);
     wait_vm_lds<2 * NLD>();
     __builtin_amdgcn_s_barrier();
   };
-  // Loads of tile t + 3 (into the stage of tile t - 1, free in period t).
-  // Each group issues them in its VALU half, next to the short softmax
-  // work, so that the issue stalls stay out of the matrix-core phases.
   auto load_next = [&](int t) { issue(min(t + 3, ntiles - 1), (t + 3) & (kStages - 1)); };
-  auto half = [&]() {
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // this half's LDS reads done (vmcnt untouched)
-    __builtin_amdgcn_s_barrier();
+  auto rescale = [&]() {
+    if (resc) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+      resc = 0;
+    }
   };
-  // Each wave: full periods while it needs the next tile's scores, one
-  // period with the products of its last tile, then barriers only.
   constexpr std::true_type kFull{};
   constexpr std::false_type kPvOnly{};
   int t = 0;
-  if (grp == 0) {
-    valu_phase(0);
-    for (; t + 1 < nact; ++t) {
-      sync(t);
-      mfma_phase(t, kFull);
-      half();
-      valu_phase(t + 1);
-      load_next(t);
-    }
+  for (; t + 1 < nact; ++t) {
     sync(t);
-    mfma_phase(t, kPvOnly);
-    half();
-    load_next(t);
-  } else {
-    for (; t + 1 < nact; ++t) {
-      sync(t);
-      load_next(t);
-      valu_phase(t);
-      half();
-      mfma_phase(t, kFull);
-    }
-    sync(t);
-    load_next(t);
-    valu_phase(t);
-    half();
-    mfma_phase(t, kPvOnly);
+    rescale();
+    period(t, kFull);   // issues the loads of tile t + 3 as well
   }
+  sync(t);
+  load_next(t);
+  rescale();
+  period(t, kPvOnly);
   for (++t; t < ntiles; ++t) {
     sync(t);
     load_next(t);
-    half();
   }
   // Clamped re-loads of the last tile may still be in flight: they must
   // land before the workgroup's LDS can be handed to another workgroup.
