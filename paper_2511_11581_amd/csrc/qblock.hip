@@ -63,6 +63,23 @@ typedef __bf16 bf16v2 __attribute__((ext_vector_type(2)));
 
 constexpr uint32_t kOnesBf16x2 = 0x3f803f80u;   // bf16 pair (1, 1)
 
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
+  return (uint32_t)(uintptr_t)(const LDS_AS uint8_t*)p;
+}
+
+// Global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4): lane
+// i's 16 bytes at g land at LDS byte lds + 16 i (lds wave-uniform).  Issued
+// as inline asm, outside the compiler's view of LDS: otherwise every LDS
+// read after it would first wait for all such copies in flight.  The
+// kernel orders copies and reads itself, with explicit vmcnt waits before
+// its barriers.
+__device__ __forceinline__ void dma16(const uint8_t* g, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"   // (one wait state after the M0 write)
+               :
+               : "v"(g), "{m0}"(lds)
+               : "memory");
+}
+
 // c + lo(a) lo(b) + hi(a) hi(b) for bf16 pairs, accumulated in fp32.
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16v2, a), __builtin_bit_cast(bf16v2, b), c, false);
@@ -203,12 +220,10 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   auto issue_part = [&](int st, int j) {
     const int k = j >> 1;
     const int ldo = (wave * NLD + k) * 1024;
-    // (the source is passed as void*: a const pointer here makes the host
-    // pass drop the kernel's launch stub without a diagnostic)
     if ((j & 1) == 0)
-      __builtin_amdgcn_global_load_lds((void*)(kp + koff[k]), (LDS_AS void*)(lds + st * TB + ldo), 16, 0, 0);
+      dma16(kp + koff[k], lds_addr(lds + st * TB + ldo));
     else
-      __builtin_amdgcn_global_load_lds((void*)(vp + voff[k]), (LDS_AS void*)(lds + VBASE + st * TB + ldo), 16, 0, 0);
+      dma16(vp + voff[k], lds_addr(lds + VBASE + st * TB + ldo));
   };
   auto issue = [&](int t, int st) {
     issue_prep(t);
