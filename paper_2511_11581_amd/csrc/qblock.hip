@@ -9,21 +9,20 @@
 //   online softmax, one lane per row (max / sum finish with permlane32)
 //   O^T[d x 32 rows]      += V^T P^T         (P^T from S^T's registers)
 //
-// Ping-pong: waves 0-3 and 4-7 form two groups with one wave of each on
-// every SIMD, and the groups work half a tile period apart, separated by a
-// workgroup barrier at every half period.  In one half a wave runs its
-// matrix-core phase (scores of tile t + 1 and O += V^T P^T of tile t, LDS
-// operand reads only) while the other wave on the SIMD runs its VALU phase
-// (mask, row max, rescale, weights 2^(S scale - m) packed to bf16 for tile
-// t + 1); in the next half they swap.  The matrix cores of a SIMD thus see
-// one wave's products while its VALU serves the other wave's softmax.
+// Per period t every wave runs one fixed sequence of matrix-core products:
+// the scores of tile t + 1, then O += V^T P^T of tile t with the softmax of
+// tile t + 1 (one exp, one pack and one dot2 per weight) placed between its
+// products, so that the VALU work runs under the wave's own products; the
+// second wave on the SIMD does the same.  Q carries scale * log2(e) and the
+// score products start from -m, so no per-weight arithmetic precedes the
+// exp.
 //
 // K/V tiles of 64 keys move from HBM into a ring of 4 LDS stages with
 // global_load_lds_dwordx4 (no staging registers, no VALU), three tiles
 // ahead of their use; each wave issues its share of a tile (whole 16-byte
 // row chunks, 4 or 8 rows of one cache block per instruction, scalar page
-// base).  The waits are explicit vmcnt counts, so the two tiles still in
-// flight are never waited for.
+// base) between its score products.  The waits are explicit vmcnt counts,
+// so the tiles still in flight are never waited for.
 //
 // LDS layouts (rows of 2d bytes, 16-byte chunks XOR-swizzled by row; the
 // swizzles were chosen with SQ_LDS_BANK_CONFLICT on the device, which reads
@@ -40,9 +39,12 @@
 // 0-3 come from keys 16u + 4(l/32) + 0..3 and slots 4-7 from 16u + 8 +
 // 4(l/32) + 0..3.
 //
-// The running max is only raised when a row's tile max exceeds it by more
-// than 8 (log2 units): the weights then stay below 2^8 and the final
-// division uses the same reference, so the result is unchanged.
+// The reference m of a row is the first tile's row max and is only raised
+// when a weight of the row exceeds 2^12 (the lane's 32-key weight sum tells):
+// the final division uses the same reference, so the result is unchanged.
+//
+// The output goes through the K ring (free once the last scores are done)
+// so that every store writes whole rows.
 #include <type_traits>
 
 #include "common.hpp"
@@ -111,13 +113,15 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStages * TB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
-  const int grp = wave >> 2;                       // ping-pong group
   const int n = lane & 31, hf = lane >> 5;
   const int Hkv = a.num_kv_heads;
+  const int G = a.group, BQ = pp.block_q, bsl = a.bs_log2, bsm = a.block_size - 1;
+  // One workgroup per (Q-block, kv head) unit, kv head fastest: with
+  // round-robin dispatch over the 8 XCDs, the units of one kv head (Hkv =
+  // 8) share an XCD and its L2, which serves the K/V re-reads of a
+  // sequence's Q-blocks.
   const int g = blockIdx.x % Hkv;
   const int wi = blockIdx.x / Hkv;
-  const int G = a.group, BQ = pp.block_q, bsl = a.bs_log2, bsm = a.block_size - 1;
-
   if (wi >= pp.count[0]) return;
   const int seq = uniform(pp.list_seq[wi]);
   const int qb = uniform(pp.list_qb[wi]);
@@ -398,8 +402,10 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       if (i + kAhead < NS + NP) ring[(i - I0) % kAhead] = rd(i + kAhead);
       if constexpr (kFullP) {
         // loads of tile t + 3 between the score products
-        if (i == 1) issue_prep(min(t + 3, ntiles - 1));
-        if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) issue_part((t + 3) & (kStages - 1), (i - 2) / 3);
+        if (t + 3 < ntiles) {
+          if (i == 1) issue_prep(t + 3);
+          if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) issue_part((t + 3) & (kStages - 1), (i - 2) / 3);
+        }
         if (i == NS - 1 && t + 1 >= nfull) mask(t + 1);
         if (i >= NS) valu_step(i - NS);
       }
@@ -414,11 +420,16 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   // ---- prologue: tiles 0, 1, 2 in flight; scores and weights of tile 0,
   //      whose row max becomes the first reference
   issue(0, 0);
-  issue(min(1, ntiles - 1), 1);
-  issue(min(2, ntiles - 1), 2);
-  wait_vm_lds<4 * NLD>();
+  if (ntiles > 1) issue(1, 1);
+  if (ntiles > 2) issue(2, 2);
+  auto wait_first = [&]() {   // tile 0 landed; tiles 1, 2 may still fly
+    if (ntiles > 2) wait_vm_lds<2 * ND>();
+    else if (ntiles == 2) wait_vm_lds<ND>();
+    else wait_vm_lds<0>();
+  };
+  wait_first();
   if (ntiles == 1) zero_tail(0);
-  wait_vm_lds<4 * NLD>();
+  wait_first();
   __builtin_amdgcn_s_barrier();
   {
     const uint8_t* ks = lds;
@@ -442,12 +453,20 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   //      takes the loads of tile t + 3.  The O rescale owed by the softmax
   //      of tile t is applied before the products of tile t.
   auto sync = [&](int t) {
-    wait_vm_lds<2 * NLD>();   // this wave's loads of tile t + 1 have landed
+    // this wave's loads of tile t + 1 have landed (those of t + 2, if it
+    // exists, may still fly)
+    auto wait_next = [&]() {
+      if (t + 2 < ntiles) wait_vm_lds<ND>();
+      else wait_vm_lds<0>();
+    };
+    wait_next();
     if (t + 1 == ntiles - 1) zero_tail(t + 1);
-    wait_vm_lds<2 * NLD>();
+    wait_next();
     __builtin_amdgcn_s_barrier();
   };
-  auto load_next = [&](int t) { issue(min(t + 3, ntiles - 1), (t + 3) & (kStages - 1)); };
+  auto load_next = [&](int t) {
+    if (t + 3 < ntiles) issue(t + 3, (t + 3) & (kStages - 1));
+  };
   auto rescale = [&]() {
     if (resc) {
 #pragma unroll
@@ -471,24 +490,35 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     sync(t);
     load_next(t);
   }
-  // Clamped re-loads of the last tile may still be in flight: they must
-  // land before the workgroup's LDS can be handed to another workgroup.
-  __builtin_amdgcn_s_waitcnt(0);
 
-  // ---- finalise: out = O / l, bf16
+  // ---- finalise: out = O / l, bf16, staged through the K ring so that
+  //      the stores write whole rows.  Every wave has finished its K reads
+  //      (the last were before the last sync barrier) and no copy is in
+  //      flight, so each wave writes its own 32 rows there (row-major,
+  //      16-byte chunk c of row r at slot c ^ (r mod CPR)) and reads them
+  //      back as 1 KB runs: 1024 / RB rows per store, 16 bytes per lane.
   const float l_tot = xor32_sum(l_run);
-  if (rvalid) {
-    const float inv = a.v_scale / l_tot;
-    uint8_t* orow = a.out + (int64_t)(t0 + tl) * a.o_tok + (int64_t)(g * G + row % G) * a.o_head;
+  const float inv = a.v_scale / l_tot;
+  {
+    uint8_t* orow_l = lds + row * RB;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int d0 = 32 * db + 8 * q + 4 * hf;
+        const int c = 4 * db + q;   // 16-byte chunk of d 32db + 8q .. + 7
         u32x2 w = {pack_bf16(o[db][4 * q] * inv, o[db][4 * q + 1] * inv),
                    pack_bf16(o[db][4 * q + 2] * inv, o[db][4 * q + 3] * inv)};
-        *(u32x2*)(orow + 2 * d0) = w;
+        *(u32x2*)(orow_l + 16 * (c ^ (row & (CPR - 1))) + 8 * hf) = w;
       }
+  }
+  constexpr int RPS = 1024 / RB;   // rows per store instruction
+#pragma unroll
+  for (int j = 0; j < kQblockWaveRows / RPS; ++j) {
+    const int r = wave * kQblockWaveRows + j * RPS + lane / CPR, c = lane % CPR;
+    const u32x4 w = *(const u32x4*)(lds + r * RB + 16 * (c ^ (r & (CPR - 1))));
+    const int tr = tok_lo + r / G;
+    if (tr < tok_hi)
+      *(u32x4*)(a.out + (int64_t)(t0 + tr) * a.o_tok + (int64_t)(g * G + r % G) * a.o_head + 16 * c) = w;
   }
 }
 
