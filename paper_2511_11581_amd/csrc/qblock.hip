@@ -156,16 +156,6 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
     for (int t = 0; t < NT; ++t)
       qt[t] = __builtin_bit_cast(bf16x8, ld16_cached(qrow + 2 * (16 * t + 8 * hf)));
-    // Scores come out in log2 units: Q times scale * log2(e), rounded to
-    // bf16 (a relative change below 2^-9 per element).
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      u32x4 w = __builtin_bit_cast(u32x4, qt[t]);
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-        w[h] = pack_bf16(__uint_as_float(w[h] << 16) * a.sl2, __uint_as_float(w[h] & 0xffff0000u) * a.sl2);
-      qt[t] = __builtin_bit_cast(bf16x8, w);
-    }
   }
 
   // ---- loader geometry.  A wave loads kTile / kWaves = 8 consecutive rows
@@ -198,7 +188,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     twin = p < 0 ? 0 : (p >= a.num_blocks ? a.num_blocks - 1 : p);
   };
   load_twin(0);
-  __builtin_amdgcn_s_waitcnt(0);   // Q and the window; nothing else in flight
+  __builtin_amdgcn_s_waitcnt(0);   // Q and the window (one latency for both)
 
   // Loads of tile t into ring stage st, in two parts so that the address
   // work can sit between matrix-core products: issue_prep(t) finds the
@@ -427,6 +417,17 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     else if (ntiles == 2) wait_vm_lds<ND>();
     else wait_vm_lds<0>();
   };
+  // While the first tiles fly: scores come out in log2 units, Q times
+  // scale * log2(e), rounded to bf16 (a relative change below 2^-9 per
+  // element).
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    u32x4 w = __builtin_bit_cast(u32x4, qt[t]);
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      w[h] = pack_bf16(__uint_as_float(w[h] << 16) * a.sl2, __uint_as_float(w[h] & 0xffff0000u) * a.sl2);
+    qt[t] = __builtin_bit_cast(bf16x8, w);
+  }
   wait_first();
   if (ntiles == 1) zero_tail(0);
   wait_first();
