@@ -117,6 +117,34 @@ def time_steps(w, att, out, steps, warmup):
     return ev0.elapsed_time(ev1) / steps
 
 
+def time_graph(w, att, out, steps, warmup):
+    """Mean ms per replay of one pa_forward captured in a HIP graph (the
+    launch overhead of the eager calls gone; the same kernels and work)."""
+    import torch
+    args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        att.forward(*args, w.scale, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        att.forward(*args, w.scale, out=out)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(steps):
+        g.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    del g
+    return ev0.elapsed_time(ev1) / steps
+
+
 def per_kernel_ms(w, out, steps, warmup):
     """Average duration of each kernel (HIP events recorded by the library
     around every launch on the same stream)."""
@@ -141,13 +169,14 @@ def measure(k, steps, warmup):
     att = make_attention(w)
     out = torch.empty_like(w.q)
     ms = time_steps(w, att, out, steps, warmup)
+    gms = time_graph(w, att, out, steps, warmup)
     kms = per_kernel_ms(w, out, steps, warmup)
     plan = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]))
     att.close()
     B, F = alg_bytes(w), alg_flops(w)
     res = {
         "config": k, "name": W.CONFIG_NAMES[k], "seed": w.seed, "sum_L": sum(w.seq_len_list),
-        "us_per_batch": ms * 1e3, "alg_bytes": B, "alg_flops": F,
+        "us_per_batch": ms * 1e3, "graph_us_per_batch": gms * 1e3, "alg_bytes": B, "alg_flops": F,
         "GBps": B / (ms * 1e-3) / 1e9, "TFLOPs": F / (ms * 1e-3) / 1e12,
         "per_kernel_us": {kk: v * 1e3 for kk, v in kms.items() if v > 0},
         "plan": {kk: plan[kk] for kk in ("decode_step", "decode_workers", "decode_min_steps",
@@ -241,7 +270,8 @@ def main():
                 torch.cuda.empty_cache()
     for k in sorted(configs):
         r = configs[k]
-        print(f"# config {k}: {r['us_per_batch']:.1f} us/batch, {r['GBps']:.0f} GB/s "
+        print(f"# config {k}: {r['us_per_batch']:.1f} us/batch ({r['graph_us_per_batch']:.1f} replayed "
+              f"from a HIP graph), {r['GBps']:.0f} GB/s "
               f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
               f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}", file=sys.stderr)
 
@@ -273,7 +303,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if not headline_w.kv_fp8 else "bf16/fp8-kv",
         "data": "synthetic (seeded N(0,1) bf16 Q/K/V, random block tables)",
         "config": {"workload": h["name"], "seq_lens_sum": h["sum_L"], "seed": h["seed"],
-                   "us_per_batch": h["us_per_batch"], "parallelism": "single GPU"},
+                   "us_per_batch": h["us_per_batch"], "graph_us_per_batch": h["graph_us_per_batch"],
+                   "parallelism": "single GPU"},
         "roofline": roof, "cpu_baseline": cpu,
         "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
     }

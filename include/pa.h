@@ -126,7 +126,10 @@ typedef struct pa_profile {
  * share is a segment ("piece").  The device activates
  * min(decode_workers / HU, ceil(total steps / decode_min_steps)) groups, so
  * a single pair of 32 steps with decode_min_steps = 8 is cut into 4
- * segments of 8 steps (the example of Fig. 4). */
+ * segments of 8 steps (the example of Fig. 4).  The default minimum share is
+ * 1 step (environment PA_DECODE_MIN_STEPS, read when a handle is created):
+ * for batches too small to fill the grid, the serial steps of one worker
+ * cost more than the merge of more segments. */
 typedef struct pa_plan_info {
   int32_t decode_launch;     /* 1 if the decode kernels are launched */
   int32_t decode_step;       /* keys per decode step (32, 64 or 128) */

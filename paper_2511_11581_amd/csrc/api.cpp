@@ -64,7 +64,7 @@ pa_status fail(pa_status st, const char* fmt, ...) {
 }
 
 constexpr int kMaxCus = 256;
-constexpr int kMinStepsDefault = 8;
+constexpr int kMinStepsDefault = 1;   // small batches: latency, not the merge, decides
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
 constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel

@@ -71,10 +71,12 @@ def fig4_example():
     return n_tiles, tps, [tuple(int(x) for x in part.split()) for part in tail.split(";")]
 
 
-def test_plan_reproduces_the_papers_partition_example():
+def test_plan_reproduces_the_papers_partition_example(monkeypatch):
     # Fig. 4 (Sec. 4.5): the tiles of one long decode row are distributed over
-    # segments of 8 tiles, here 32 tiles over 4 segments.
+    # segments of 8 tiles, here 32 tiles over 4 segments (the minimum share
+    # set to the figure's segment length; the default is 1 step).
     n_tiles, tps, expect = fig4_example()
+    monkeypatch.setenv("PA_DECODE_MIN_STEPS", str(tps))
     c = cfg(4, 1, 128)
     p = plan(c, cus=256, T=1, S=1, MB=n_tiles * 2)
     assert p["decode_step"] == 32 and p["decode_min_steps"] == tps
