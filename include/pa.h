@@ -145,6 +145,7 @@ typedef struct pa_plan_info {
   int64_t decode_grid[3];
   int64_t merge_grid[3];
   int64_t prefill_grid[3];
+  int64_t prefill_units;     /* Q-block slots x kv heads: the prefill work units */
   uint64_t workspace_bytes;  /* workspace this batch shape needs */
 } pa_plan_info;
 

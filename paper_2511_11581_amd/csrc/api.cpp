@@ -136,9 +136,9 @@ int decode_unit_heads(const pa_config& c) {
 // Workspace layout: validation header, decode-list counters, decode list
 // [S + 1] int4, piece partials [workers, 2, HU, G, d] and
 // [workers, 2, HU, G, 2] fp32, then the Q-block work list (seq_start
-// [S + 1], list_seq, list_qb, count).
+// [S + 1], list_seq, list_qb, the per-item records, count).
 struct WsLayout {
-  uint64_t meta, dec, part_o, part_ml, seq_start, list_seq, list_qb, count, total;
+  uint64_t meta, dec, part_o, part_ml, seq_start, list_seq, list_qb, rec, count, total;
 };
 
 WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
@@ -159,6 +159,8 @@ WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
   off += align256((uint64_t)items * 4);
   l.list_qb = off;
   off += align256((uint64_t)items * 4);
+  l.rec = off;
+  off += align256((uint64_t)items * 16);
   l.count = off;
   off += items > 0 ? 256 : 0;
   l.total = off;
@@ -200,7 +202,8 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
     if (T >= 2 && max_len >= 2) {
       p->prefill_launch = 1;
       items = prefill_items(T, S, p->block_q);
-      p->prefill_grid[0] = items * c.num_kv_heads;
+      p->prefill_units = items * c.num_kv_heads;
+      p->prefill_grid[0] = p->prefill_units;   // one workgroup per unit
       p->prefill_grid[1] = 1;
       p->prefill_grid[2] = 1;
     }
@@ -581,7 +584,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   a.v_scale = c.v_scale;
 
   if (!p.decode_launch) return PA_OK;
-  const int64_t items = p.prefill_launch ? p.prefill_grid[0] / c.num_kv_heads : 0;
+  const int64_t items = p.prefill_launch ? p.prefill_units / c.num_kv_heads : 0;
   const WsLayout wl = ws_layout(c, p.decode_workers, sh.S, items);
   pa::DecodePlan dp;
   dp.workers = p.decode_workers;
@@ -599,6 +602,7 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   pp.list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
   pp.list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
   pp.count = reinterpret_cast<int32_t*>(ws + wl.count);
+  pp.rec = reinterpret_cast<int4*>(ws + wl.rec);
 
   hipError_t e = timed_launch(h, PA_KERNEL_PLAN, st,
                               [&] { return pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st); });

@@ -97,6 +97,7 @@ struct PrefillPlan {
   int32_t* list_seq;   // [work_items] sequence of the w-th Q-block (planned order)
   int32_t* list_qb;    // [work_items] Q-block index inside that sequence
   int32_t* count;      // [1] number of Q-blocks
+  int4* rec;           // [work_items] (sequence, first token, rows, keys before the first row)
 };
 
 struct GatherArgs {

@@ -134,12 +134,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     seq = lo;
     qb = idx - start_of(lo);
   };
+  // The record of a Q-block: its sequence, its first token, its row count
+  // and the keys before its first token.
+  auto place = [&](int at, int seq, int qb) {
+    const int t0 = a.qsl[seq], q = a.qsl[seq + 1] - t0;
+    const int L = min(a.seq_lens[seq], cap);
+    pp.list_seq[at] = seq;
+    pp.list_qb[at] = qb;
+    pp.rec[at] = make_int4(seq, t0 + qb * bq, min(bq, q - qb * bq), (L - q) + qb * bq);
+  };
   if (N > kPlanSortCap) {
     for (int idx = tid; idx < N; idx += kPlanThreads) {
       int seq, qb;
       locate(idx, seq, qb);
-      pp.list_seq[idx] = seq;
-      pp.list_qb[idx] = qb;
+      place(idx, seq, qb);
     }
     return;
   }
@@ -171,9 +179,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
   for (int idx = tid; idx < N; idx += kPlanThreads) {
     int seq, qb;
     locate(idx, seq, qb);
-    const int pos = atomicAdd(&hist[keys[idx]], 1);
-    pp.list_seq[pos] = seq;
-    pp.list_qb[pos] = qb;
+    place(atomicAdd(&hist[keys[idx]], 1), seq, qb);
   }
 }
 

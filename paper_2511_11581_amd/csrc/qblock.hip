@@ -87,6 +87,16 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16v2, a), __builtin_bit_cast(bf16v2, b), c, false);
 }
 
+// Scalar-cache loads (wave-uniform address): a table entry, a Q-block record.
+__device__ __forceinline__ int load_s32(const int* p) {
+  return *(const __attribute__((address_space(4))) int*)p;
+}
+__device__ __forceinline__ int4 load_rec(const int4* p) {
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+  const i32x4 v = *(const __attribute__((address_space(4))) i32x4*)p;
+  return make_int4(v[0], v[1], v[2], v[3]);
+}
+
 // s_waitcnt with the vector-memory count bounded by N and every LDS
 // operation drained (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4],
 // lgkmcnt[11:8]).
@@ -112,27 +122,27 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   static_assert(RPI <= 16, "one instruction stays inside one 16-key block");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStages * TB];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int tid = __builtin_amdgcn_workitem_id_x(), lane = tid & 63, wave = uniform(tid >> 6);
   const int n = lane & 31, hf = lane >> 5;
   const int Hkv = a.num_kv_heads;
-  const int G = a.group, BQ = pp.block_q, bsl = a.bs_log2, bsm = a.block_size - 1;
+  const int G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
   // One workgroup per (Q-block, kv head) unit, kv head fastest: with
   // round-robin dispatch over the 8 XCDs, the units of one kv head (Hkv =
   // 8) share an XCD and its L2, which serves the K/V re-reads of a
   // sequence's Q-blocks.
-  const int g = blockIdx.x % Hkv;
-  const int wi = blockIdx.x / Hkv;
-  if (wi >= pp.count[0]) return;
-  const int seq = uniform(pp.list_seq[wi]);
-  const int qb = uniform(pp.list_qb[wi]);
-  const int t0 = uniform(a.qsl[seq]);
-  const int qlen = uniform(a.qsl[seq + 1]) - t0;
-  const int L = min(uniform(a.seq_lens[seq]), a.mb * a.block_size);
-  const int ctx = L - qlen;
-  if (ctx < 0 || t0 < 0 || t0 + qlen > a.num_tokens) return;
-  const int tok_lo = qb * BQ;
-  const int tok_hi = min(tok_lo + BQ, qlen);
-  if (tok_lo >= tok_hi) return;
+  const int wg = __builtin_amdgcn_workgroup_id_x();
+  const int g = wg % Hkv;
+  const int wi = wg / Hkv;
+  if (wi >= load_s32(pp.count)) return;
+  // The Q-block's record from the plan kernel, in one scalar load: its
+  // sequence, first token, tokens, and the keys before its first token.
+  const int4 rec = load_rec(pp.rec + wi);
+  const int seq = rec.x;
+  const int t0 = rec.y;        // token of the block's row 0 (rows are relative to it)
+  const int tok_lo = 0;
+  const int tok_hi = rec.z;    // the block's tokens (1 .. BLOCK_Q)
+  const int ctx = rec.w;       // keys before the block's first token
+  if (tok_hi <= 0) return;
   const int kv_len = ctx + tok_hi;                 // keys the block needs
   const int ntiles = (kv_len + kTile - 1) / kTile;
   const int last_blk = (kv_len - 1) >> bsl;

@@ -66,7 +66,8 @@ class pa_plan_info(ctypes.Structure):
                 ("prefill_launch", ctypes.c_int32), ("block_m", ctypes.c_int32),
                 ("block_q", ctypes.c_int32), ("prefill_tile", ctypes.c_int32),
                 ("decode_grid", ctypes.c_int64 * 3), ("merge_grid", ctypes.c_int64 * 3),
-                ("prefill_grid", ctypes.c_int64 * 3), ("workspace_bytes", ctypes.c_uint64)]
+                ("prefill_grid", ctypes.c_int64 * 3), ("prefill_units", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_uint64)]
 
     def as_dict(self):
         d = {}

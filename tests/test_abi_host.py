@@ -211,7 +211,8 @@ def test_plan_prefill_grid_bounds_the_q_blocks():
     # sum ceil(q_i / BLOCK_Q) <= ceil(T / BLOCK_Q) + S
     qs = [2048, 1024, 3000, 517]
     need = sum(-(-q // 64) for q in qs)
-    assert p["prefill_grid"][0] >= need * 8
+    assert p["prefill_units"] >= need * 8
+    assert p["prefill_grid"][0] == p["prefill_units"]   # one workgroup per (Q-block, kv head)
     pf = plan(cfg(32, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3), cus=256, T=6589, S=4, MB=188)
     assert pf["block_m"] == 128 and pf["block_q"] == 32
     p1 = plan(cfg(), T=1, S=1, MB=4)
