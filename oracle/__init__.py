@@ -16,6 +16,12 @@ weight row sums, uniform attention, two-key closed forms, split/merge
 identity, decode == last prefill row, chunked == whole prefill,
 GQA == repeated-head MHA, the fp8 decode table against torch, and the
 paper's 32-tile / 4-segment partition example (Fig. 4).
+
+``cache_write`` is the step before the path (new tokens' K/V into their
+slots, with fp8 quantisation; Sec. 4.2 / Sec. 4.3 take it as done), pinned
+in ``tests/test_oracle_cache_write.py``: its e4m3fn encoder against torch's
+conversion and an exhaustive round trip, write-then-gather identity, skipped
+slots, and the half-step error bound.
 """
 from __future__ import annotations
 
@@ -71,6 +77,11 @@ def _load():
     lib.pa_oracle_bf16_to_f64.restype = D
     lib.pa_oracle_fp8e4m3_to_f64.argtypes = [ctypes.c_uint8]
     lib.pa_oracle_fp8e4m3_to_f64.restype = D
+    lib.pa_oracle_f32_to_fp8e4m3.argtypes = [ctypes.c_float]
+    lib.pa_oracle_f32_to_fp8e4m3.restype = ctypes.c_uint8
+    lib.pa_oracle_cache_write.argtypes = [P, P, I, I, I, I, I, I, I, P, P, P, I, I, ctypes.c_int,
+                                          ctypes.c_float, ctypes.c_float]
+    lib.pa_oracle_cache_write.restype = ctypes.c_int
     lib.pa_oracle_last_error.restype = ctypes.c_char_p
     _lib = lib
     return lib
@@ -246,3 +257,31 @@ def bf16_to_f64(bits: int) -> float:
 
 def fp8e4m3_to_f64(bits: int) -> float:
     return _load().pa_oracle_fp8e4m3_to_f64(int(bits))
+
+
+def f32_to_fp8e4m3(x: float) -> int:
+    """e4m3fn code of the fp32 value x (limited to +-448, nearest, ties to even)."""
+    return int(_load().pa_oracle_f32_to_fp8e4m3(float(x)))
+
+
+def cache_write(key, value, slot_mapping, k_cache, v_cache, k_scale=1.0, v_scale=1.0):
+    """The caches after writing row t of key / value ([T, Hkv, d] bf16) into
+    slot slot_mapping[t] (= block * block_size + offset; slots outside the
+    cache are skipped).  fp8 caches store the e4m3fn code of value / scale
+    (the division in fp32).  Returns two new numpy arrays of the caches'
+    stored bits (uint16 for bf16, uint8 for fp8); the inputs are not changed."""
+    lib = _load()
+    kb, _ = _bits(key)
+    vb, _ = _bits(value)
+    sm, _ = _bits(slot_mapping)
+    sm = np.ascontiguousarray(sm, dtype=np.int32)
+    kc, fp8 = _bits(k_cache)
+    vc, _ = _bits(v_cache)
+    kc = kc.copy()
+    vc = vc.copy()
+    T, Hkv, d = kb.shape
+    NB, bs = kc.shape[0], kc.shape[1]
+    _check(lib.pa_oracle_cache_write(_ptr(kb), _ptr(vb), T, Hkv, d, Hkv * d, d, Hkv * d, d,
+                                     _ptr(sm), _ptr(kc), _ptr(vc), NB, bs, 1 if fp8 else 0,
+                                     float(k_scale), float(v_scale)))
+    return kc, vc

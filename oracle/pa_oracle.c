@@ -407,3 +407,65 @@ int64_t pa_oracle_segment_ranges(int64_t n_tiles, int64_t tps, int64_t *ranges, 
     }
     return nseg;
 }
+
+/* ---- KV-cache write (the step before the path: new tokens' K/V into their
+ * slots; the paper takes it as done, Sec. 4.2 / Sec. 4.3) ------------------ */
+
+/* The e4m3fn code of x: x is first limited to [-448, 448] (the largest
+ * finite magnitude), then the nearest representable value is chosen, ties
+ * to the even code (mantissa bit 0 clear).  Written as the definition: a
+ * search over the 127 non-negative finite codes.  NaN maps to the NaN code
+ * with x's sign. */
+uint8_t pa_oracle_f32_to_fp8e4m3(float x) {
+    if (isnan(x)) return (uint8_t)(signbit(x) ? 0xFF : 0x7F);
+    int neg = signbit(x) ? 1 : 0;
+    double a = fabs((double)x);
+    if (a > 448.0) a = 448.0;
+    int best = 0;
+    double best_err = INFINITY;
+    for (int c = 0; c <= 0x7E; ++c) {
+        double err = fabs(pa_oracle_fp8e4m3_to_f64((uint8_t)c) - a);
+        if (err < best_err || (err == best_err && (c & 1) == 0)) {
+            best = c;
+            best_err = err;
+        }
+    }
+    if (best == 0 && neg) return 0x80;   /* -0 keeps its sign */
+    return (uint8_t)(best | (neg << 7));
+}
+
+/* Write row t of key/value ([T, Hkv, d] bf16 bits, token stride k_tok /
+ * v_tok and head stride k_head / v_head in elements) into slot
+ * slot_mapping[t] = block * bs + offset of the caches [NB, bs, Hkv, d]
+ * (bf16 bits, or fp8 codes of the value divided by k_scale / v_scale in
+ * fp32).  Slots < 0 or >= NB * bs are skipped.  When two tokens name the
+ * same slot, the later one wins. */
+int pa_oracle_cache_write(const uint16_t *key, const uint16_t *value, int64_t T, int64_t Hkv,
+                          int64_t d, int64_t k_tok, int64_t k_head, int64_t v_tok,
+                          int64_t v_head, const int32_t *slot_mapping, void *k_cache,
+                          void *v_cache, int64_t NB, int64_t bs, int kv_fp8, float k_scale,
+                          float v_scale) {
+    if (T < 0 || Hkv < 1 || d < 1 || NB < 0 || bs < 1) return fail("bad cache_write sizes", T, d);
+    if (kv_fp8 && (!(k_scale > 0.0f) || !(v_scale > 0.0f))) return fail("fp8 scales must be > 0", 0, 0);
+    for (int64_t t = 0; t < T; ++t) {
+        int64_t slot = slot_mapping[t];
+        if (slot < 0 || slot >= NB * bs) continue;
+        int64_t blk = slot / bs, off = slot % bs;
+        for (int64_t h = 0; h < Hkv; ++h)
+            for (int64_t i = 0; i < d; ++i) {
+                int64_t dst = ((blk * bs + off) * Hkv + h) * d + i;
+                uint16_t kb = key[t * k_tok + h * k_head + i];
+                uint16_t vb = value[t * v_tok + h * v_head + i];
+                if (kv_fp8) {
+                    float kf = (float)pa_oracle_bf16_to_f64(kb) / k_scale;   /* fp32 division */
+                    float vf = (float)pa_oracle_bf16_to_f64(vb) / v_scale;
+                    ((uint8_t *)k_cache)[dst] = pa_oracle_f32_to_fp8e4m3(kf);
+                    ((uint8_t *)v_cache)[dst] = pa_oracle_f32_to_fp8e4m3(vf);
+                } else {
+                    ((uint16_t *)k_cache)[dst] = kb;
+                    ((uint16_t *)v_cache)[dst] = vb;
+                }
+            }
+    }
+    return 0;
+}
