@@ -192,6 +192,58 @@ def measure(k, steps, warmup):
     return w, res
 
 
+def measure_cache_write(kv, steps, warmup, T=4216, Hkv=8, d=128, bs=16):
+    """pa_cache_write of the mixed batch's 4216 new tokens (Hkv 8, d 128) into a
+    pool of random slots: us per call and GB/s over the bytes it must move
+    (K and V read as bf16, written as bf16 or fp8)."""
+    import torch
+    from paper_2511_11581_amd import pa
+    FP8 = torch.float8_e4m3fn
+    g = torch.Generator(device="cuda").manual_seed(4216)
+    NB = (T + bs - 1) // bs * 4
+    key = torch.randn(T, Hkv, d, device="cuda", generator=g).bfloat16()
+    value = torch.randn(T, Hkv, d, device="cuda", generator=g).bfloat16()
+    slots = torch.randperm(NB * bs, device="cuda", generator=g)[:T].to(torch.int32)
+    cdt = FP8 if kv == "fp8" else torch.bfloat16
+    kc = torch.zeros(NB, bs, Hkv, d, device="cuda", dtype=torch.bfloat16).to(cdt)
+    vc = torch.zeros_like(kc)
+    att = pa.PagedAttention(4 * Hkv, Hkv, d, bs, kv_dtype=cdt, k_scale=0.03, v_scale=0.03,
+                            max_tokens=T, max_seqs=1, max_blocks_per_seq=1)
+    for _ in range(warmup):
+        att.cache_write(key, value, slots, kc, vc)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        att.cache_write(key, value, slots, kc, vc)
+    e1.record()
+    torch.cuda.synchronize()
+    us_eager = e0.elapsed_time(e1) * 1e3 / steps
+    # the same call replayed from a HIP graph: the GPU time without the
+    # per-call host work (argument checks, marshalling) between launches
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        att.cache_write(key, value, slots, kc, vc, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    reps = 20
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            att.cache_write(key, value, slots, kc, vc, stream=torch.cuda.current_stream())
+    graph.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(max(1, steps // reps)):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (max(1, steps // reps) * reps)
+    nbytes = T * Hkv * d * 2 * (2 + (1 if kv == "fp8" else 2)) + T * 4
+    return {"tokens": T, "kv_heads": Hkv, "head_dim": d, "kv": kv, "us": us, "us_eager": us_eager,
+            "GBps": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
+
+
 def cpu_baseline(w, budget_s=15.0, flops=False):
     """The fp64 oracle on the host cores over the first m sequences of the
     batch (m chosen so the run takes about budget_s), in the headline's unit
@@ -275,6 +327,16 @@ def main():
               f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
               f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}", file=sys.stderr)
 
+    cache_write = {}
+    if not args.only:
+        for kv in ("bf16", "fp8"):
+            cw = measure_cache_write(kv, args.steps, args.warmup)
+            cache_write[kv] = cw
+            print(f"# cache write ({cw['tokens']} tokens, Hkv {cw['kv_heads']}, d {cw['head_dim']}, "
+                  f"{kv} cache): {cw['us']:.1f} us per call replayed from a HIP graph "
+                  f"({cw['us_eager']:.1f} us eager), {cw['GBps']:.0f} GB/s "
+                  f"({100 * cw['frac_hbm']:.1f}% HBM)", file=sys.stderr)
+
     decode_like = args.config != 3
     h = headline
     if decode_like:
@@ -307,6 +369,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": roof, "cpu_baseline": cpu,
         "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
+        "cache_write": cache_write,
     }
     print(json.dumps(line))
 

@@ -200,6 +200,23 @@ pa_status pa_debug_gather(pa_handle *h, const pa_tensor *k_cache, const pa_tenso
                           const pa_tensor *block_table, const pa_tensor *seq_lens,
                           const pa_tensor *k_dense, const pa_tensor *v_dense, pa_stream stream);
 
+/* Write the keys and values of new tokens into the paged caches (the step
+ * before attention; arxiv 2511.11581 Sec. 4.2 / 4.3 take it as done).
+ *   key, value      bf16 [T, Hkv, d], last dimension contiguous, rows 16-byte
+ *                   aligned (views into a larger projection output are fine)
+ *   slot_mapping    int32 [T]: slot = block * block_size + offset of token t;
+ *                   slots < 0 (padding) or >= num_blocks * block_size are
+ *                   skipped
+ *   k_cache/v_cache kv_dtype [num_blocks, block_size, Hkv, d] as for pa_forward
+ * bf16 caches receive the bits unchanged; fp8 caches receive the e4m3fn code
+ * of value / k_scale (resp. v_scale) computed in fp32, limited to +-448,
+ * rounded to nearest with ties to even (so that pa_forward's
+ * decode(cache) * scale returns the value).  Two tokens with the same slot
+ * race.  Asynchronous on `stream`; allocates nothing; capturable. */
+pa_status pa_cache_write(pa_handle *h, const pa_tensor *key, const pa_tensor *value,
+                         const pa_tensor *slot_mapping, const pa_tensor *k_cache,
+                         const pa_tensor *v_cache, pa_stream stream);
+
 /* The launch plan pa_forward would use for a batch with these host-visible
  * sizes on a device with num_cus compute units (num_cus <= 0: the handle's
  * device, or 256 without a handle).  Host only; no HIP call.  h may be NULL,

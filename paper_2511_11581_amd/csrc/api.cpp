@@ -677,4 +677,60 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   return PA_OK;
 }
 
+pa_status pa_cache_write(pa_handle* h, const pa_tensor* key, const pa_tensor* value,
+                         const pa_tensor* slot_mapping, const pa_tensor* k_cache,
+                         const pa_tensor* v_cache, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
+  const pa_config& c = h->cfg;
+  TRY(check_tensor(key, "key", PA_DTYPE_BF16, 3));
+  TRY(check_tensor(value, "value", PA_DTYPE_BF16, 3));
+  TRY(check_tensor(slot_mapping, "slot_mapping", PA_DTYPE_I32, 1));
+  TRY(check_tensor(k_cache, "k_cache", c.kv_dtype, 4));
+  TRY(check_tensor(v_cache, "v_cache", c.kv_dtype, 4));
+  const int64_t T = key->shape[0], NB = k_cache->shape[0];
+  for (const pa_tensor* x : {key, value})
+    if (x->shape[0] != T || x->shape[1] != c.num_kv_heads || x->shape[2] != c.head_dim)
+      return fail(PA_ERR_INVALID_ARG, "key and value must be [T, %d, %d]", c.num_kv_heads, c.head_dim);
+  for (const pa_tensor* x : {key, value})
+    if (x->stride[2] != 1 || x->stride[0] % 8 != 0 || x->stride[1] % 8 != 0)
+      return fail(PA_ERR_INVALID_ARG, "key / value: last dim contiguous, token and head strides multiples of 8");
+  if (slot_mapping->shape[0] != T || slot_mapping->stride[0] != 1)
+    return fail(PA_ERR_INVALID_ARG, "slot_mapping must be a contiguous int32 [T]");
+  for (const pa_tensor* kv : {k_cache, v_cache})
+    if (kv->shape[0] != NB || kv->shape[1] != c.block_size || kv->shape[2] != c.num_kv_heads ||
+        kv->shape[3] != c.head_dim || kv->stride[3] != 1)
+      return fail(PA_ERR_INVALID_ARG, "caches must be [num_blocks, %d, %d, %d] with contiguous rows",
+                  c.block_size, c.num_kv_heads, c.head_dim);
+  if (T > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "at most 2^31 - 1 tokens");
+  TRY(check_aligned16(key, "key"));
+  TRY(check_aligned16(value, "value"));
+  TRY(check_aligned16(k_cache, "k_cache"));
+  TRY(check_aligned16(v_cache, "v_cache"));
+  if (T == 0) return PA_OK;
+  pa::CacheWriteArgs a;
+  a.key = static_cast<const uint8_t*>(key->data);
+  a.value = static_cast<const uint8_t*>(value->data);
+  a.k_tok = key->stride[0] * 2;
+  a.k_head = key->stride[1] * 2;
+  a.v_tok = value->stride[0] * 2;
+  a.v_head = value->stride[1] * 2;
+  a.slots = static_cast<const int32_t*>(slot_mapping->data);
+  a.kc = static_cast<uint8_t*>(k_cache->data);
+  a.vc = static_cast<uint8_t*>(v_cache->data);
+  a.kg = geom(k_cache);
+  a.vg = geom(v_cache);
+  a.num_slots = NB * c.block_size;
+  a.num_tokens = (int32_t)T;
+  a.num_kv_heads = c.num_kv_heads;
+  a.head_dim = c.head_dim;
+  a.block_size = c.block_size;
+  a.bs_log2 = __builtin_ctz(c.block_size);
+  a.fp8 = c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 0;
+  a.k_scale = c.k_scale;
+  a.v_scale = c.v_scale;
+  hipError_t e = pa::launch_cache_write(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "cache write launch");
+  return PA_OK;
+}
+
 }  // extern "C"

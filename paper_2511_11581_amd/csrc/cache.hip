@@ -1,0 +1,89 @@
+// KV-cache write: row t of the new keys and values goes to slot
+// slot_mapping[t] = block * block_size + offset of the paged caches
+// [num_blocks, block_size, Hkv, d] (arxiv 2511.11581, Sec. 4.2 paged KV
+// cache, Sec. 4.3 block table; the paper's kernels take this step as done).
+// bf16 caches store the bits unchanged; fp8 caches store the e4m3fn code of
+// value / scale (fp32 division, limited to +-448, then v_cvt_pk_fp8_f32:
+// nearest, ties to even; NaN stays NaN).
+// Slots outside [0, num_blocks * block_size) are skipped.
+//
+// One wave per token (4 per workgroup); each lane loads up to 4 16-byte
+// chunks (8 values) of the token's K and V rows before storing them: a
+// streaming copy, bound by HBM (2 Hkv d * 2 bytes read and 2 Hkv d * (2 or
+// 1) bytes written per token).
+#include "common.hpp"
+#include "kernels.h"
+
+namespace pa {
+
+namespace {
+
+constexpr int kPer = 4;   // chunks per lane in flight (loads before stores)
+
+__device__ __forceinline__ const uint8_t* chunk_src(const CacheWriteArgs& a, int t, int i, int nch,
+                                                    int cpr) {
+  const bool isv = i >= nch;
+  const int j = isv ? i - nch : i;
+  const int h = j / cpr, c = j % cpr;
+  return (isv ? a.value + (int64_t)t * a.v_tok + (int64_t)h * a.v_head
+              : a.key + (int64_t)t * a.k_tok + (int64_t)h * a.k_head) + 16 * c;
+}
+
+__global__ __launch_bounds__(256) void cache_write_kernel(CacheWriteArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);   // one wave per token
+  if (t >= a.num_tokens) return;
+  const int slot = uniform(a.slots[t]);
+  if (slot < 0 || (int64_t)slot >= a.num_slots) return;
+  const int blk = slot >> a.bs_log2, off = slot & (a.block_size - 1);
+  const int cpr = a.head_dim / 8;   // 16-byte input chunks per head row
+  const int nch = a.num_kv_heads * cpr;
+  uint8_t* krow = a.kc + (int64_t)blk * a.kg.blk + (int64_t)off * a.kg.slot;
+  uint8_t* vrow = a.vc + (int64_t)blk * a.vg.blk + (int64_t)off * a.vg.slot;
+  for (int base = 0; base < 2 * nch; base += 64 * kPer) {
+    u32x4 w[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = base + 64 * k + lane;
+      if (i < 2 * nch) w[k] = ld16(chunk_src(a, t, i, nch, cpr));
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = base + 64 * k + lane;
+      if (i >= 2 * nch) continue;
+      const bool isv = i >= nch;
+      const int j = isv ? i - nch : i;
+      const int h = j / cpr, c = j % cpr;
+      uint8_t* dst = isv ? vrow + (int64_t)h * a.vg.head : krow + (int64_t)h * a.kg.head;
+      if (!a.fp8) {
+        *(u32x4*)(dst + 16 * c) = w[k];
+      } else {
+        const float s = isv ? a.v_scale : a.k_scale;
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t bits = (w[k][e >> 1] >> (16 * (e & 1))) & 0xffffu;
+          const float x = __uint_as_float(bits << 16) / s;
+          f[e] = x != x ? x : fminf(fmaxf(x, -448.f), 448.f);
+        }
+        // v_cvt_pk_fp8_f32: two values to e4m3fn, nearest even
+        u32x2 q;
+        q[0] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[0], f[1], 0, false);
+        q[0] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[2], f[3], (int)q[0], true);
+        q[1] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[4], f[5], 0, false);
+        q[1] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(f[6], f[7], (int)q[1], true);
+        *(u32x2*)(dst + 8 * c) = q;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_cache_write(const CacheWriteArgs& a, hipStream_t st) {
+  if (a.num_tokens <= 0) return hipSuccess;
+  cache_write_kernel<<<dim3((unsigned)((a.num_tokens + 3) / 4)), dim3(256), 0, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace pa

@@ -136,6 +136,22 @@ hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim
                           hipStream_t st);
 hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
+
+// KV-cache write (csrc/cache.hip).
+struct CacheWriteArgs {
+  const uint8_t* key;      // bf16 [T, Hkv, d], last dim contiguous
+  const uint8_t* value;
+  int64_t k_tok, k_head, v_tok, v_head;   // input strides (bytes)
+  const int32_t* slots;    // [T] block * block_size + offset; outside the cache: skipped
+  uint8_t* kc;             // caches [NB, bs, Hkv, d] (bf16 or fp8 e4m3fn)
+  uint8_t* vc;
+  KvGeom kg, vg;
+  int64_t num_slots;       // NB * block_size
+  int32_t num_tokens, num_kv_heads, head_dim, block_size, bs_log2;
+  int32_t fp8;
+  float k_scale, v_scale;  // fp8: stored code = e4m3fn(value / scale)
+};
+hipError_t launch_cache_write(const CacheWriteArgs& a, hipStream_t st);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t st);
 
 }  // namespace pa

@@ -41,7 +41,7 @@ KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
 
 # Every function declared in include/pa.h.
-EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
+EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_cache_write", "pa_debug_gather", "pa_plan",
            "pa_decode_pieces", "pa_profile_read", "pa_destroy", "pa_last_error")
 
 
@@ -112,6 +112,7 @@ def load_library(path: str = LIB_PATH):
     lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
     lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, T, P]
+    lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
     lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                             ctypes.POINTER(pa_plan_info)]
     I32P = ctypes.POINTER(ctypes.c_int32)
@@ -244,6 +245,11 @@ def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, k_dense, v_dense
     _check(load_library().pa_debug_gather(h, *(ctypes.byref(d) for d in ds), _stream(stream)))
 
 
+def pa_cache_write(h, key, value, slot_mapping, k_cache, v_cache, stream=None) -> None:
+    ds = [describe(t) for t in (key, value, slot_mapping, k_cache, v_cache)]
+    _check(load_library().pa_cache_write(h, *(ctypes.byref(d) for d in ds), _stream(stream)))
+
+
 class PagedAttention:
     """A handle plus a torch-allocated workspace sized for the given maxima."""
 
@@ -279,6 +285,10 @@ class PagedAttention:
 
     def profile(self, reset: bool = True) -> dict:
         return pa_profile_read(self.handle, reset)
+
+    def cache_write(self, key, value, slot_mapping, k_cache, v_cache, stream=None):
+        """Write new tokens' K/V (bf16 [T, Hkv, d]) into their slots of the caches."""
+        pa_cache_write(self.handle, key, value, slot_mapping, k_cache, v_cache, stream)
 
     def gather(self, k_cache, v_cache, block_table, seq_lens, stream=None):
         S, MB = block_table.shape

@@ -1,0 +1,96 @@
+"""GPU parity of pa_cache_write (new tokens' K/V into their slots; bf16 bits
+unchanged, fp8 as e4m3fn codes of value / scale) against the oracle, byte
+for byte."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_11581_amd import pa
+
+pytestmark = pytest.mark.gpu
+FP8 = torch.float8_e4m3fn
+
+
+def _special(n, g):
+    """Values that decide the e4m3fn rounding: midpoints between codes (ties),
+    subnormals, the saturation edge and signed zeros (all exact in bf16)."""
+    codes = torch.tensor([oracle.fp8e4m3_to_f64(c) for c in range(0x7F)], dtype=torch.float64)
+    mids = ((codes[1:] + codes[:-1]) / 2).float()
+    vals = torch.cat([codes.float(), mids, torch.tensor([448.0, 464.0, 480.0, 1e4, 0.0, 2.0 ** -10,
+                                                          3 * 2.0 ** -10, 2.0 ** -12])])
+    vals = torch.cat([vals, -vals])
+    keep = vals.bfloat16().float() == vals   # exact in bf16 only
+    vals = vals[keep]
+    return vals[torch.randint(0, len(vals), (n,), generator=g)].bfloat16()
+
+
+def _case(T, Hkv, d, bs, NB, kv, ks=1.0, vs=1.0, seed=0, strided=False, special=False):
+    g = torch.Generator().manual_seed(seed)
+    if strided:   # key / value as views into a fused [T, 3 Hkv, d] projection
+        fused = torch.randn(T, 3 * Hkv, d, generator=g).bfloat16()
+        fused_dev = fused.cuda()
+        key_dev, value_dev = fused_dev[:, Hkv:2 * Hkv], fused_dev[:, 2 * Hkv:]
+        key, value = fused[:, Hkv:2 * Hkv], fused[:, 2 * Hkv:]
+    else:
+        key = torch.randn(T, Hkv, d, generator=g).bfloat16()
+        value = torch.randn(T, Hkv, d, generator=g).bfloat16()
+        if special:
+            key = _special(T * Hkv * d, g).view(T, Hkv, d)
+            value = (_special(T * Hkv * d, g).float() * vs).bfloat16().view(T, Hkv, d)
+        key_dev, value_dev = key.cuda(), value.cuda()
+    slots = torch.randperm(NB * bs, generator=g)[:T].to(torch.int32)
+    slots[::7] = -1                                   # padding tokens
+    if T > 3:
+        slots[3] = NB * bs + 5                        # past the cache: skipped
+    if kv == "fp8":
+        kc0 = torch.randint(0, 0x7F, (NB, bs, Hkv, d), generator=g, dtype=torch.uint8).view(FP8)
+        vc0 = torch.randint(0, 0x7F, (NB, bs, Hkv, d), generator=g, dtype=torch.uint8).view(FP8)
+    else:
+        kc0 = torch.randn(NB, bs, Hkv, d, generator=g).bfloat16()
+        vc0 = torch.randn(NB, bs, Hkv, d, generator=g).bfloat16()
+    ek, ev = oracle.cache_write(key, value, slots, kc0, vc0, ks, vs)
+    att = pa.PagedAttention(4 * Hkv, Hkv, d, bs, kv_dtype=FP8 if kv == "fp8" else torch.bfloat16,
+                            k_scale=ks, v_scale=vs, max_tokens=max(T, 1), max_seqs=1,
+                            max_blocks_per_seq=1)
+    kc, vc = kc0.cuda(), vc0.cuda()
+    att.cache_write(key_dev, value_dev, slots.cuda(), kc, vc)
+    torch.cuda.synchronize()
+    view = torch.uint8 if kv == "fp8" else torch.int16
+    gk = kc.cpu().view(view).numpy()
+    gv = vc.cpu().view(view).numpy()
+    if kv != "fp8":
+        gk, gv = gk.view(np.uint16), gv.view(np.uint16)
+    bad = np.argwhere(gk != ek)
+    assert bad.size == 0, f"K mismatch at {bad[:5].tolist()}: gpu {gk[tuple(bad[0])]} oracle {ek[tuple(bad[0])]}"
+    assert np.array_equal(gv, ev), "V mismatch"
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+@pytest.mark.parametrize("Hkv,d", [(8, 128), (2, 64)])
+def test_cache_write_matches_oracle(kv, Hkv, d):
+    _case(T=300, Hkv=Hkv, d=d, bs=16, NB=40, kv=kv, ks=0.05, vs=0.03, seed=Hkv + d)
+
+
+def test_fp8_rounding_ties_subnormals_and_saturation():
+    _case(T=96, Hkv=2, d=64, bs=16, NB=12, kv="fp8", ks=1.0, vs=0.5, seed=11, special=True)
+
+
+def test_strided_views_and_block_size_32():
+    _case(T=77, Hkv=4, d=128, bs=32, NB=9, kv="bf16", seed=3, strided=True)
+    _case(T=77, Hkv=4, d=128, bs=32, NB=9, kv="fp8", ks=0.02, vs=0.02, seed=4, strided=True)
+
+
+def test_full_mixed_batch_token_count():
+    # the mixed batch's 4216 new tokens, Hkv 8, d 128, into a 300-block pool
+    _case(T=4216, Hkv=8, d=128, bs=16, NB=300, kv="bf16", seed=21)
+    _case(T=4216, Hkv=8, d=128, bs=16, NB=300, kv="fp8", ks=0.03, vs=0.04, seed=22)
+
+
+def test_empty_batch_is_a_no_op():
+    att = pa.PagedAttention(8, 2, 64, 16, max_tokens=1, max_seqs=1, max_blocks_per_seq=1)
+    kc = torch.zeros(2, 16, 2, 64, dtype=torch.bfloat16, device="cuda")
+    e = torch.empty(0, 2, 64, dtype=torch.bfloat16, device="cuda")
+    att.cache_write(e, e, torch.empty(0, dtype=torch.int32, device="cuda"), kc, kc.clone())
+    torch.cuda.synchronize()
+    assert int(kc.abs().sum()) == 0
