@@ -286,6 +286,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="headline batch (1..5)")
     ap.add_argument("--only", action="store_true", help="measure the headline batch only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cache-write", action="store_true",
+                    help="only measure pa_cache_write (mixed batch's 4216 tokens, bf16 and fp8 caches)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -309,6 +311,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": max(1, args.steps)}))
+        return
+
+    if args.cache_write:
+        print(json.dumps({kv: measure_cache_write(kv, args.steps, args.warmup) for kv in ("bf16", "fp8")}))
         return
 
     configs = {}
