@@ -244,6 +244,45 @@ def measure_cache_write(kv, steps, warmup, T=4216, Hkv=8, d=128, bs=16):
             "GBps": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
 
 
+def measure_ladder(steps=3, warmup=1):
+    """The ablation of the paper's optimisation ladder on this GPU: the
+    baseline decomposition (one wave per (token, q head), one page per tile)
+    against the full path, for 16 sequences (ctx U[512, 4096], Hq 32 / Hkv 8,
+    d 128, bf16) whose decode share is 0, 50 or 100 % (decode rows q = 1,
+    the others chunked prefill q = 128).  Relative numbers only."""
+    import torch
+    from paper_2511_11581_amd import workloads as W
+    g = torch.Generator().manual_seed(805)
+    ctxs = torch.randint(512, 4097, (16,), generator=g).tolist()
+    res = {}
+    for share in (0, 50, 100):
+        nd = 16 * share // 100
+        seqs = [(c, 1) for c in ctxs[:nd]] + [(c, 128) for c in ctxs[nd:]]
+        w = W.make_batch(seqs, 32, 8, 128, seed=805 + share, name=f"ladder{share}", device="cuda",
+                         poison=False)
+        att = make_attention(w)
+        out = torch.empty_like(w.q)
+        timings = {}
+        for rung, fn in (("baseline", att.forward_baseline), ("full", att.forward)):
+            for _ in range(warmup):
+                fn(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc,
+                   w.scale, out=out)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(steps):
+                fn(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc,
+                   w.scale, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            timings[rung + "_us"] = e0.elapsed_time(e1) * 1e3 / steps
+        timings["speedup"] = timings["baseline_us"] / timings["full_us"]
+        res[str(share)] = timings
+        del w, att, out
+        torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(w, budget_s=15.0, flops=False):
     """The fp64 oracle on the host cores over the first m sequences of the
     batch (m chosen so the run takes about budget_s), in the headline's unit
@@ -343,6 +382,13 @@ def main():
                   f"({cw['us_eager']:.1f} us eager), {cw['GBps']:.0f} GB/s "
                   f"({100 * cw['frac_hbm']:.1f}% HBM)", file=sys.stderr)
 
+    ladder = None
+    if not args.only:
+        ladder = measure_ladder()
+        for share, r in ladder.items():
+            print(f"# ladder, decode share {share}%: baseline decomposition {r['baseline_us']:.0f} us, "
+                  f"full path {r['full_us']:.0f} us ({r['speedup']:.1f}x)", file=sys.stderr)
+
     decode_like = args.config != 3
     h = headline
     if decode_like:
@@ -376,6 +422,7 @@ def main():
         "roofline": roof, "cpu_baseline": cpu,
         "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
         "cache_write": cache_write,
+        "ladder": ladder,
     }
     print(json.dumps(line))
 

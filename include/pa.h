@@ -191,6 +191,17 @@ pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,
                      const pa_tensor *out, pa_stream stream);
 
+/* Ablation only: the same attention as pa_forward, computed with the
+ * paper's baseline decomposition (Sec. 4 / App. A, the first rung of the
+ * optimisation ladder of Sec. 7): one wave per (query token, query head),
+ * the sequence found by binary search over query_start_loc, one page per
+ * key tile, no GQA packing, no split, no matrix cores.  Same arguments,
+ * checks and output as pa_forward; much slower; not for production use. */
+pa_status pa_forward_baseline(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
+                              const pa_tensor *v_cache, const pa_tensor *block_table,
+                              const pa_tensor *seq_lens, const pa_tensor *query_start_loc,
+                              float scale, const pa_tensor *out, pa_stream stream);
+
 /* Debug: copy the stored bytes of every valid K and V row (positions
  * p < seq_lens[i]) in logical order into k_dense / v_dense, both of the
  * cache dtype and shape [S, MB * block_size, Hkv, d], walking the block

@@ -514,10 +514,10 @@ pa_status pa_profile_read(pa_handle* h, pa_profile* out, int reset) {
   return PA_OK;
 }
 
-pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
-                     const pa_tensor* v_cache, const pa_tensor* block_table,
-                     const pa_tensor* seq_lens, const pa_tensor* query_start_loc, float scale,
-                     const pa_tensor* out, pa_stream stream) {
+static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                              const pa_tensor* v_cache, const pa_tensor* block_table,
+                              const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
+                              float scale, const pa_tensor* out, pa_stream stream, bool baseline) {
   if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   const pa_config& c = h->cfg;
   if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
@@ -583,6 +583,11 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   a.sl2 = scale * c.k_scale * 1.4426950408889634f;
   a.v_scale = c.v_scale;
 
+  if (baseline) {
+    hipError_t e = pa::launch_baseline(a, c.head_dim, fp8, st);
+    if (e != hipSuccess) return hip_fail(e, "baseline launch");
+    return PA_OK;
+  }
   if (!p.decode_launch) return PA_OK;
   const int64_t items = p.prefill_launch ? p.prefill_units / c.num_kv_heads : 0;
   const WsLayout wl = ws_layout(c, p.decode_workers, sh.S, items);
@@ -618,6 +623,22 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }
   return PA_OK;
+}
+
+pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                     const pa_tensor* v_cache, const pa_tensor* block_table,
+                     const pa_tensor* seq_lens, const pa_tensor* query_start_loc, float scale,
+                     const pa_tensor* out, pa_stream stream) {
+  return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                      stream, false);
+}
+
+pa_status pa_forward_baseline(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                              const pa_tensor* v_cache, const pa_tensor* block_table,
+                              const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
+                              float scale, const pa_tensor* out, pa_stream stream) {
+  return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                      stream, true);
 }
 
 pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tensor* v_cache,

@@ -152,6 +152,8 @@ struct CacheWriteArgs {
   float k_scale, v_scale;  // fp8: stored code = e4m3fn(value / scale)
 };
 hipError_t launch_cache_write(const CacheWriteArgs& a, hipStream_t st);
+// The paper's baseline decomposition, for the ablation (csrc/baseline.hip).
+hipError_t launch_baseline(const BatchArgs& a, int head_dim, bool fp8, hipStream_t st);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t st);
 
 }  // namespace pa

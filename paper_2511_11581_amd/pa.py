@@ -41,7 +41,7 @@ KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
 
 # Every function declared in include/pa.h.
-EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_cache_write", "pa_debug_gather", "pa_plan",
+EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
            "pa_decode_pieces", "pa_profile_read", "pa_destroy", "pa_last_error")
 
 
@@ -111,6 +111,7 @@ def load_library(path: str = LIB_PATH):
                                        ctypes.POINTER(ctypes.c_uint64)]
     lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
     lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
+    lib.pa_forward_baseline.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, T, P]
     lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
     lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
@@ -239,6 +240,13 @@ def pa_forward(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, s
                                      ctypes.byref(ds[6]), _stream(stream)))
 
 
+def pa_forward_baseline(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale,
+                        out, stream=None) -> None:
+    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
+    _check(load_library().pa_forward_baseline(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
+                                              ctypes.byref(ds[6]), _stream(stream)))
+
+
 def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, k_dense, v_dense,
                     stream=None) -> None:
     ds = [describe(t) for t in (k_cache, v_cache, block_table, seq_lens, k_dense, v_dense)]
@@ -281,6 +289,18 @@ class PagedAttention:
             scale = q.shape[-1] ** -0.5
         pa_forward(self.handle, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
                    scale, out, stream)
+        return out
+
+    def forward_baseline(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
+                         scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                         stream=None):
+        """The same attention with the paper's baseline decomposition (ablation only)."""
+        if out is None:
+            out = torch.empty_like(q)
+        if scale is None:
+            scale = q.shape[-1] ** -0.5
+        pa_forward_baseline(self.handle, q, k_cache, v_cache, block_table, seq_lens,
+                            query_start_loc, scale, out, stream)
         return out
 
     def profile(self, reset: bool = True) -> dict:
