@@ -64,7 +64,10 @@ pa_status fail(pa_status st, const char* fmt, ...) {
 }
 
 constexpr int kMaxCus = 256;
-constexpr int kMinStepsDefault = 1;   // small batches: latency, not the merge, decides
+// Minimum decode share (steps per active worker group), from an offline
+// sweep over 15 decode shapes (1..128 sequences, 1K..32K keys; Sec. 5's
+// tuning exported as a rule): 1 was best or within noise in all but one.
+constexpr int kMinStepsDefault = 1;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
 constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel
