@@ -94,3 +94,37 @@ def test_empty_batch_is_a_no_op():
     att.cache_write(e, e, torch.empty(0, dtype=torch.int32, device="cuda"), kc, kc.clone())
     torch.cuda.synchronize()
     assert int(kc.abs().sum()) == 0
+
+
+def test_cache_write_replays_from_a_hip_graph():
+    # Captured once, replayed with new key / value / slot contents copied into
+    # the captured tensors; every replay is checked against the oracle.
+    T, Hkv, d, bs, NB = 64, 2, 64, 16, 12
+    att = pa.PagedAttention(8, Hkv, d, bs, max_tokens=T, max_seqs=1, max_blocks_per_seq=1)
+    key = torch.zeros(T, Hkv, d, dtype=torch.bfloat16, device="cuda")
+    value = torch.zeros_like(key)
+    slots = torch.zeros(T, dtype=torch.int32, device="cuda")
+    kc = torch.zeros(NB, bs, Hkv, d, dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        att.cache_write(key, value, slots, kc, vc, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        att.cache_write(key, value, slots, kc, vc, stream=torch.cuda.current_stream())
+    for rep in range(3):
+        g = torch.Generator().manual_seed(100 + rep)
+        k_new = torch.randn(T, Hkv, d, generator=g).bfloat16()
+        v_new = torch.randn(T, Hkv, d, generator=g).bfloat16()
+        s_new = torch.randperm(NB * bs, generator=g)[:T].to(torch.int32)
+        before_k, before_v = kc.cpu(), vc.cpu()
+        key.copy_(k_new)
+        value.copy_(v_new)
+        slots.copy_(s_new)
+        graph.replay()
+        torch.cuda.synchronize()
+        ek, ev = oracle.cache_write(k_new, v_new, s_new, before_k, before_v)
+        assert np.array_equal(kc.cpu().view(torch.int16).numpy().view(np.uint16), ek), f"replay {rep}"
+        assert np.array_equal(vc.cpu().view(torch.int16).numpy().view(np.uint16), ev), f"replay {rep}"
