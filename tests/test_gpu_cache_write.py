@@ -128,3 +128,26 @@ def test_cache_write_replays_from_a_hip_graph():
         ek, ev = oracle.cache_write(k_new, v_new, s_new, before_k, before_v)
         assert np.array_equal(kc.cpu().view(torch.int16).numpy().view(np.uint16), ek), f"replay {rep}"
         assert np.array_equal(vc.cpu().view(torch.int16).numpy().view(np.uint16), ev), f"replay {rep}"
+
+
+def test_cache_write_rejects_bad_arguments():
+    # checked on the host before any launch; the caches stay untouched
+    att = pa.PagedAttention(8, 2, 64, 16, max_tokens=8, max_seqs=1, max_blocks_per_seq=1)
+    kc = torch.zeros(4, 16, 2, 64, dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    key = torch.randn(8, 2, 64, device="cuda").bfloat16()
+    slots = torch.arange(8, dtype=torch.int32, device="cuda")
+    bad = [
+        (key.float(), key, slots, kc, vc),                                  # key not bf16
+        (key[:, :1], key[:, :1], slots, kc, vc),                            # wrong head count
+        (key, key, slots.long(), kc, vc),                                   # slots not int32
+        (key, key, slots[:4], kc, vc),                                      # slots shorter than T
+        (key, key, slots, kc.float(), vc),                                  # cache dtype != handle's
+        (key, key, slots, kc[:, :8], vc),                                   # block size mismatch
+        (key.transpose(1, 2).contiguous().transpose(1, 2), key, slots, kc, vc),   # d not contiguous
+    ]
+    for args in bad:
+        with pytest.raises(pa.PaError):
+            att.cache_write(*args)
+    torch.cuda.synchronize()
+    assert int(kc.float().abs().sum()) == 0 and int(vc.float().abs().sum()) == 0
