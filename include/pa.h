@@ -222,8 +222,12 @@ pa_status pa_debug_gather(pa_handle *h, const pa_tensor *k_cache, const pa_tenso
  * bf16 caches receive the bits unchanged; fp8 caches receive the e4m3fn code
  * of value / k_scale (resp. v_scale) computed in fp32, limited to +-448,
  * rounded to nearest with ties to even (so that pa_forward's
- * decode(cache) * scale returns the value).  Two tokens with the same slot
- * race.  Asynchronous on `stream`; allocates nothing; capturable. */
+ * decode(cache) * scale returns the value).  Every new token owns its slot
+ * (Sec. 4.3): slot_mapping must not name one slot twice among its non-skipped
+ * entries; if it does, that slot ends up holding an unspecified mix of the
+ * tokens' 16-byte chunks (the tokens are written concurrently) and the call
+ * still returns PA_OK.  Asynchronous on `stream`; allocates nothing;
+ * capturable. */
 pa_status pa_cache_write(pa_handle *h, const pa_tensor *key, const pa_tensor *value,
                          const pa_tensor *slot_mapping, const pa_tensor *k_cache,
                          const pa_tensor *v_cache, pa_stream stream);

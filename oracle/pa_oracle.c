@@ -164,14 +164,17 @@ static void row_attend(const problem *P, int64_t i, int64_t t, int64_t h, int64_
         acc_add(&l, s[p]);
     }
     double lsum = acc_get(&l);
-    for (int64_t x = 0; x < P->d; ++x) {
-        acc_t o = {0, 0};
-        for (int64_t p = 0; p < nkeys; ++p) {
-            int64_t blk = P->block_table[i * P->MB + p / P->bs];
-            acc_add(&o, s[p] * kv_at(P, P->v_cache, P->v_scale, blk, p % P->bs, g, x));
-        }
-        out[x] = acc_get(&o) / lsum;
+    /* out[x] = sum_p w_p V[p, x] / l: one compensated sum per x, each taking
+     * the keys in increasing order (keys in the outer loop, so that a key's
+     * V row is read once). */
+    acc_t *o = (acc_t *)calloc((size_t)P->d, sizeof(acc_t));
+    for (int64_t p = 0; p < nkeys; ++p) {
+        int64_t blk = P->block_table[i * P->MB + p / P->bs];
+        for (int64_t x = 0; x < P->d; ++x)
+            acc_add(&o[x], s[p] * kv_at(P, P->v_cache, P->v_scale, blk, p % P->bs, g, x));
     }
+    for (int64_t x = 0; x < P->d; ++x) out[x] = acc_get(&o[x]) / lsum;
+    free(o);
     if (lse) *lse = m + log(lsum);
     if (weights)
         for (int64_t p = 0; p < nkeys; ++p) weights[p] = s[p] / lsum;
@@ -179,10 +182,17 @@ static void row_attend(const problem *P, int64_t i, int64_t t, int64_t h, int64_
 
 /* ---- threaded full forward --------------------------------------------- */
 
+/* Work unit: one query token row t and one kv head g (its G query heads),
+ * handed out most keys first. */
+typedef struct {
+    int64_t keys, unit; /* unit = t * Hkv + g */
+} unit_t;
+
 typedef struct {
     const problem *P;
     double *out, *lse;
-    int64_t *units; /* (i * Hkv + g), longest first */
+    unit_t *units;
+    int64_t *seq; /* sequence owning each token row, -1 for rows past qsl[S] */
     int64_t nunits;
     int64_t next;
     pthread_mutex_t mu;
@@ -198,33 +208,24 @@ static void *worker(void *arg) {
     int64_t G = P->Hq / P->Hkv;
     for (;;) {
         pthread_mutex_lock(&J->mu);
-        int64_t u = J->next < J->nunits ? J->units[J->next++] : -1;
+        int64_t u = J->next < J->nunits ? J->units[J->next++].unit : -1;
         pthread_mutex_unlock(&J->mu);
         if (u < 0) break;
-        int64_t i = u / P->Hkv, g = u % P->Hkv;
+        int64_t t = u / P->Hkv, g = u % P->Hkv, i = J->seq[t];
         int64_t t0 = P->qsl[i], q = P->qsl[i + 1] - t0, L = P->seq_lens[i], c = L - q;
-        for (int64_t j = 0; j < q; ++j)
-            for (int64_t h = g * G; h < (g + 1) * G; ++h) {
-                int64_t t = t0 + j;
-                row_attend(P, i, t, h, c + j + 1, s, J->out + (t * P->Hq + h) * P->d,
-                           J->lse ? J->lse + t * P->Hq + h : NULL, NULL);
-            }
+        int64_t j = t - t0;
+        for (int64_t h = g * G; h < (g + 1) * G; ++h)
+            row_attend(P, i, t, h, c + j + 1, s, J->out + (t * P->Hq + h) * P->d,
+                       J->lse ? J->lse + t * P->Hq + h : NULL, NULL);
     }
     free(s);
     return NULL;
 }
 
-static const problem *g_sort_P;
 static int cmp_units(const void *a, const void *b) {
-    const problem *P = g_sort_P;
-    int64_t ua = *(const int64_t *)a, ub = *(const int64_t *)b;
-    int64_t ia = ua / P->Hkv, ib = ub / P->Hkv;
-    /* cost ~ q * L */
-    double ca = (double)(P->qsl[ia + 1] - P->qsl[ia]) * P->seq_lens[ia];
-    double cb = (double)(P->qsl[ib + 1] - P->qsl[ib]) * P->seq_lens[ib];
-    if (ca > cb) return -1;
-    if (ca < cb) return 1;
-    return ua < ub ? -1 : (ua > ub);
+    const unit_t *x = (const unit_t *)a, *y = (const unit_t *)b;
+    if (x->keys != y->keys) return x->keys > y->keys ? -1 : 1;
+    return x->unit < y->unit ? -1 : (x->unit > y->unit);
 }
 
 #define PROBLEM_ARGS                                                                     \
@@ -248,11 +249,19 @@ int pa_oracle_forward(PROBLEM_ARGS, double *out, double *lse, int num_threads) {
     J.P = &P;
     J.out = out;
     J.lse = lse;
-    J.nunits = P.S * P.Hkv;
-    J.units = (int64_t *)malloc(sizeof(int64_t) * (size_t)(J.nunits > 0 ? J.nunits : 1));
-    for (int64_t u = 0; u < J.nunits; ++u) J.units[u] = u;
-    g_sort_P = &P;
-    qsort(J.units, (size_t)J.nunits, sizeof(int64_t), cmp_units);
+    int64_t rows = P.S > 0 ? P.qsl[P.S] : 0;
+    J.seq = (int64_t *)malloc(sizeof(int64_t) * (size_t)(rows > 0 ? rows : 1));
+    for (int64_t i = 0; i < P.S; ++i)
+        for (int64_t t = P.qsl[i]; t < P.qsl[i + 1]; ++t) J.seq[t] = i;
+    J.nunits = rows * P.Hkv;
+    J.units = (unit_t *)malloc(sizeof(unit_t) * (size_t)(J.nunits > 0 ? J.nunits : 1));
+    for (int64_t u = 0; u < J.nunits; ++u) {
+        int64_t t = u / P.Hkv, i = J.seq[t];
+        int64_t q = P.qsl[i + 1] - P.qsl[i];
+        J.units[u].keys = (P.seq_lens[i] - q) + (t - P.qsl[i]) + 1;
+        J.units[u].unit = u;
+    }
+    qsort(J.units, (size_t)J.nunits, sizeof(unit_t), cmp_units);
     J.next = 0;
     pthread_mutex_init(&J.mu, NULL);
     int nt = num_threads > 0 ? num_threads : 1;
@@ -262,6 +271,7 @@ int pa_oracle_forward(PROBLEM_ARGS, double *out, double *lse, int num_threads) {
     pthread_mutex_destroy(&J.mu);
     free(th);
     free(J.units);
+    free(J.seq);
     return ORACLE_OK;
 }
 
@@ -438,8 +448,9 @@ uint8_t pa_oracle_f32_to_fp8e4m3(float x) {
  * v_tok and head stride k_head / v_head in elements) into slot
  * slot_mapping[t] = block * bs + offset of the caches [NB, bs, Hkv, d]
  * (bf16 bits, or fp8 codes of the value divided by k_scale / v_scale in
- * fp32).  Slots < 0 or >= NB * bs are skipped.  When two tokens name the
- * same slot, the later one wins. */
+ * fp32).  Slots < 0 or >= NB * bs are skipped.  Every new token owns its
+ * own slot (Sec. 4.3: the block table gives each token position one slot),
+ * so a mapping that names one slot twice is rejected. */
 int pa_oracle_cache_write(const uint16_t *key, const uint16_t *value, int64_t T, int64_t Hkv,
                           int64_t d, int64_t k_tok, int64_t k_head, int64_t v_tok,
                           int64_t v_head, const int32_t *slot_mapping, void *k_cache,
@@ -447,6 +458,12 @@ int pa_oracle_cache_write(const uint16_t *key, const uint16_t *value, int64_t T,
                           float v_scale) {
     if (T < 0 || Hkv < 1 || d < 1 || NB < 0 || bs < 1) return fail("bad cache_write sizes", T, d);
     if (kv_fp8 && (!(k_scale > 0.0f) || !(v_scale > 0.0f))) return fail("fp8 scales must be > 0", 0, 0);
+    for (int64_t t = 0; t < T; ++t) {
+        int64_t slot = slot_mapping[t];
+        if (slot < 0 || slot >= NB * bs) continue;
+        for (int64_t u = 0; u < t; ++u)
+            if (slot_mapping[u] == slot) return fail("two tokens name the same slot", u, t);
+    }
     for (int64_t t = 0; t < T; ++t) {
         int64_t slot = slot_mapping[t];
         if (slot < 0 || slot >= NB * bs) continue;

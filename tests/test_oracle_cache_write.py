@@ -99,3 +99,40 @@ def test_fp8_write_is_within_half_a_step_of_the_value():
         assert np.all(np.abs(np.abs(got) - xa) <= step / 2 + 1e-12)
         ref = torch.from_numpy((key[t].float() / ks).numpy()).clamp(-448, 448).to(FP8).view(torch.uint8).numpy()
         assert np.array_equal(k2.reshape(-1, 2, 16)[s], ref)
+
+
+def test_fp8_v_half_uses_v_scale():
+    # Library pin of the V branch: the stored V codes are torch's e4m3fn
+    # conversion of value / v_scale (fp32 division, limited to +-448), with
+    # v_scale different from k_scale, so a swapped or shared scale fails.
+    key, value, slots = _batch(seed=6)
+    kc = torch.zeros(11, 16, 2, 16, dtype=torch.uint8)
+    vc = torch.zeros_like(kc)
+    ks, vs = 0.02, 0.0037
+    k2, v2 = oracle.cache_write(key, value, slots, kc, vc, ks, vs)
+    for t, s in enumerate(slots.tolist()):
+        vref = (value[t].float() / vs).clamp(-448, 448).to(FP8).view(torch.uint8).numpy()
+        kref = (key[t].float() / ks).clamp(-448, 448).to(FP8).view(torch.uint8).numpy()
+        assert np.array_equal(v2.reshape(-1, 2, 16)[s], vref)
+        assert np.array_equal(k2.reshape(-1, 2, 16)[s], kref)
+    # large values saturate to the largest finite code on the V side too
+    big = value.clone()
+    big[0] = 1000.0
+    _, v3 = oracle.cache_write(key, big, slots, kc, vc, ks, vs)
+    row = v3.reshape(-1, 2, 16)[int(slots[0])]
+    assert np.all((row & 0x7F) == 0x7E)
+
+
+def test_duplicate_slots_are_rejected():
+    # Every new token owns its own slot (Sec. 4.3); a mapping that names one
+    # slot twice has no single result and is refused.  Skipped (negative or
+    # out-of-range) slots may repeat.
+    key, value, slots = _batch(T=8)
+    kc = torch.zeros(11, 16, 2, 16).to(torch.bfloat16)
+    slots[5] = slots[2]
+    with pytest.raises(oracle.OracleError, match="same slot"):
+        oracle.cache_write(key, value, slots, kc, kc.clone())
+    slots[5] = -1
+    slots[6] = -1
+    slots[7] = 11 * 16 + 3
+    oracle.cache_write(key, value, slots, kc, kc.clone())

@@ -15,7 +15,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "pa_oracle.c")
-PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
+PINS = [os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+        os.path.join(ROOT, "tests", "test_oracle_cache_write.py")]
 
 # (name, original text, planted text, occurrences replaced)
 MUTANTS = [
@@ -32,12 +33,12 @@ MUTANTS = [
     ("bf16_shift_wrong", "((uint32_t)bits) << 16", "((uint32_t)bits) << 15", 1),
     ("v_scale_missing", "kv_at(P, P->v_cache, P->v_scale,", "kv_at(P, P->v_cache, 1.0,", 1),
     ("k_scale_on_v", "kv_at(P, P->v_cache, P->v_scale,", "kv_at(P, P->v_cache, P->k_scale,", 1),
-    ("normalisation_missing", "out[x] = acc_get(&o) / lsum;", "out[x] = acc_get(&o);", 1),
+    ("normalisation_missing", "out[x] = acc_get(&o[x]) / lsum;", "out[x] = acc_get(&o[x]);", 1),
     ("lse_not_logged", "*lse = m + log(lsum);", "*lse = m + lsum;", 1),
     ("table_row_stride", "P->block_table[i * P->MB + p / P->bs]", "P->block_table[i * P->bs + p / P->bs]", 2),
     ("slot_index", "int64_t slot = p % P->bs;", "int64_t slot = (p + 1) % P->bs;", 1),
-    ("v_uses_k_cache", "kv_at(P, P->v_cache, P->v_scale, blk, p % P->bs, g, x));\n        }\n        out[x]",
-     "kv_at(P, P->k_cache, P->v_scale, blk, p % P->bs, g, x));\n        }\n        out[x]", 1),
+    ("v_uses_k_cache", "acc_add(&o[x], s[p] * kv_at(P, P->v_cache, P->v_scale,",
+     "acc_add(&o[x], s[p] * kv_at(P, P->k_cache, P->v_scale,", 1),
     ("q_head_transposed", "P->q + (t * P->Hq + h) * P->d", "P->q + (h * P->T + t) * P->d", 1),
     ("merge_weight_dropped", "acc_add(&den, exp(m[k] - M) * l[k]);", "acc_add(&den, l[k]);", 1),
     ("merge_numerator_unscaled", "acc_add(&num, exp(m[k] - M) * acc[k * d + x]);",
@@ -50,6 +51,13 @@ MUTANTS = [
      "if (blk < 0) return fail(\"block id out of range\", i, blk);", 1),
     ("gather_slot", "int64_t src = ((int64_t)blk * block_size + p % block_size) * row;",
      "int64_t src = ((int64_t)blk * block_size + p / block_size) * row;", 1),
+    ("cache_write_v_uses_k_scale", "float vf = (float)pa_oracle_bf16_to_f64(vb) / v_scale;",
+     "float vf = (float)pa_oracle_bf16_to_f64(vb) / k_scale;", 1),
+    ("cache_write_v_unscaled", "float vf = (float)pa_oracle_bf16_to_f64(vb) / v_scale;",
+     "float vf = (float)pa_oracle_bf16_to_f64(vb);", 1),
+    ("cache_write_duplicates_accepted", "if (slot_mapping[u] == slot) return fail(",
+     "if (slot_mapping[u] == slot && 0) return fail(", 1),
+    ("fp8_encoder_ties_to_odd", "(err == best_err && (c & 1) == 0)", "(err == best_err && (c & 1) == 1)", 1),
 ]
 
 
@@ -66,7 +74,7 @@ def _run_mutant(tmp, name, old, new, count):
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-shared", "-fPIC", "-o", so, c,
                            "-lpthread", "-lm"])
     env = dict(os.environ, PA_ORACLE_LIB=so)
-    r = subprocess.run([sys.executable, "-m", "pytest", PINS, "-x", "-q", "-p", "no:cacheprovider"],
+    r = subprocess.run([sys.executable, "-m", "pytest", *PINS, "-x", "-q", "-p", "no:cacheprovider"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
     return name, r.returncode, r.stdout[-400:]
 
