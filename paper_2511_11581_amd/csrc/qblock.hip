@@ -13,9 +13,10 @@
 // the scores of tile t + 1, then O += V^T P^T of tile t with the softmax of
 // tile t + 1 (one exp, one pack and one dot2 per weight) placed between its
 // products, so that the VALU work runs under the wave's own products; the
-// second wave on the SIMD does the same.  Q carries scale * log2(e) and the
-// score products start from -m, so no per-weight arithmetic precedes the
-// exp.
+// second wave on the SIMD does the same.  The score products start from
+// -m / c (c = scale * log2(e)), so one multiply by c precedes each exp; Q
+// enters the products unchanged (rounding Q * c to bf16 would add a relative
+// error of 2^-9 to every score, which grows with the logit).
 //
 // K/V tiles of 64 keys move from HBM into a ring of 4 LDS stages with
 // global_load_lds_dwordx4 (no staging registers, no VALU), three tiles
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   const int n = lane & 31, hf = lane >> 5;
   const int Hkv = a.num_kv_heads;
   const int G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
+  const float c = a.sl2, inv_c = 1.f / a.sl2;   // scale * log2(e) (* k_scale)
   // One workgroup per (Q-block, kv head) unit, kv head fastest: with
   // round-robin dispatch over the 8 XCDs, the units of one kv head (Hkv =
   // 8) share an XCD and its L2, which serves the K/V re-reads of a
@@ -264,7 +266,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 
   f32x16 o[NDB];     // O^T accumulators
   f32x16 s[2];       // S^T of one tile (two 32-key halves), relative to m_run
-  f32x16 nm;         // -m_run in every element: the score products start from it
+  f32x16 nm;         // -m_run / c in every element: the score products start from it
   bf16x8 pb[4];      // P^T operands (four 16-key steps)
   float m_run = 0.f, l_run = 0.f;
   float psum = 0.f;                   // row sum of the tile in progress
@@ -275,11 +277,11 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
 
-  // ---- softmax pieces.  Q carries the factor scale * log2(e), so a score
-  //      product started from nm = -m_run leaves s = S scale log2(e) - m_run
-  //      and the weight is 2^s with no further arithmetic.  Element e is
-  //      s[e / 16][e % 16], key 8(e % 16 / 4) + 4 hf + e % 4 + 32 (e / 16) of
-  //      the tile.  Causal mask of tile t (tiles crossing a diagonal only):
+  // ---- softmax pieces.  A score product started from nm = -m_run / c
+  //      leaves s = S - m_run / c (S = q . k, c = scale * log2(e)), and the
+  //      weight is 2^(c s) = 2^(c S - m_run).  Element e is s[e / 16][e % 16],
+  //      key 8(e % 16 / 4) + 4 hf + e % 4 + 32 (e / 16) of the tile.  Causal
+  //      mask of tile t (tiles crossing a diagonal only):
   auto mask = [&](int t) {
     const int lim = pos - t * kTile - 4 * hf;
 #pragma unroll
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       for (int i = 0; i < 16; ++i)
         s[kb][i] = (32 * kb + 8 * (i >> 2) + (i & 3)) <= lim ? s[kb][i] : kNegInf;
   };
-  // Weights of elements 8u .. 8u + 7, 2^(s - d), to the bf16 operand pb[u];
+  // Weights of elements 8u .. 8u + 7, 2^(c s - d), to the bf16 operand pb[u];
   // the row sum adds the rounded weights (the ones the products use) with
   // dot2.  (Used where the reference moves; the products' schedule splits
   // the d = 0 case into exp_pair and pack_group below.)
@@ -297,7 +299,8 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     u32x4 pw;
 #pragma unroll
     for (int h = 0; h < 4; ++h)
-      pw[h] = pack_bf16(fast_exp2(s[kb][i0 + 2 * h] - d), fast_exp2(s[kb][i0 + 2 * h + 1] - d));
+      pw[h] = pack_bf16(fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h], c, -d)),
+                        fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h + 1], c, -d)));
     pb[u] = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
     for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
@@ -308,8 +311,8 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   float ex[8];
   auto exp_pair = [&](int u, int h) {
     const int kb = u >> 1, i0 = 8 * (u & 1);
-    ex[2 * h] = fast_exp2(s[kb][i0 + 2 * h]);
-    ex[2 * h + 1] = fast_exp2(s[kb][i0 + 2 * h + 1]);
+    ex[2 * h] = fast_exp2(s[kb][i0 + 2 * h] * c);
+    ex[2 * h + 1] = fast_exp2(s[kb][i0 + 2 * h + 1] * c);
   };
   auto pack_group = [&](int u) {
     u32x4 pw;
@@ -319,7 +322,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
     for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
   };
-  // Row max of the tile (relative to m_run), across the lane pair.
+  // Row max of the tile in log2 units relative to m_run, across the lane pair.
   auto tile_max = [&]() {
     float mA = kNegInf, mB = kNegInf;
 #pragma unroll
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       mA = fmaxf(fmaxf(mA, s[0][i]), s[0][i + 1]);
       mB = fmaxf(fmaxf(mB, s[1][i]), s[1][i + 1]);
     }
-    return xor32_max(fmaxf(mA, mB));
+    return xor32_max(fmaxf(mA, mB)) * c;
   };
   // End of a tile's softmax.  The reference is kept while every weight of
   // the row stays below 2^12 (the lane's 32-key sum tells); otherwise it
@@ -345,7 +348,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
       for (int u = 0; u < 4; ++u) group(u, d);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) nm[i] = -m_run;
+      for (int i = 0; i < 16; ++i) nm[i] = -m_run * inv_c;
     }
     l_run += psum;
     psum = 0.f;
@@ -427,17 +430,6 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     else if (ntiles == 2) wait_vm_lds<ND>();
     else wait_vm_lds<0>();
   };
-  // While the first tiles fly: scores come out in log2 units, Q times
-  // scale * log2(e), rounded to bf16 (a relative change below 2^-9 per
-  // element).
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    u32x4 w = __builtin_bit_cast(u32x4, qt[t]);
-#pragma unroll
-    for (int h = 0; h < 4; ++h)
-      w[h] = pack_bf16(__uint_as_float(w[h] << 16) * a.sl2, __uint_as_float(w[h] & 0xffff0000u) * a.sl2);
-    qt[t] = __builtin_bit_cast(bf16x8, w);
-  }
   wait_first();
   if (ntiles == 1) zero_tail(0);
   wait_first();
@@ -457,7 +449,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   l_run = psum;
   psum = 0.f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) nm[i] = -m_run;
+  for (int i = 0; i < 16; ++i) nm[i] = -m_run * inv_c;
 
   // ---- tile periods.  sync(t): tile t + 1 has landed for every wave and
   //      every wave has finished period t - 1, so the stage of tile t - 1

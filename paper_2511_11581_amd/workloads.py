@@ -98,23 +98,30 @@ class Workload:
             query_start_loc=f(self.query_start_loc))
 
 
-def _fill_normal(shape, gen, device, out_dtype, chunk=1 << 26):
-    """N(0,1) fp32 draws rounded to ``out_dtype``, drawn in chunks."""
+def _fill_normal(shape, gen, device, out_dtype, chunk=1 << 26, mult=1.0):
+    """N(0,1) fp32 draws (times ``mult``) rounded to ``out_dtype``, drawn in chunks."""
     n = math.prod(shape)
     out = torch.empty(n, dtype=out_dtype, device=device)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
-        out[s:e] = torch.randn(e - s, generator=gen, device=device, dtype=torch.float32).to(out_dtype)
+        x = torch.randn(e - s, generator=gen, device=device, dtype=torch.float32)
+        if mult != 1.0:
+            x = x * mult
+        out[s:e] = x.to(out_dtype)
     return out.view(*shape)
 
 
-def _fill_fp8(shape, gen, device, chunk=1 << 26):
-    """N(0,1) fp32 draws quantised per tensor to e4m3fn; returns (tensor, scale)."""
+def _fill_fp8(shape, gen, device, chunk=1 << 26, plant=None):
+    """N(0,1) fp32 draws quantised per tensor to e4m3fn; returns (tensor, scale).
+    ``plant`` may overwrite rows of the fp32 draws (viewed with ``shape``)
+    before the scale is taken."""
     n = math.prod(shape)
     x = torch.empty(n, dtype=torch.float32, device=device)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
         x[s:e] = torch.randn(e - s, generator=gen, device=device, dtype=torch.float32)
+    if plant is not None:
+        plant(x.view(*shape))
     amax = float(x.abs().max()) if n else 1.0
     scale = amax / FP8_MAX if amax > 0 else 1.0
     out = torch.empty(n, dtype=FP8, device=device)
@@ -130,12 +137,19 @@ def make_batch(seqs: Sequence[Tuple[int, int]], num_q_heads: int, num_kv_heads: 
                pool_blocks: Optional[int] = None, poison: bool = True, device="cpu",
                table_width: Optional[int] = None, token_pad: int = 0,
                name: str = "custom", scale: Optional[float] = None,
+               q_scale: float = 1.0, spikes: Sequence[Tuple[int, int, int, float]] = (),
                _gen: Optional[torch.Generator] = None) -> Workload:
     """Build a paged batch from explicit (context_len, query_len) pairs.
 
     ``pool_blocks`` defaults to the blocks the batch needs; ``table_width``
     defaults to the longest sequence's block count; ``token_pad`` appends
-    query rows past ``query_start_loc[S]`` that no sequence owns."""
+    query rows past ``query_start_loc[S]`` that no sequence owns.
+
+    Large logits: ``q_scale`` multiplies the fp32 Q draws before rounding.
+    ``spikes`` plants keys aligned with a query: for (i, p, j, c), key
+    position p of sequence i gets, in every kv head g, c times the mean of
+    the G query rows of token j of sequence i in that group, so those rows
+    score it far above the rest (set before rounding / quantisation)."""
     gen = _gen if _gen is not None else torch.Generator().manual_seed(seed)
     ctx = [int(c) for c, _ in seqs]
     ql = [int(q) for _, q in seqs]
@@ -161,14 +175,27 @@ def make_batch(seqs: Sequence[Tuple[int, int]], num_q_heads: int, num_kv_heads: 
     T = int(qsl[-1]) + token_pad
 
     vgen = torch.Generator(device=device).manual_seed(seed + 1)
-    q = _fill_normal((T, num_q_heads, head_dim), vgen, device, torch.bfloat16)
+    q = _fill_normal((T, num_q_heads, head_dim), vgen, device, torch.bfloat16, mult=q_scale)
     shape = (NB, block_size, num_kv_heads, head_dim)
+    G = num_q_heads // num_kv_heads
+
+    def plant(kx):
+        # kx: [NB, bs, Hkv, d] (fp32 draws or the bf16 cache)
+        for (i, p, j, c) in spikes:
+            if not (0 <= p < L[i] and 0 <= j < ql[i]):
+                raise ValueError(f"spike {(i, p, j)} outside sequence {i}")
+            page, slot = int(table[i, p // block_size]), p % block_size
+            qrow = q[int(qsl[i]) + j].float().view(num_kv_heads, G, head_dim).mean(1)
+            kx[page, slot] = (c * qrow).to(kx.dtype)
+
     if kv_dtype == "bf16":
         k = _fill_normal(shape, vgen, device, torch.bfloat16)
         v = _fill_normal(shape, vgen, device, torch.bfloat16)
+        if spikes:
+            plant(k)
         ks = vs = 1.0
     elif kv_dtype == "fp8":
-        k, ks = _fill_fp8(shape, vgen, device)
+        k, ks = _fill_fp8(shape, vgen, device, plant=plant if spikes else None)
         v, vs = _fill_fp8(shape, vgen, device)
     else:
         raise ValueError(f"unknown kv_dtype {kv_dtype}")

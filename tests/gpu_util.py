@@ -1,7 +1,9 @@
 """Helpers shared by the GPU tests: run the HIP path through the C ABI and
 compare with the fp64 oracle."""
 import concurrent.futures as cf
+import contextlib
 import os
+import zlib
 
 import numpy as np
 import torch
@@ -12,6 +14,27 @@ from paper_2511_11581_amd import pa
 SENTINEL = 7.0  # written into out before a call; rows the call must not touch keep it
 
 TOL = {False: (2e-2, 2e-3), True: (5e-2, 5e-3)}  # (max abs, mean abs) for bf16 / fp8 KV
+LOG2E = 1.4426950408889634
+
+
+def seed_of(name: str) -> int:
+    """A seed that is the same in every process (str hashes are not)."""
+    return zlib.crc32(name.encode()) % 100000
+
+
+@contextlib.contextmanager
+def decode_min_steps(n):
+    """Handles created inside take the decode minimum share n (the planner
+    knob PA_DECODE_MIN_STEPS, read when a handle is created)."""
+    old = os.environ.get("PA_DECODE_MIN_STEPS")
+    os.environ["PA_DECODE_MIN_STEPS"] = str(n)
+    try:
+        yield
+    finally:
+        if old is None:
+            del os.environ["PA_DECODE_MIN_STEPS"]
+        else:
+            os.environ["PA_DECODE_MIN_STEPS"] = old
 
 
 def attention_for(w, validate=False, max_tokens=None, max_seqs=None, max_blocks=None):
@@ -92,3 +115,39 @@ def sample_rows(w, n, seed=0):
     while len(rows) < n and T > 0:
         rows.add((int(rng.integers(T)), int(rng.integers(w.num_q_heads))))
     return sorted(rows)
+
+
+def row_scores_log2(w, rows):
+    """Per-key scores of each (token, head) row in log2 units, from the
+    oracle's normalised weights and log-sum-exp: s_p = (lse + ln w_p) log2(e).
+    Returns a list of 1-D arrays (one per row, over the row's visible keys)."""
+    wc = cpu_inputs(w)
+    rows = np.asarray(rows, dtype=np.int64).reshape(-1, 2)
+    qsl = wc.query_start_loc.numpy()
+    sl = wc.seq_lens.numpy()
+    maxk = int(sl.max()) if len(sl) else 1
+    _, lse, wt = oracle.rows(wc.q, wc.k_cache, wc.v_cache, wc.block_table, wc.seq_lens,
+                             wc.query_start_loc, wc.scale, rows, k_scale=wc.k_scale,
+                             v_scale=wc.v_scale, with_lse=True, max_keys=maxk)
+    out = []
+    for k, (t, h) in enumerate(rows):
+        i = int(np.searchsorted(qsl, t, side="right") - 1)
+        n = int(sl[i] - (qsl[i + 1] - qsl[i]) + (t - qsl[i]) + 1)
+        with np.errstate(divide="ignore"):
+            out.append((lse[k] + np.log(wt[k, :n])) * LOG2E)
+    return out
+
+
+def tile_maxima(s, first, end, size):
+    """Maxima of s over consecutive tiles of `size` keys of [first, end)."""
+    return [float(np.max(s[a:min(a + size, end)])) for a in range(first, end, size)]
+
+
+def jumps_over_running_max(tm):
+    """Largest rise of a tile's maximum over the running maximum of the
+    tiles before it (-inf for a single tile)."""
+    best, run = float("-inf"), tm[0]
+    for x in tm[1:]:
+        best = max(best, x - run)
+        run = max(run, x)
+    return best
