@@ -202,13 +202,22 @@ pa_status pa_forward_baseline(pa_handle *h, const pa_tensor *q, const pa_tensor 
                               const pa_tensor *seq_lens, const pa_tensor *query_start_loc,
                               float scale, const pa_tensor *out, pa_stream stream);
 
-/* Debug: copy the stored bytes of every valid K and V row (positions
- * p < seq_lens[i]) in logical order into k_dense / v_dense, both of the
- * cache dtype and shape [S, MB * block_size, Hkv, d], walking the block
- * table with the same addressing as the attention kernels.  Rows at
- * positions >= seq_lens[i] are untouched. */
+/* Debug: the block-table walk of the attention kernels, checked bit for
+ * bit (Sec. 4.3).  Runs the same work lists and the same K/V loaders as
+ * pa_forward for a batch with this metadata, but stores the bytes each
+ * loader reads instead of computing with them: every key p < seq_lens[i] of
+ * a sequence with query length 1 through the decode kernel's loads, of a
+ * sequence with query length >= 2 through the Q-block kernel's loads (its
+ * last Q-block, which reads all of the sequence's keys).  The bytes go to
+ * k_dense / v_dense, both of the cache dtype and shape
+ * [S, MB * block_size, Hkv, d], at [i, p, g, :]; positions >= seq_lens[i]
+ * and sequences with query length 0 (which attention reads nothing of) are
+ * untouched.  num_tokens is the q row count pa_forward would get (T); the
+ * handle's workspace must fit the batch as for pa_forward.  Asynchronous on
+ * `stream`. */
 pa_status pa_debug_gather(pa_handle *h, const pa_tensor *k_cache, const pa_tensor *v_cache,
                           const pa_tensor *block_table, const pa_tensor *seq_lens,
+                          const pa_tensor *query_start_loc, int64_t num_tokens,
                           const pa_tensor *k_dense, const pa_tensor *v_dense, pa_stream stream);
 
 /* Write the keys and values of new tokens into the paged caches (the step

@@ -306,6 +306,28 @@ pa_status check_batch(const pa_config& c, const pa_tensor* q, const pa_tensor* k
   return PA_OK;
 }
 
+// The decode and Q-block work-list descriptors of plan p inside workspace ws.
+void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_t S,
+                  pa::DecodePlan* dp, pa::PrefillPlan* pp) {
+  const int64_t items = p.prefill_launch ? p.prefill_units / c.num_kv_heads : 0;
+  const WsLayout wl = ws_layout(c, p.decode_workers, S, items);
+  dp->workers = p.decode_workers;
+  dp->step_keys = p.decode_step;
+  dp->min_steps = p.decode_min_steps;
+  dp->unit_heads = p.decode_unit_heads;
+  dp->meta = reinterpret_cast<int32_t*>(ws + wl.meta);
+  dp->dec = reinterpret_cast<int4*>(ws + wl.dec);
+  dp->part_o = reinterpret_cast<float*>(ws + wl.part_o);
+  dp->part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
+  pp->block_q = p.block_q;
+  pp->work_items = (int32_t)items;
+  pp->seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
+  pp->list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
+  pp->list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
+  pp->count = reinterpret_cast<int32_t*>(ws + wl.count);
+  pp->rec = reinterpret_cast<int4*>(ws + wl.rec);
+}
+
 pa::KvGeom geom(const pa_tensor* t) {
   const int eb = elem_bytes(t->dtype);
   return pa::KvGeom{t->stride[0] * eb, t->stride[1] * eb, t->stride[2] * eb};
@@ -585,6 +607,8 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   a.group = c.num_q_heads / c.num_kv_heads;
   a.sl2 = scale * c.k_scale * 1.4426950408889634f;
   a.v_scale = c.v_scale;
+  a.kd = a.vd = nullptr;
+  a.d_seq = a.d_tok = a.d_head = 0;
 
   if (baseline) {
     hipError_t e = pa::launch_baseline(a, c.head_dim, fp8, st);
@@ -592,25 +616,9 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     return PA_OK;
   }
   if (!p.decode_launch) return PA_OK;
-  const int64_t items = p.prefill_launch ? p.prefill_units / c.num_kv_heads : 0;
-  const WsLayout wl = ws_layout(c, p.decode_workers, sh.S, items);
   pa::DecodePlan dp;
-  dp.workers = p.decode_workers;
-  dp.step_keys = p.decode_step;
-  dp.min_steps = p.decode_min_steps;
-  dp.unit_heads = p.decode_unit_heads;
-  dp.meta = reinterpret_cast<int32_t*>(ws + wl.meta);
-  dp.dec = reinterpret_cast<int4*>(ws + wl.dec);
-  dp.part_o = reinterpret_cast<float*>(ws + wl.part_o);
-  dp.part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
   pa::PrefillPlan pp;
-  pp.block_q = p.block_q;
-  pp.work_items = (int32_t)items;
-  pp.seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
-  pp.list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
-  pp.list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
-  pp.count = reinterpret_cast<int32_t*>(ws + wl.count);
-  pp.rec = reinterpret_cast<int4*>(ws + wl.rec);
+  device_plans(c, p, ws, sh.S, &dp, &pp);
 
   hipError_t e = timed_launch(h, PA_KERNEL_PLAN, st,
                               [&] { return pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st); });
@@ -646,6 +654,7 @@ pa_status pa_forward_baseline(pa_handle* h, const pa_tensor* q, const pa_tensor*
 
 pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tensor* v_cache,
                           const pa_tensor* block_table, const pa_tensor* seq_lens,
+                          const pa_tensor* query_start_loc, int64_t num_tokens,
                           const pa_tensor* k_dense, const pa_tensor* v_dense, pa_stream stream) {
   if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   const pa_config& c = h->cfg;
@@ -653,6 +662,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   TRY(check_tensor(v_cache, "v_cache", c.kv_dtype, 4));
   TRY(check_tensor(block_table, "block_table", PA_DTYPE_I32, 2));
   TRY(check_tensor(seq_lens, "seq_lens", PA_DTYPE_I32, 1));
+  TRY(check_tensor(query_start_loc, "query_start_loc", PA_DTYPE_I32, 1));
   TRY(check_tensor(k_dense, "k_dense", c.kv_dtype, 4));
   TRY(check_tensor(v_dense, "v_dense", c.kv_dtype, 4));
   const int64_t S = seq_lens->shape[0], MB = block_table->shape[1], NB = k_cache->shape[0];
@@ -662,6 +672,9 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
       return fail(PA_ERR_INVALID_ARG, "caches must be [num_blocks, %d, %d, %d]", c.block_size,
                   c.num_kv_heads, c.head_dim);
   if (block_table->shape[0] != S) return fail(PA_ERR_INVALID_ARG, "block_table rows != num_seqs");
+  if (query_start_loc->shape[0] != S + 1)
+    return fail(PA_ERR_INVALID_ARG, "query_start_loc must have num_seqs + 1 entries");
+  if (num_tokens < 0 || num_tokens > INT32_MAX) return fail(PA_ERR_INVALID_ARG, "num_tokens out of range");
   for (const pa_tensor* dn : {k_dense, v_dense})
     if (dn->shape[0] != S || dn->shape[1] != MB * c.block_size || dn->shape[2] != c.num_kv_heads ||
         dn->shape[3] != c.head_dim)
@@ -671,33 +684,67 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
     return fail(PA_ERR_INVALID_ARG, "k_dense and v_dense must share strides");
   if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences");
   if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
+  if (MB * c.block_size > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
+  for (const pa_tensor* kv : {k_cache, v_cache})
+    if ((int64_t)c.block_size * kv->stride[1] * elem_bytes(kv->dtype) >= INT32_MAX ||
+        kv->stride[2] * elem_bytes(kv->dtype) >= INT32_MAX ||
+        kv->stride[0] * elem_bytes(kv->dtype) >= ((int64_t)1 << 32))
+      return fail(PA_ERR_UNSUPPORTED, "cache strides too large for the loaders' offsets");
   TRY(check_aligned16(k_cache, "k_cache"));
   TRY(check_aligned16(v_cache, "v_cache"));
   TRY(check_aligned16(k_dense, "k_dense"));
   TRY(check_aligned16(v_dense, "v_dense"));
+  if (reinterpret_cast<uintptr_t>(block_table->data) & 3 || reinterpret_cast<uintptr_t>(seq_lens->data) & 3 ||
+      reinterpret_cast<uintptr_t>(query_start_loc->data) & 3)
+    return fail(PA_ERR_INVALID_ARG, "int32 metadata must be 4-byte aligned");
+  pa_plan_info p;
+  make_plan(c, h->tun, h->cus, num_tokens, S, MB, &p);
+  if (S * cdiv(MB * c.block_size, p.decode_step) * c.num_kv_heads > INT32_MAX)
+    return fail(PA_ERR_UNSUPPORTED, "batch too large for 32-bit decode step indices");
+  if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
+    return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
+                (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
+  if (S == 0 || num_tokens == 0 || !p.decode_launch) return PA_OK;
   const int eb = elem_bytes(c.kv_dtype);
-  pa::GatherArgs g;
-  g.k = static_cast<const uint8_t*>(k_cache->data);
-  g.v = static_cast<const uint8_t*>(v_cache->data);
-  g.kg = geom(k_cache);
-  g.vg = geom(v_cache);
-  g.bt = static_cast<const int32_t*>(block_table->data);
-  g.bt_row = block_table->stride[0];
-  g.mb = (int32_t)MB;
-  g.seq_lens = static_cast<const int32_t*>(seq_lens->data);
-  g.kd = static_cast<uint8_t*>(k_dense->data);
-  g.vd = static_cast<uint8_t*>(v_dense->data);
-  g.d_seq = k_dense->stride[0] * eb;
-  g.d_tok = k_dense->stride[1] * eb;
-  g.d_head = k_dense->stride[2] * eb;
-  g.num_seqs = (int32_t)S;
-  g.num_blocks = (int32_t)std::min<int64_t>(NB, INT32_MAX);
-  g.block_size = c.block_size;
-  g.bs_log2 = __builtin_ctz(c.block_size);
-  g.num_kv_heads = c.num_kv_heads;
-  g.row_bytes = c.head_dim * eb;
-  hipError_t e = pa::launch_gather(g, reinterpret_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  pa::BatchArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.k = static_cast<const uint8_t*>(k_cache->data);
+  a.v = static_cast<const uint8_t*>(v_cache->data);
+  a.kg = geom(k_cache);
+  a.vg = geom(v_cache);
+  a.bt = static_cast<const int32_t*>(block_table->data);
+  a.bt_row = block_table->stride[0];
+  a.mb = (int32_t)MB;
+  a.seq_lens = static_cast<const int32_t*>(seq_lens->data);
+  a.qsl = static_cast<const int32_t*>(query_start_loc->data);
+  a.num_seqs = (int32_t)S;
+  a.num_tokens = (int32_t)num_tokens;
+  a.num_blocks = (int32_t)std::min<int64_t>(NB, INT32_MAX);
+  a.block_size = c.block_size;
+  a.bs_log2 = __builtin_ctz(c.block_size);
+  a.num_q_heads = c.num_q_heads;
+  a.num_kv_heads = c.num_kv_heads;
+  a.group = c.num_q_heads / c.num_kv_heads;
+  a.sl2 = 1.f;
+  a.v_scale = 1.f;
+  a.kd = static_cast<uint8_t*>(k_dense->data);
+  a.vd = static_cast<uint8_t*>(v_dense->data);
+  a.d_seq = k_dense->stride[0] * eb;
+  a.d_tok = k_dense->stride[1] * eb;
+  a.d_head = k_dense->stride[2] * eb;
+  pa::DecodePlan dp;
+  pa::PrefillPlan pp;
+  device_plans(c, p, static_cast<uint8_t*>(c.workspace), S, &dp, &pp);
+  const bool fp8 = c.kv_dtype == PA_DTYPE_FP8_E4M3;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st);
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  e = pa::launch_decode(a, dp, c.head_dim, fp8, st, true);
+  if (e != hipSuccess) return hip_fail(e, "decode gather launch");
+  if (p.prefill_launch) {
+    e = pa::launch_prefill(a, pp, c.head_dim, fp8, st, true);
+    if (e != hipSuccess) return hip_fail(e, "Q-block gather launch");
+  }
   return PA_OK;
 }
 

@@ -86,7 +86,10 @@ struct Piece {
   int head, tail;      // the pair starts before / continues after this worker
 };
 
-template <int D, bool FP8, int HU>
+// GATHER: the same partition, block-table walk and loads, but every loaded
+// row chunk of a valid key is stored into the dense outputs a.kd / a.vd
+// instead of being computed with (pa_debug_gather).
+template <int D, bool FP8, int HU, bool GATHER>
 __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs a, DecodePlan p) {
   constexpr int EB = FP8 ? 1 : 2;          // bytes per cached element
   constexpr int UB = HU * D * EB;          // bytes of one token's unit row (HU heads)
@@ -483,9 +486,33 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
     }
     consume_v(k, vx, pt);
   };
+  // Gather-only: the rows of step k go straight from the load registers
+  // to the dense outputs (keys < L only).
+  auto store_rows = [&](int k, LT (&kx)[R], LT (&vx)[R]) {
+    const int64_t base = (int64_t)cur.s * a.d_seq + (int64_t)(cur.g + hl) * a.d_head + ci * LB;
+#pragma unroll
+    for (int b = 0; b < BPS; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int key = k * KS + 16 * b + 4 * r4 + lq;
+        if (key < cur.L) {
+          *(LT*)(a.kd + base + (int64_t)key * a.d_tok) = kx[4 * b + r4];
+          *(LT*)(a.vd + base + (int64_t)key * a.d_tok) = vx[4 * b + r4];
+        }
+      }
+  };
   for (;;) {
     cb = uniform(cur.k0 * BPS);
     load_window(cur, cb, win);
+    if constexpr (GATHER) {
+      __builtin_amdgcn_s_waitcnt(0);
+      for (int k = cur.k0; k < cur.k1; ++k) {
+        refill(k);
+        issue(a.k, a.kg, koff, k, krA);
+        issue(a.v, a.vg, voff, k, vrA);
+        store_rows(k, krA, vrA);
+      }
+    } else {
     load_q(cur, qc);
     __builtin_amdgcn_s_waitcnt(0);
     int k = cur.k0;
@@ -503,6 +530,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
       step(k, false, krA, vrA, krA, vrA);
     }
     finalize();
+    }
     t += cur.k1 - cur.k0;
     if (t >= t_end) break;
     const int jj = cur.gu + 1 < Hu ? cur.j : cur.j + 1;
@@ -587,22 +615,29 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
   else *(__bf16*)orow = (__bf16)(num[0] * inv);
 }
 
+template <bool GATHER>
+hipError_t launch_decode_t(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
+                           hipStream_t st) {
+  const dim3 grid((unsigned)((p.workers + kDecodeWaves - 1) / kDecodeWaves)), block(64 * kDecodeWaves);
+  const int hu = p.unit_heads;
+  if (head_dim == 128 && !fp8 && hu == 1) decode_kernel<128, false, 1, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128 && fp8 && hu == 2) decode_kernel<128, true, 2, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128 && fp8 && hu == 1) decode_kernel<128, true, 1, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !fp8 && hu == 2) decode_kernel<64, false, 2, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !fp8 && hu == 1) decode_kernel<64, false, 1, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 4) decode_kernel<64, true, 4, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 2) decode_kernel<64, true, 2, GATHER><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && fp8 && hu == 1) decode_kernel<64, true, 1, GATHER><<<grid, block, 0, st>>>(a, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
-                         hipStream_t st) {
-  const dim3 grid((unsigned)((p.workers + kDecodeWaves - 1) / kDecodeWaves)), block(64 * kDecodeWaves);
-  const int hu = p.unit_heads;
-  if (head_dim == 128 && !fp8 && hu == 1) decode_kernel<128, false, 1><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 128 && fp8 && hu == 2) decode_kernel<128, true, 2><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 128 && fp8 && hu == 1) decode_kernel<128, true, 1><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && !fp8 && hu == 2) decode_kernel<64, false, 2><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && !fp8 && hu == 1) decode_kernel<64, false, 1><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 4) decode_kernel<64, true, 4><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 2) decode_kernel<64, true, 2><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 1) decode_kernel<64, true, 1><<<grid, block, 0, st>>>(a, p);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+                         hipStream_t st, bool gather) {
+  return gather ? launch_decode_t<true>(a, p, head_dim, fp8, st)
+                : launch_decode_t<false>(a, p, head_dim, fp8, st);
 }
 
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st) {

@@ -48,6 +48,11 @@ struct BatchArgs {
   int32_t num_q_heads, num_kv_heads, group;  // group = Hq / Hkv
   float sl2;                    // softmax scale * log2(e) * k_scale
   float v_scale;
+  // Gather-only launches (pa_debug_gather): dense [S, MB * bs, Hkv, d]
+  // outputs that receive the cache bytes the attention loaders read.
+  uint8_t* kd;
+  uint8_t* vd;
+  int64_t d_seq, d_tok, d_head;  // dense strides (bytes)
 };
 
 struct DecodePlan {
@@ -100,22 +105,6 @@ struct PrefillPlan {
   int4* rec;           // [work_items] (sequence, first token, rows, keys before the first row)
 };
 
-struct GatherArgs {
-  const uint8_t* k;
-  const uint8_t* v;
-  KvGeom kg, vg;
-  const int32_t* bt;
-  int64_t bt_row;
-  int32_t mb;
-  const int32_t* seq_lens;
-  uint8_t* kd;
-  uint8_t* vd;
-  int64_t d_seq, d_tok, d_head;  // dense output strides (bytes)
-  int32_t num_seqs, num_blocks, block_size, num_kv_heads;
-  int32_t bs_log2;
-  int32_t row_bytes;             // bytes of one head's row (head_dim * elem)
-};
-
 struct ValidateArgs {
   const int32_t* bt;
   int64_t bt_row;
@@ -126,16 +115,18 @@ struct ValidateArgs {
   uint32_t* error_word;
 };
 
-// Launchers (return hipGetLastError() of the launch).
+// Launchers (return hipGetLastError() of the launch).  With gather = true
+// the attention kernels run their K/V loaders only and store the loaded
+// bytes of every valid key into a.kd / a.vd (pa_debug_gather).
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
-                         hipStream_t st);
+                         hipStream_t st, bool gather = false);
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st);
 hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
                        bool with_prefill, hipStream_t st);
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
-                          hipStream_t st);
-hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st);
-hipError_t launch_gather(const GatherArgs& a, hipStream_t st);
+                          hipStream_t st, bool gather = false);
+hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st,
+                         bool gather = false);
 
 // KV-cache write (csrc/cache.hip).
 struct CacheWriteArgs {

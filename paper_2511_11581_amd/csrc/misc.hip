@@ -1,9 +1,4 @@
-// Debug gather and device-side metadata validation.
-//
-// gather_kernel walks the block table exactly as the attention kernels do
-// (page_of + slot offset, 16-byte loads) and stores the bytes of every valid
-// key/value row in logical order into dense [S, MB*bs, Hkv, row] buffers, so
-// block-table addressing can be checked bit for bit (Sec. 4.3).
+// Device-side metadata validation.
 //
 // validate_kernel checks the preconditions of a well-formed paged batch
 // (Sec. 4.2 terminology, Sec. 4.3 block table) and ORs an error code into a
@@ -14,27 +9,6 @@
 namespace pa {
 
 namespace {
-
-// grid: (ceil(MB*bs / 4), S, Hkv); block 256 = 4 keys x 64 lanes of 16 B.
-__global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
-  const int s = blockIdx.y, g = blockIdx.z;
-  const int key = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  const int L = min(a.seq_lens[s], a.mb * a.block_size);
-  if (key >= L) return;
-  const int32_t* bt_row = a.bt + (int64_t)s * a.bt_row;
-  const int pg = page_of(bt_row, key, a.bs_log2, a.num_blocks);
-  const int slot = key & (a.block_size - 1);
-  for (int c = lane; c * 16 < a.row_bytes; c += 64) {
-    const u32x4 kw = ld16(a.k + (int64_t)pg * a.kg.blk + (int64_t)slot * a.kg.slot +
-                          (int64_t)g * a.kg.head + 16 * c);
-    const u32x4 vw = ld16(a.v + (int64_t)pg * a.vg.blk + (int64_t)slot * a.vg.slot +
-                          (int64_t)g * a.vg.head + 16 * c);
-    const int64_t off = (int64_t)s * a.d_seq + (int64_t)key * a.d_tok + (int64_t)g * a.d_head + 16 * c;
-    *(u32x4*)(a.kd + off) = kw;
-    *(u32x4*)(a.vd + off) = vw;
-  }
-}
 
 // Error bits written by validate_kernel.
 enum : uint32_t {
@@ -69,14 +43,6 @@ __global__ __launch_bounds__(256) void validate_kernel(ValidateArgs a) {
 }
 
 }  // namespace
-
-hipError_t launch_gather(const GatherArgs& a, hipStream_t st) {
-  const int64_t keys = (int64_t)a.mb * a.block_size;
-  if (a.num_seqs <= 0 || keys <= 0) return hipSuccess;
-  dim3 grid((unsigned)((keys + 3) / 4), a.num_seqs, a.num_kv_heads), block(256);
-  gather_kernel<<<grid, block, 0, st>>>(a);
-  return hipGetLastError();
-}
 
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t st) {
   if (a.num_seqs <= 0) return hipSuccess;

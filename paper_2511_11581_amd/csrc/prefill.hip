@@ -30,7 +30,10 @@ namespace {
 constexpr int kTileN = kPrefillTileKeys;  // keys per tile
 constexpr int kThreads = 256;
 
-template <int D, bool FP8>
+// GATHER: only the last Q-block of each sequence runs its tile loads, and
+// the loaded registers (raw cache bytes) of every valid key are stored into
+// the dense outputs a.kd / a.vd (pa_debug_gather).
+template <int D, bool FP8, bool GATHER>
 __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, PrefillPlan pp) {
   constexpr int EB = FP8 ? 1 : 2;
   constexpr int CH = D * EB / 16;                 // 16-byte chunks per cached row
@@ -81,7 +84,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 
   // Q^T B operands: d = 16t + 8hf + j of this row.
   bf16x8 qt[NT];
-  {
+  if constexpr (!GATHER) {
     const uint8_t* qrow = a.q + (int64_t)(t0 + (rvalid ? tl : tok_hi - 1)) * a.q_tok +
                           (int64_t)(g * G + hh) * a.q_head;
 #pragma unroll
@@ -291,6 +294,29 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     }
   };
 
+  if constexpr (GATHER) {
+    if (tok_hi != qlen) return;   // not the sequence's last Q-block
+    const int64_t d0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
+    for (int tile = 0; tile < ntiles; ++tile) {
+      const int tb = tile * kTileN;
+      load_pages(tile, pg_k, pg_v);
+      load_tile(tile, pg_k, pg_v);
+#pragma unroll
+      for (int i = 0; i < KLD; ++i) {
+        const int flat = tid + kThreads * i;
+        const int key = tb + flat / CH;
+        if (key < kv_len) *(u32x4*)(a.kd + d0 + (int64_t)key * a.d_tok + 16 * (flat % CH)) = kreg[i];
+      }
+      if (tid < VTASKS)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = tb + 4 * vm + r;
+          if (key < kv_len) *(u32x4*)(a.vd + d0 + (int64_t)key * a.d_tok + 16 * vc) = vreg[r];
+        }
+    }
+    return;
+  }
+
   load_pages(0, pg_k, pg_v);
   load_tile(0, pg_k, pg_v);
   load_pages(min(1, ntiles - 1), pg_k, pg_v);
@@ -334,13 +360,15 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 
 
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
-                          hipStream_t st) {
-  if (!fp8) return launch_qblock(a, p, head_dim, st);
+                          hipStream_t st, bool gather) {
+  if (!fp8) return launch_qblock(a, p, head_dim, st, gather);
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   dim3 grid((unsigned)blocks), block(kThreads);
-  if (head_dim == 128) prefill_kernel<128, true><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64) prefill_kernel<64, true><<<grid, block, 0, st>>>(a, p);
+  if (head_dim == 128 && !gather) prefill_kernel<128, true, false><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !gather) prefill_kernel<64, true, false><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128) prefill_kernel<128, true, true><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64) prefill_kernel<64, true, true><<<grid, block, 0, st>>>(a, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

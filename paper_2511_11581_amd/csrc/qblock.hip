@@ -107,7 +107,12 @@ __device__ __forceinline__ void wait_vm_lds() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
 }
 
-template <int D>
+// GATHER: only the last Q-block of each sequence runs; it walks the block
+// table and copies every tile into the ring with the same loads, then
+// stores the bytes of every valid key into the dense outputs a.kd / a.vd:
+// K read back at the matrix-core operand addresses, V through the loader's
+// swizzle (pa_debug_gather).
+template <int D, bool GATHER>
 __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, PrefillPlan pp) {
   constexpr int RB = 2 * D;                        // bytes per cached row
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
@@ -162,7 +167,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 
   // Q^T operands: d = 16t + 8hf + 0..7 of this row.
   bf16x8 qt[NT];
-  {
+  if constexpr (!GATHER) {
     const uint8_t* qrow = a.q + (int64_t)(t0 + (rvalid ? tl : tok_hi - 1)) * a.q_tok +
                           (int64_t)(g * G + row % G) * a.q_head;
 #pragma unroll
@@ -420,6 +425,38 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     }
   };
 
+  if constexpr (GATHER) {
+    if (ctx + tok_hi != min(a.seq_lens[seq], a.mb * a.block_size)) return;   // not the last Q-block
+    const int64_t kd0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
+    for (int t = 0; t < ntiles; ++t) {
+      issue(t, 0);
+      wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();   // every wave's rows of tile t have landed
+      // K: waves 0 / 1 store keys 0..31 / 32..63 from the operand addresses
+      // (lane (n, hf), k-step tt: key n (+ 32), d = 16 tt + 8 hf .. + 7)
+      if (wave < 2) {
+        const int key = t * kTile + 32 * wave + n;
+        if (key < kv_len)
+#pragma unroll
+          for (int tt = 0; tt < NT; ++tt)
+            *(u32x4*)(a.kd + kd0 + (int64_t)key * a.d_tok + 16 * (2 * tt + hf)) =
+                *(const u32x4*)(lds + kaddr[tt] + 32 * RB * wave);
+      }
+      // V: each wave its own rows, chunk slot s holding logical chunk s ^ fV(row)
+#pragma unroll
+      for (int k = 0; k < NLD; ++k) {
+        const int r = wrow + RPI * k + lane / CPR, c = (lane % CPR) ^ fV(r);
+        const int key = t * kTile + r;
+        if (key < kv_len)
+          *(u32x4*)(a.vd + kd0 + (int64_t)key * a.d_tok + 16 * c) =
+              *(const u32x4*)(lds + VBASE + (wave * NLD + k) * 1024 + 16 * lane);
+      }
+      wait_vm_lds<0>();
+      __builtin_amdgcn_s_barrier();   // stage 0 read by every wave before the next copies
+    }
+    return;
+  }
+
   // ---- prologue: tiles 0, 1, 2 in flight; scores and weights of tile 0,
   //      whose row max becomes the first reference
   issue(0, 0);
@@ -527,12 +564,15 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 
 }  // namespace
 
-hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st) {
+hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st,
+                         bool gather) {
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   dim3 grid((unsigned)blocks), block(kThreads);
-  if (head_dim == 128) qblock_kernel<128><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64) qblock_kernel<64><<<grid, block, 0, st>>>(a, p);
+  if (head_dim == 128 && !gather) qblock_kernel<128, false><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64 && !gather) qblock_kernel<64, false><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 128) qblock_kernel<128, true><<<grid, block, 0, st>>>(a, p);
+  else if (head_dim == 64) qblock_kernel<64, true><<<grid, block, 0, st>>>(a, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -112,7 +112,7 @@ def load_library(path: str = LIB_PATH):
     lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
     lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_forward_baseline.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
-    lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, T, P]
+    lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, ctypes.c_int64, T, T, P]
     lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
     lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                             ctypes.POINTER(pa_plan_info)]
@@ -247,10 +247,12 @@ def pa_forward_baseline(h, q, k_cache, v_cache, block_table, seq_lens, query_sta
                                               ctypes.byref(ds[6]), _stream(stream)))
 
 
-def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, k_dense, v_dense,
-                    stream=None) -> None:
-    ds = [describe(t) for t in (k_cache, v_cache, block_table, seq_lens, k_dense, v_dense)]
-    _check(load_library().pa_debug_gather(h, *(ctypes.byref(d) for d in ds), _stream(stream)))
+def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, query_start_loc, num_tokens,
+                    k_dense, v_dense, stream=None) -> None:
+    ds = [describe(t) for t in (k_cache, v_cache, block_table, seq_lens, query_start_loc)]
+    dn = [describe(t) for t in (k_dense, v_dense)]
+    _check(load_library().pa_debug_gather(h, *(ctypes.byref(d) for d in ds), int(num_tokens),
+                                          *(ctypes.byref(d) for d in dn), _stream(stream)))
 
 
 def pa_cache_write(h, key, value, slot_mapping, k_cache, v_cache, stream=None) -> None:
@@ -310,12 +312,16 @@ class PagedAttention:
         """Write new tokens' K/V (bf16 [T, Hkv, d]) into their slots of the caches."""
         pa_cache_write(self.handle, key, value, slot_mapping, k_cache, v_cache, stream)
 
-    def gather(self, k_cache, v_cache, block_table, seq_lens, stream=None):
+    def gather(self, k_cache, v_cache, block_table, seq_lens, query_start_loc, num_tokens,
+               stream=None):
+        """The K/V bytes the attention loaders read for this batch (debug):
+        dense [S, MB * bs, Hkv, d] tensors, zero where nothing is read."""
         S, MB = block_table.shape
         shape = (S, MB * k_cache.shape[1], k_cache.shape[2], k_cache.shape[3])
         kd = torch.zeros(shape, dtype=k_cache.dtype, device=k_cache.device)
         vd = torch.zeros(shape, dtype=v_cache.dtype, device=v_cache.device)
-        pa_debug_gather(self.handle, k_cache, v_cache, block_table, seq_lens, kd, vd, stream)
+        pa_debug_gather(self.handle, k_cache, v_cache, block_table, seq_lens, query_start_loc,
+                        num_tokens, kd, vd, stream)
         return kd, vd
 
     def close(self):

@@ -1,5 +1,15 @@
-"""Bit-exact block-table addressing (gather-only debug mode) and the ABI's
-error reporting on a GPU."""
+"""Bit-exact block-table addressing of the attention kernels' own loaders
+(gather-only debug mode, Sec. 4.3) and the ABI's error reporting on a GPU.
+
+pa_debug_gather runs the plan kernel and the decode / Q-block kernels'
+loads for a batch and stores the bytes each loader reads; every key a row
+attends to must arrive exactly as the oracle's independent block-table walk
+copies it.  Sequences with query length 1 go through the decode kernel's
+loader (its block-id window, 16-key block addressing and head units),
+those with query length >= 2 through the Q-block kernel of the cache dtype
+(bf16: the copies straight into the LDS ring and its swizzles; fp8: the
+register-staged loads); sequences with no query rows are read by nothing.
+"""
 import numpy as np
 import pytest
 import torch
@@ -7,33 +17,36 @@ import torch
 import oracle
 from paper_2511_11581_amd import pa
 from paper_2511_11581_amd import workloads as W
-from gpu_util import attention_for, run_gpu
+from gpu_util import attention_for, run_gpu, seed_of
 
 pytestmark = pytest.mark.gpu
 
 
-def gather_check(w):
-    att = attention_for(w)
+def gather_check(w, att=None):
+    att = att or attention_for(w)
     wd = w.to("cuda")
-    kd, vd = att.gather(wd.k_cache, wd.v_cache, wd.block_table, wd.seq_lens)
+    kd, vd = att.gather(wd.k_cache, wd.v_cache, wd.block_table, wd.seq_lens, wd.query_start_loc,
+                        w.num_tokens)
     torch.cuda.synchronize()
     wc = w.to("cpu")
     rk, rv = oracle.gather(wc.k_cache, wc.v_cache, wc.block_table, wc.seq_lens)
-    eb = 1 if w.kv_fp8 else 2
     kb = kd.cpu().view(torch.uint8).numpy().reshape(rk.shape)
     vb = vd.cpu().view(torch.uint8).numpy().reshape(rv.shape)
-    for i, L in enumerate(wc.seq_lens.tolist()):
-        assert np.array_equal(kb[i, :L], rk[i, :L]), f"K bytes differ in sequence {i}"
-        assert np.array_equal(vb[i, :L], rv[i, :L]), f"V bytes differ in sequence {i}"
-        assert not kb[i, L:].any(), "positions past seq_len were written"
+    for i, (L, ql) in enumerate(zip(wc.seq_lens.tolist(), wc.q_lens)):
+        n = L if ql >= 1 else 0
+        assert np.array_equal(kb[i, :n], rk[i, :n]), f"K bytes differ in sequence {i} (q_len {ql})"
+        assert np.array_equal(vb[i, :n], rv[i, :n]), f"V bytes differ in sequence {i} (q_len {ql})"
+        assert not kb[i, n:].any() and not vb[i, n:].any(), f"sequence {i}: unread positions written"
 
 
-@pytest.mark.parametrize("k", [1, 2])
+@pytest.mark.parametrize("k", [1, 2, 3])
 def test_gather_benchmark_batches(k):
     gather_check(W.make_config(k))
 
 
 def test_gather_long_fp8_subset():
+    # three of the long-context fp8 sequences (32K-128K keys), decode loader
+    # with two-head units and windows of block ids far past the first
     w = W.make_config(5, device="cuda")
     sub = W.Workload(**{**w.__dict__})
     sub.block_table = w.block_table[:3].contiguous()
@@ -44,10 +57,27 @@ def test_gather_long_fp8_subset():
     gather_check(sub)
 
 
-@pytest.mark.parametrize("bs,kv", [(16, "bf16"), (32, "fp8"), (64, "bf16")])
-def test_gather_random_small(bs, kv):
-    w = W.make_batch([(37, 1), (0, 100), (250, 7), (1, 0)], 8, 2, 64, kv_dtype=kv, block_size=bs,
-                     seed=bs, pool_blocks=64, table_width=20)
+GATHER_CASES = {
+    # name: (seqs, Hq, Hkv, d, kv, block_size, extra)
+    "bf16_d64_bs16": ([(37, 1), (0, 100), (250, 7), (1, 0), (5000, 1)], 8, 2, 64, "bf16", 16, {}),
+    "fp8_d64_bs32": ([(37, 1), (0, 100), (250, 7), (1, 0), (3000, 1)], 8, 4, 64, "fp8", 32, {}),
+    "bf16_d128_bs64": ([(37, 1), (0, 100), (250, 7), (1, 0), (4100, 1)], 8, 2, 128, "bf16", 64, {}),
+    "fp8_d128_bs128": ([(600, 1), (0, 300), (190, 66), (8000, 1)], 16, 2, 128, "fp8", 128, {}),
+    "bf16_d128_bs256_g1": ([(999, 1), (0, 257), (300, 2)], 4, 4, 128, "bf16", 256, {}),
+    "fp8_d128_g8_hu1": ([(2000, 1), (70, 40), (5, 1)], 8, 1, 128, "fp8", 16, {}),
+    "bf16_d64_hu1_odd_heads": ([(700, 1), (20, 90)], 3, 3, 64, "bf16", 16, {}),
+    "fp8_d64_hu4": ([(1500, 1), (0, 77), (33, 1)], 16, 8, 64, "fp8", 16, {}),
+    "wide_table_padded_rows": ([(70, 1), (0, 40), (0, 0)], 8, 2, 128, "bf16", 16,
+                               dict(token_pad=5, table_width=20, pool_blocks=64)),
+    "strided_window_moves": ([(70000, 1), (300, 1)], 8, 8, 128, "bf16", 16, {}),
+}
+
+
+@pytest.mark.parametrize("name", list(GATHER_CASES))
+def test_gather_random_tables(name):
+    seqs, Hq, Hkv, d, kv, bs, extra = GATHER_CASES[name]
+    w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=seed_of(name), name=name,
+                     **extra)
     gather_check(w)
 
 
