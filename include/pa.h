@@ -191,6 +191,23 @@ pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,
                      const pa_tensor *out, pa_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP-graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * attention, kernels and arguments as pa_forward, but the call's scratch
+ * (decode list, decode partials, Q-block work list) lives in a static
+ * device array of the library (48 MiB, held on every GPU the library runs
+ * on until the process ends) instead of the handle's workspace, which may
+ * be NULL.  The handle must have been created on the device of `stream`.
+ * Returns PA_ERR_WORKSPACE, before enqueuing anything, when the batch's
+ * plan needs more scratch than the array holds (pa_plan reports the
+ * bytes).  Allocates nothing.  Every call on one GPU shares that GPU's
+ * array: calls that overlap in time on one GPU (other streams, other
+ * threads, other handles) race and must be serialised by the caller. */
+pa_status pa_forward_noalloc(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
+                             const pa_tensor *v_cache, const pa_tensor *block_table,
+                             const pa_tensor *seq_lens, const pa_tensor *query_start_loc,
+                             float scale, const pa_tensor *out, pa_stream stream);
+
 /* Ablation only: the same attention as pa_forward, computed with the
  * paper's baseline decomposition (Sec. 4 / App. A, the first rung of the
  * optimisation ladder of Sec. 7): one wave per (query token, query head),

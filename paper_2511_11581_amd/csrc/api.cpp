@@ -19,6 +19,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -42,6 +43,7 @@ struct pa_handle {
   pa_config cfg;
   int device;
   int cus;
+  uint8_t* scratch;   // this device's copy of the library's static scratch (pa_forward_noalloc)
   pa_tunables tun;
   bool profile;
   pa_event_ring ring[PA_KERNEL_KINDS];
@@ -50,6 +52,18 @@ struct pa_handle {
 };
 
 namespace {
+
+// Scratch for pa_forward_noalloc: the same contents as a caller's workspace
+// (decode list, decode partials, Q-block work list), in a file-scope device
+// array that every GPU the library runs on holds until the process ends.
+// Host code never passes `scratch` itself to a kernel: its name is a
+// host-side stand-in, not a device address; pa_create takes each device's
+// address with hipGetSymbolAddress once and keeps it in g_scratch[device].
+constexpr uint64_t kScratchBytes = 48ull << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+uint8_t* g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
 
 thread_local std::string g_err;
 
@@ -486,10 +500,22 @@ pa_status pa_create(const pa_config* cfg, pa_handle** out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+  uint8_t* scr = nullptr;
+  if (dev >= 0 && dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+      void* ptr = nullptr;
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+      g_scratch[dev] = static_cast<uint8_t*>(ptr);
+    }
+    scr = g_scratch[dev];
+  }
   pa_handle* h = new (std::nothrow) pa_handle;
   if (!h) return fail(PA_ERR_INVALID_ARG, "out of host memory");
   h->cfg = *cfg;
   h->device = dev;
+  h->scratch = scr;
   h->cus = cus > 0 ? cus : kMaxCus;
   h->tun = tunables_from_env();
   h->profile = (cfg->flags & PA_FLAG_PROFILE) != 0;
@@ -539,10 +565,13 @@ pa_status pa_profile_read(pa_handle* h, pa_profile* out, int reset) {
   return PA_OK;
 }
 
+// ws / ws_bytes: the device scratch the call uses (the caller's workspace,
+// or this device's static scratch for pa_forward_noalloc).
 static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
                               const pa_tensor* v_cache, const pa_tensor* block_table,
                               const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
-                              float scale, const pa_tensor* out, pa_stream stream, bool baseline) {
+                              float scale, const pa_tensor* out, pa_stream stream, bool baseline,
+                              uint8_t* ws, uint64_t ws_bytes, bool static_scratch) {
   if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   const pa_config& c = h->cfg;
   if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
@@ -553,12 +582,14 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   make_plan(c, h->tun, h->cus, sh.T, sh.S, sh.MB, &p);
   if (sh.S * cdiv(sh.MB * c.block_size, p.decode_step) * c.num_kv_heads > INT32_MAX)
     return fail(PA_ERR_UNSUPPORTED, "batch too large for 32-bit decode step indices");
-  if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
+  if (static_scratch && (!ws || p.workspace_bytes > ws_bytes))
+    return fail(PA_ERR_WORKSPACE, "batch needs %llu bytes of scratch; the static scratch holds %llu",
+                (unsigned long long)p.workspace_bytes, (unsigned long long)ws_bytes);
+  if (!ws || ws_bytes < p.workspace_bytes)
     return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
-                (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
+                (unsigned long long)p.workspace_bytes, (unsigned long long)ws_bytes);
   if (sh.S == 0 || sh.T == 0) return PA_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  uint8_t* ws = static_cast<uint8_t*>(c.workspace);
 
   if (c.flags & PA_FLAG_VALIDATE) {
     uint32_t* word = reinterpret_cast<uint32_t*>(ws);
@@ -640,16 +671,32 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
                      const pa_tensor* v_cache, const pa_tensor* block_table,
                      const pa_tensor* seq_lens, const pa_tensor* query_start_loc, float scale,
                      const pa_tensor* out, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
-                      stream, false);
+                      stream, false, static_cast<uint8_t*>(h->cfg.workspace), h->cfg.workspace_bytes,
+                      false);
+}
+
+pa_status pa_forward_noalloc(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                             const pa_tensor* v_cache, const pa_tensor* block_table,
+                             const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
+                             float scale, const pa_tensor* out, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
+  if (!h->scratch)
+    return fail(PA_ERR_UNSUPPORTED, "no static scratch on device %d (devices 0..%d only)", h->device,
+                kMaxDevices - 1);
+  return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                      stream, false, h->scratch, kScratchBytes, true);
 }
 
 pa_status pa_forward_baseline(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
                               const pa_tensor* v_cache, const pa_tensor* block_table,
                               const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
                               float scale, const pa_tensor* out, pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
-                      stream, true);
+                      stream, true, static_cast<uint8_t*>(h->cfg.workspace), h->cfg.workspace_bytes,
+                      false);
 }
 
 pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tensor* v_cache,

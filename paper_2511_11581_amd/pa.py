@@ -41,7 +41,8 @@ KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
 
 # Every function declared in include/pa.h.
-EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
+EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_noalloc",
+           "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
            "pa_decode_pieces", "pa_profile_read", "pa_destroy", "pa_last_error")
 
 
@@ -111,6 +112,7 @@ def load_library(path: str = LIB_PATH):
                                        ctypes.POINTER(ctypes.c_uint64)]
     lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
     lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
+    lib.pa_forward_noalloc.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_forward_baseline.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, ctypes.c_int64, T, T, P]
     lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
@@ -126,7 +128,8 @@ def load_library(path: str = LIB_PATH):
     lib.pa_destroy.restype = None
     lib.pa_last_error.argtypes = []
     lib.pa_last_error.restype = ctypes.c_char_p
-    for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_debug_gather", "pa_plan",
+    for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_noalloc",
+                 "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
                  "pa_decode_pieces", "pa_profile_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -238,6 +241,15 @@ def pa_forward(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, s
     ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
     _check(load_library().pa_forward(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
                                      ctypes.byref(ds[6]), _stream(stream)))
+
+
+def pa_forward_noalloc(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                       stream=None) -> None:
+    """pa_forward with the library's static device scratch instead of a
+    workspace (for callers that cannot allocate)."""
+    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
+    _check(load_library().pa_forward_noalloc(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
+                                             ctypes.byref(ds[6]), _stream(stream)))
 
 
 def pa_forward_baseline(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale,
