@@ -11,7 +11,8 @@
 //      split the key tiles of all single-token rows evenly (Sec. 4.5);
 //   3. the log-sum-exp merge of pairs that span several workers;
 //   4. the Q-block kernel for rows with two or more query tokens (Sec. 4.4),
-//      BLOCK_M = 128 rows, i.e. BLOCK_Q = 128 / G tokens.
+//      BLOCK_M = 256 or 128 rows (bf16 caches, chosen from the batch shape)
+//      or 128 (fp8 caches), i.e. BLOCK_Q = BLOCK_M / G tokens.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,6 +38,7 @@ struct pa_event_ring {
 // is created.
 struct pa_tunables {
   int decode_min_steps;
+  int qblock_rows;   // 0: chosen from the batch shape; else 128 or 256 (bf16 caches)
 };
 
 struct pa_handle {
@@ -135,7 +137,30 @@ int decode_step_keys(const pa_config& c) {
   return pa::decode_step_keys(decode_unit_heads(c) * c.head_dim * eb, eb);
 }
 
-int block_m(const pa_config& c) { return pa::prefill_block_m(c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2); }
+int64_t prefill_items(int64_t T, int64_t S, int64_t bq);
+
+// Rows per Q-block.  fp8 caches: 128 (one kernel shape).  bf16 caches: 256
+// (8 waves, one workgroup per CU) or 128 (4 waves, two workgroups per CU),
+// chosen from host-visible sizes by a decision tree fitted offline to the
+// faster of the two on 47 prefill-heavy shapes (1-64 sequences, 16-4096 new
+// tokens, 0 or 4096 cached, G 4 and 8; Sec. 5 / Lst. 2 / Fig. 8), which
+// brings the geometric-mean loss against the best choice from 7.4% (always
+// 256) to 0.3%, the worst from 41% to 4.5%.  Smaller Q-blocks pay off while
+// sequences are short or the 256-row grid would not fill the CUs twice.
+// PA_QBLOCK_ROWS (128 or 256, read when a handle is created) forces one.
+constexpr int kBlockMMin = 128;
+int block_m(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S, int64_t MB) {
+  if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return 128;
+  if (tun.qblock_rows) return tun.qblock_rows;
+  if (T < 2 || S < 1) return 256;
+  const int G = c.num_q_heads / c.num_kv_heads;
+  const double waves256 =
+      (double)(prefill_items(T, S, 256 / G) * c.num_kv_heads) / (double)std::max(cus, 1);
+  const double tokens_per_seq = (double)T / (double)S;
+  const int64_t max_keys = MB * c.block_size;
+  if (tokens_per_seq <= 1536.0) return (max_keys <= 4736 || waves256 <= 1.33) ? 128 : 256;
+  return (tokens_per_seq <= 3072.0 && waves256 > 9.14) ? 128 : 256;
+}
 
 int decode_workers(int cus) { return std::min(std::max(cus, 1), kMaxCus) * pa::kDecodeWaves; }
 
@@ -185,10 +210,14 @@ WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
 }
 
 pa_tunables tunables_from_env() {
-  pa_tunables t{kMinStepsDefault};
+  pa_tunables t{kMinStepsDefault, 0};
   if (const char* e = std::getenv("PA_DECODE_MIN_STEPS")) {
     const int v = std::atoi(e);
     if (v >= 1) t.decode_min_steps = std::min(v, 4096);
+  }
+  if (const char* e = std::getenv("PA_QBLOCK_ROWS")) {
+    const int v = std::atoi(e);
+    if (v == 128 || v == 256) t.qblock_rows = v;
   }
   return t;
 }
@@ -203,8 +232,8 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   p->decode_workers = decode_workers(cus);
   p->decode_min_steps = tun.decode_min_steps;
   p->decode_unit_heads = decode_unit_heads(c);
-  p->block_m = block_m(c);
-  p->block_q = block_m(c) / G;
+  p->block_m = block_m(c, tun, cus, T, S, MB);
+  p->block_q = p->block_m / G;
   p->prefill_tile = kPrefillTile;
   int64_t items = 0;
   if (S >= 1 && T >= 1 && max_len >= 1) {
@@ -333,6 +362,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   dp->dec = reinterpret_cast<int4*>(ws + wl.dec);
   dp->part_o = reinterpret_cast<float*>(ws + wl.part_o);
   dp->part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
+  pp->block_m = p.block_m;
   pp->block_q = p.block_q;
   pp->work_items = (int32_t)items;
   pp->seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
@@ -413,7 +443,7 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   // largest on the largest device, so that batch and device bound all.
   uint64_t best = kHeader;
   if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
-    const int64_t bq = block_m(*cfg) / (cfg->num_q_heads / cfg->num_kv_heads);
+    const int64_t bq = kBlockMMin / (cfg->num_q_heads / cfg->num_kv_heads);   // most Q-blocks
     const int64_t items = max_tokens >= 2 ? prefill_items(max_tokens, max_seqs, bq) : 0;
     best = ws_layout(*cfg, decode_workers(kMaxCus), max_seqs, items).total;
   }

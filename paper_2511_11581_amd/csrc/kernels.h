@@ -7,15 +7,11 @@
 namespace pa {
 
 constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernels
-// Q-block kernels: bf16 caches use 8 waves x 32 rows (BLOCK_M = 256, two
-// waves per SIMD working in alternating phases) with tiles loaded straight
-// into LDS; fp8 caches 4 waves x 32 rows (BLOCK_M = 128) with tiles
-// converted to bf16 on their way into LDS.
-constexpr int kQblockWaves = 8;
+// Q-block kernels: waves of 32 rows.  bf16 caches: 8 waves (BLOCK_M = 256,
+// one workgroup per CU, two waves per SIMD) or 4 waves (BLOCK_M = 128, two
+// workgroups per CU), tiles copied straight into LDS; fp8 caches: 4 waves
+// (BLOCK_M = 128), tiles converted to bf16 on their way into LDS.
 constexpr int kQblockWaveRows = 32;
-__host__ __device__ constexpr int prefill_block_m(int elem_bytes) {
-  return elem_bytes == 1 ? 128 : kQblockWaveRows * kQblockWaves;
-}
 // Decode workgroup: 4 waves, one workgroup per CU (its LDS use keeps a
 // second one out), so one wave per SIMD.  With two waves on a SIMD the
 // memory system serves the first wave slot first and the second finishes
@@ -96,6 +92,7 @@ __host__ __device__ inline int active_workers(int64_t total, int64_t min_steps, 
 }
 
 struct PrefillPlan {
+  int32_t block_m;     // rows per Q-block (BLOCK_M; bf16: 256 or 128, i.e. 8 or 4 waves)
   int32_t block_q;     // query tokens per Q-block (BLOCK_M / group)
   int32_t work_items;  // Q-block slots in the grid (upper bound)
   int32_t* seq_start;  // [num_seqs + 1] prefix sums of Q-blocks per sequence

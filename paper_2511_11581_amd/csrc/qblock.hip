@@ -55,10 +55,7 @@ namespace pa {
 
 namespace {
 
-constexpr int kWaves = kQblockWaves;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kTile = kPrefillTileKeys;
-constexpr int kStages = 4;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16v2 __attribute__((ext_vector_type(2)));
@@ -112,21 +109,33 @@ __device__ __forceinline__ void wait_vm_lds() {
 // stores the bytes of every valid key into the dense outputs a.kd / a.vd:
 // K read back at the matrix-core operand addresses, V through the loader's
 // swizzle (pa_debug_gather).
-template <int D, bool GATHER>
-__global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, PrefillPlan pp) {
+//
+// W waves of 32 rows: BLOCK_M = 32 W.  W = 8: one workgroup per CU (128 KB
+// of LDS: K and V rings of 4 stages, tiles t + 1 .. t + 3 in flight).  W =
+// 4: two workgroups per CU (80 KB each: a K ring of 3 stages and a V ring of
+// 2; period t loads V of tile t + 1 and K of tile t + 3), so that one
+// workgroup's barrier waits and start-up run under the other's products.
+template <int D, int W, bool GATHER>
+__global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, PrefillPlan pp) {
   constexpr int RB = 2 * D;                        // bytes per cached row
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
   constexpr int TB = kTile * RB;                   // bytes per K (or V) tile
   constexpr int RPI = 1024 / RB;                   // rows per load instruction
-  constexpr int NLD = kTile / (RPI * kWaves);      // load instructions per wave, tile and tensor
+  constexpr int NLD = kTile / (RPI * W);           // load instructions per wave, tile and tensor
   constexpr int KRW = 256 / RB;                    // K rows per 256-byte bank window
   constexpr int NT = D / 16;                       // k-steps of K Q^T
   constexpr int NDB = D / 32;                      // 32-row d blocks of O^T
-  constexpr int VBASE = kStages * TB;              // V ring after the K ring
-  static_assert(kQblockWaveRows == 32 && kWaves == 8, "two groups of 4 waves x 32 rows");
-  static_assert(NLD >= 1 && NLD * RPI * kWaves == kTile, "tile loads");
+  constexpr int KSTG = W == 8 ? 4 : 3;             // K ring stages
+  constexpr int VSTG = W == 8 ? 4 : 2;             // V ring stages
+  constexpr bool kSplit = W != 8;                  // K and V of one period from different tiles
+  constexpr int VBASE = KSTG * TB;                 // V ring after the K ring
+  static_assert(kQblockWaveRows == 32 && (W == 8 || W == 4), "8 or 4 waves x 32 rows");
+  static_assert(NLD >= 1 && NLD * RPI * W == kTile, "tile loads");
   static_assert(RPI <= 16, "one instruction stays inside one 16-key block");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStages * TB];
+  static_assert((KSTG + VSTG) * TB * (8 / W) <= 160 * 1024, "workgroups per CU fit the LDS");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[(KSTG + VSTG) * TB];
+  auto kst = [](int t) { return t % KSTG; };   // ring stage of tile t's K
+  auto vst = [](int t) { return t % VSTG; };   // ring stage of tile t's V
 
   const int tid = __builtin_amdgcn_workitem_id_x(), lane = tid & 63, wave = uniform(tid >> 6);
   const int n = lane & 31, hf = lane >> 5;
@@ -175,13 +184,13 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
       qt[t] = __builtin_bit_cast(bf16x8, ld16_cached(qrow + 2 * (16 * t + 8 * hf)));
   }
 
-  // ---- loader geometry.  A wave loads kTile / kWaves = 8 consecutive rows
+  // ---- loader geometry.  A wave loads kTile / W = 8 or 16 consecutive rows
   //      of every tile, which lie in one cache block (block_size >= 16):
   //      instruction k covers rows wrow + RPI k .. + RPI - 1, lane i takes
   //      row wrow + RPI k + i / CPR and LDS slot i % CPR, i.e. logical chunk
   //      (i % CPR) ^ f(row).
-  constexpr int kWaveRows = kTile / kWaves;
-  static_assert(kWaveRows * kWaves == kTile && kWaveRows <= 16, "a wave's rows of a tile stay in one block");
+  constexpr int kWaveRows = kTile / W;
+  static_assert(kWaveRows * W == kTile && kWaveRows <= 16, "a wave's rows of a tile stay in one block");
   const int wrow = kWaveRows * wave;
   auto fK = [](int r) { return (r / KRW) & (CPR - 1); };
   auto fV = [](int r) { return (CPR / 4) * (r & 3) + (CPR / 8) * ((r >> 2) & 1); };
@@ -207,19 +216,19 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   load_twin(0);
   __builtin_amdgcn_s_waitcnt(0);   // Q and the window (one latency for both)
 
-  // Loads of tile t into ring stage st, in two parts so that the address
-  // work can sit between matrix-core products: issue_prep(t) finds the
-  // wave's page (rare: moves the window, draining the loads in flight),
-  // issue_part(j) sends instruction j of ND (K if j is even, else V).
-  // Callers clamp t to the last tile but keep st = (unclamped tile) %
-  // kStages, so a clamped re-load never lands in the stage that holds the
-  // real last tile.
+  // Loads of tile t, in parts so that the address work can sit between
+  // matrix-core products: issue_prep(t) finds the wave's page of tile t
+  // (rare: moves the window, draining the loads in flight), issue_kpart /
+  // issue_vpart(t, k) send instruction k of NLD of its K / V into the tile's
+  // ring stage.  With split rings the V tiles asked for trail the K tiles by
+  // two, so a moved window starts two tiles back.
   constexpr int ND = 2 * NLD;   // load instructions per wave and tile
+  constexpr int kLag = kSplit ? 2 : 0;
   const uint8_t* kp = kbase;
   const uint8_t* vp = vbase;
   auto issue_prep = [&](int t) {
     if (t - tb >= 64) {
-      tb = uniform(t);
+      tb = uniform(max(t - kLag, 0));
       load_twin(tb);
       __builtin_amdgcn_s_waitcnt(0);
     }
@@ -228,24 +237,35 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     kp = kbase + (uint64_t)pg * kblk + (uint32_t)(rb * (int)a.kg.slot);
     vp = vbase + (uint64_t)pg * vblk + (uint32_t)(rb * (int)a.vg.slot);
   };
-  auto issue_part = [&](int st, int j) {
-    const int k = j >> 1;
-    const int ldo = (wave * NLD + k) * 1024;
-    if ((j & 1) == 0)
-      dma16(kp + koff[k], lds_addr(lds + st * TB + ldo));
-    else
-      dma16(vp + voff[k], lds_addr(lds + VBASE + st * TB + ldo));
+  auto issue_kpart = [&](int t, int k) {
+    dma16(kp + koff[k], lds_addr(lds + kst(t) * TB + (wave * NLD + k) * 1024));
   };
-  auto issue = [&](int t, int st) {
+  auto issue_vpart = [&](int t, int k) {
+    dma16(vp + voff[k], lds_addr(lds + VBASE + vst(t) * TB + (wave * NLD + k) * 1024));
+  };
+  auto issue_k = [&](int t) {
     issue_prep(t);
 #pragma unroll
-    for (int j = 0; j < ND; ++j) issue_part(st, j);
+    for (int k = 0; k < NLD; ++k) issue_kpart(t, k);
+  };
+  auto issue_v = [&](int t) {
+    issue_prep(t);
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) issue_vpart(t, k);
+  };
+  auto issue = [&](int t) {   // K and V of tile t (K, V alternating)
+    issue_prep(t);
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) {
+      issue_kpart(t, k);
+      issue_vpart(t, k);
+    }
   };
   // V rows at or past kv_len (last tile only) may hold anything, NaN
   // included, and would poison P V even with zero weights: each lane zeroes
   // the chunks it loaded, after its own loads have landed.
   auto zero_tail = [&](int t) {
-    const int st = t & (kStages - 1);
+    const int st = vst(t);
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
       const int r = RPI * (wave * NLD + k) + lane / CPR;
@@ -379,11 +399,12 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   // LDS operands are read kAhead products ahead into a small register ring;
   // a scheduling fence after every product keeps each step's work in place.
   constexpr int kAhead = 4;
-  static_assert(2 + 3 * ND <= NS + 1, "tile loads fit between the score products");
+  static_assert(kSplit ? 3 + 4 * NLD <= NS + NP : 2 + 3 * ND <= NS + 1,
+                "tile loads fit between the products");
   auto period = [&](int t, auto full_tag) {
     constexpr bool kFullP = decltype(full_tag)::value;
-    const uint8_t* ks = lds + ((t + 1) & (kStages - 1)) * TB;
-    uint8_t* vs = lds + (t & (kStages - 1)) * TB;
+    const uint8_t* ks = lds + kst(t + 1) * TB;
+    uint8_t* vs = lds + vst(t) * TB;
     auto rd = [&](int i) -> bf16x8 {   // operand of product i (i < NS: K, else V^T)
       if (i < NS) return *(const bf16x8*)(ks + kaddr[i >> 1] + 32 * RB * (i & 1));
       const int u = (i - NS) / NDB, db = (i - NS) % NDB;
@@ -408,12 +429,30 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
         o[p % NDB] = mfma32(op, pb[p / NDB], o[p % NDB]);
       }
       if (i + kAhead < NS + NP) ring[(i - I0) % kAhead] = rd(i + kAhead);
-      if constexpr (kFullP) {
-        // loads of tile t + 3 between the score products
+      if constexpr (kFullP && !kSplit) {
+        // K and V of tile t + 3 between the score products, alternating
         if (t + 3 < ntiles) {
           if (i == 1) issue_prep(t + 3);
-          if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) issue_part((t + 3) & (kStages - 1), (i - 2) / 3);
+          if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) {
+            const int j = (i - 2) / 3;
+            if (j & 1) issue_vpart(t + 3, j >> 1);
+            else issue_kpart(t + 3, j >> 1);
+          }
         }
+      }
+      if constexpr (kFullP && kSplit) {
+        // V of tile t + 1, then K of tile t + 3, one instruction every
+        // second product
+        if (t + 1 < ntiles) {
+          if (i == 1) issue_prep(t + 1);
+          if (i >= 2 && i < 2 + 2 * NLD && (i & 1) == 0) issue_vpart(t + 1, (i - 2) / 2);
+        }
+        if (t + 3 < ntiles) {
+          if (i == 2 + 2 * NLD) issue_prep(t + 3);
+          if (i >= 3 + 2 * NLD && i < 3 + 4 * NLD && ((i - 3) & 1) == 0) issue_kpart(t + 3, (i - 3 - 2 * NLD) / 2);
+        }
+      }
+      if constexpr (kFullP) {
         if (i == NS - 1 && t + 1 >= nfull) mask(t + 1);
         if (i >= NS) valu_step(i - NS);
       }
@@ -429,7 +468,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
     if (ctx + tok_hi != min(a.seq_lens[seq], a.mb * a.block_size)) return;   // not the last Q-block
     const int64_t kd0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
     for (int t = 0; t < ntiles; ++t) {
-      issue(t, 0);
+      issue(t);
       wait_vm_lds<0>();
       __builtin_amdgcn_s_barrier();   // every wave's rows of tile t have landed
       // K: waves 0 / 1 store keys 0..31 / 32..63 from the operand addresses
@@ -440,7 +479,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
           for (int tt = 0; tt < NT; ++tt)
             *(u32x4*)(a.kd + kd0 + (int64_t)key * a.d_tok + 16 * (2 * tt + hf)) =
-                *(const u32x4*)(lds + kaddr[tt] + 32 * RB * wave);
+                *(const u32x4*)(lds + kst(t) * TB + kaddr[tt] + 32 * RB * wave);
       }
       // V: each wave its own rows, chunk slot s holding logical chunk s ^ fV(row)
 #pragma unroll
@@ -449,23 +488,37 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
         const int key = t * kTile + r;
         if (key < kv_len)
           *(u32x4*)(a.vd + kd0 + (int64_t)key * a.d_tok + 16 * c) =
-              *(const u32x4*)(lds + VBASE + (wave * NLD + k) * 1024 + 16 * lane);
+              *(const u32x4*)(lds + VBASE + vst(t) * TB + (wave * NLD + k) * 1024 + 16 * lane);
       }
       wait_vm_lds<0>();
-      __builtin_amdgcn_s_barrier();   // stage 0 read by every wave before the next copies
+      __builtin_amdgcn_s_barrier();   // the stages read by every wave before they are reused
     }
     return;
   }
 
-  // ---- prologue: tiles 0, 1, 2 in flight; scores and weights of tile 0,
-  //      whose row max becomes the first reference
-  issue(0, 0);
-  if (ntiles > 1) issue(1, 1);
-  if (ntiles > 2) issue(2, 2);
-  auto wait_first = [&]() {   // tile 0 landed; tiles 1, 2 may still fly
-    if (ntiles > 2) wait_vm_lds<2 * ND>();
-    else if (ntiles == 2) wait_vm_lds<ND>();
-    else wait_vm_lds<0>();
+  // ---- prologue: tiles 0, 1, 2 in flight (split rings: K of tiles 0, 1,
+  //      V of tile 0, K of tile 2, in that order); scores and weights of
+  //      tile 0, whose row max becomes the first reference
+  if constexpr (!kSplit) {
+    issue(0);
+    if (ntiles > 1) issue(1);
+    if (ntiles > 2) issue(2);
+  } else {
+    issue_k(0);
+    if (ntiles > 1) issue_k(1);
+    issue_v(0);
+    if (ntiles > 2) issue_k(2);
+  }
+  auto wait_first = [&]() {   // tile 0's K (and V) landed; later loads may still fly
+    if constexpr (!kSplit) {
+      if (ntiles > 2) wait_vm_lds<2 * ND>();
+      else if (ntiles == 2) wait_vm_lds<ND>();
+      else wait_vm_lds<0>();
+    } else {
+      if (ntiles > 2) wait_vm_lds<3 * NLD>();
+      else if (ntiles == 2) wait_vm_lds<2 * NLD>();
+      else wait_vm_lds<0>();
+    }
   };
   wait_first();
   if (ntiles == 1) zero_tail(0);
@@ -488,24 +541,42 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
 #pragma unroll
   for (int i = 0; i < 16; ++i) nm[i] = -m_run * inv_c;
 
-  // ---- tile periods.  sync(t): tile t + 1 has landed for every wave and
-  //      every wave has finished period t - 1, so the stage of tile t - 1
-  //      takes the loads of tile t + 3.  The O rescale owed by the softmax
-  //      of tile t is applied before the products of tile t.
+  // ---- tile periods.  sync(t): K of tile t + 1 and V of tile t have
+  //      landed for every wave and every wave has finished period t - 1, so
+  //      the stages that held tile t - 1 (K of tile t with split rings) take
+  //      this period's loads.  The O rescale owed by the softmax of tile t is
+  //      applied before the products of tile t.
   auto sync = [&](int t) {
-    // this wave's loads of tile t + 1 have landed (those of t + 2, if it
-    // exists, may still fly)
-    auto wait_next = [&]() {
-      if (t + 2 < ntiles) wait_vm_lds<ND>();
-      else wait_vm_lds<0>();
-    };
-    wait_next();
-    if (t + 1 == ntiles - 1) zero_tail(t + 1);
-    wait_next();
+    if constexpr (!kSplit) {
+      // this wave's loads of tile t + 1 have landed (those of t + 2, if it
+      // exists, may still fly)
+      auto wait_next = [&]() {
+        if (t + 2 < ntiles) wait_vm_lds<ND>();
+        else wait_vm_lds<0>();
+      };
+      wait_next();
+      if (t + 1 == ntiles - 1) zero_tail(t + 1);
+      wait_next();
+    } else {
+      // K of tile t + 1 and V of tile t have landed (K of tile t + 2, issued
+      // after them, may still fly)
+      auto wait_next = [&]() {
+        if (t + 2 < ntiles) wait_vm_lds<NLD>();
+        else wait_vm_lds<0>();
+      };
+      wait_next();
+      if (t == ntiles - 1) zero_tail(t);
+      wait_next();
+    }
     __builtin_amdgcn_s_barrier();
   };
-  auto load_next = [&](int t) {
-    if (t + 3 < ntiles) issue(t + 3, (t + 3) & (kStages - 1));
+  auto load_next = [&](int t) {   // period t's loads, outside the products
+    if constexpr (!kSplit) {
+      if (t + 3 < ntiles) issue(t + 3);
+    } else {
+      if (t + 1 < ntiles) issue_v(t + 1);
+      if (t + 3 < ntiles) issue_k(t + 3);
+    }
   };
   auto rescale = [&]() {
     if (resc) {
@@ -520,7 +591,7 @@ __global__ __launch_bounds__(kThreads, 1) void qblock_kernel(BatchArgs a, Prefil
   for (; t + 1 < nact; ++t) {
     sync(t);
     rescale();
-    period(t, kFull);   // issues the loads of tile t + 3 as well
+    period(t, kFull);   // issues this period's loads as well
   }
   sync(t);
   load_next(t);
@@ -568,12 +639,21 @@ hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim,
                          bool gather) {
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
-  dim3 grid((unsigned)blocks), block(kThreads);
-  if (head_dim == 128 && !gather) qblock_kernel<128, false><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && !gather) qblock_kernel<64, false><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 128) qblock_kernel<128, true><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64) qblock_kernel<64, true><<<grid, block, 0, st>>>(a, p);
-  else return hipErrorInvalidValue;
+  const int W = p.block_m / kQblockWaveRows;
+  const dim3 grid((unsigned)blocks), block(64 * W);
+#define PA_QB(DD, WW, GG) qblock_kernel<DD, WW, GG><<<grid, block, 0, st>>>(a, p)
+  if (W == 8) {
+    if (head_dim == 128) gather ? PA_QB(128, 8, true) : PA_QB(128, 8, false);
+    else if (head_dim == 64) gather ? PA_QB(64, 8, true) : PA_QB(64, 8, false);
+    else return hipErrorInvalidValue;
+  } else if (W == 4) {
+    if (head_dim == 128) gather ? PA_QB(128, 4, true) : PA_QB(128, 4, false);
+    else if (head_dim == 64) gather ? PA_QB(64, 4, true) : PA_QB(64, 4, false);
+    else return hipErrorInvalidValue;
+  } else {
+    return hipErrorInvalidValue;
+  }
+#undef PA_QB
   return hipGetLastError();
 }
 

@@ -23,6 +23,25 @@ def seed_of(name: str) -> int:
 
 
 @contextlib.contextmanager
+def _env(name, value):
+    old = os.environ.get(name)
+    os.environ[name] = str(value)
+    try:
+        yield
+    finally:
+        if old is None:
+            del os.environ[name]
+        else:
+            os.environ[name] = old
+
+
+def qblock_rows(n):
+    """Handles created inside use Q-blocks of n rows (PA_QBLOCK_ROWS, bf16
+    caches: 128 or 256), whatever the tuned rule would pick."""
+    return _env("PA_QBLOCK_ROWS", n)
+
+
+@contextlib.contextmanager
 def decode_min_steps(n):
     """Handles created inside take the decode minimum share n (the planner
     knob PA_DECODE_MIN_STEPS, read when a handle is created)."""

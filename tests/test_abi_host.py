@@ -219,6 +219,31 @@ def test_plan_prefill_grid_bounds_the_q_blocks():
     assert p1["prefill_launch"] == 0
 
 
+@pytest.mark.parametrize("S,q,ctx,Hq,rows", [
+    (4, 2048, 0, 32, 256),      # varlen-prefill-like: long prompts, several grid waves
+    (16, 4096, 4096, 32, 256),  # large batch over long keys
+    (1, 64, 4096, 32, 128),     # short prompt on a long context: few units
+    (64, 16, 4096, 32, 128),    # many short chunks
+    (32, 256, 0, 64, 128),      # short prompts, G = 8
+    (1, 4096, 0, 32, 256),
+])
+def test_plan_q_block_rows_follow_the_tuned_tree(S, q, ctx, Hq, rows):
+    # The exported rule of the offline BLOCK_M sweep (Sec. 5 / Fig. 8): the
+    # faster of the two Q-block shapes on each swept batch.
+    MB = -(-(q + ctx) // 16)
+    p = plan(cfg(Hq, 8, 128), cus=256, T=S * q, S=S, MB=MB)
+    assert p["block_m"] == rows and p["block_q"] == rows // (Hq // 8)
+
+
+def test_plan_q_block_rows_can_be_forced(monkeypatch):
+    monkeypatch.setenv("PA_QBLOCK_ROWS", "128")
+    assert plan(cfg(), cus=256, T=6589, S=4, MB=188)["block_m"] == 128
+    monkeypatch.setenv("PA_QBLOCK_ROWS", "256")
+    assert plan(cfg(), cus=256, T=64, S=4, MB=16)["block_m"] == 256
+    monkeypatch.setenv("PA_QBLOCK_ROWS", "100")   # not a kernel shape: ignored
+    assert plan(cfg(), cus=256, T=64, S=4, MB=16)["block_m"] == 128
+
+
 @pytest.mark.parametrize("Hq,Hkv,d,bs,kv,status", [
     (32, 8, 128, 16, pa.PA_DTYPE_BF16, pa.PA_OK),
     (12, 4, 128, 16, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),   # G = 3

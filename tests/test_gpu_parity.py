@@ -10,8 +10,8 @@ import pytest
 import torch
 
 from paper_2511_11581_amd import workloads as W
-from gpu_util import (SENTINEL, attention_for, check_close, oracle_full, oracle_rows, run_gpu,
-                      sample_rows, seed_of, valid_token_count)
+from gpu_util import (SENTINEL, attention_for, check_close, oracle_full, oracle_rows, qblock_rows,
+                      run_gpu, sample_rows, seed_of, valid_token_count)
 
 pytestmark = pytest.mark.gpu
 
@@ -76,6 +76,27 @@ def test_small_batches_match_oracle(name):
     w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=seed_of(name),
                      name=name, **extra)
     full_check(w)
+
+
+FORCED_ROWS = ["prefill_g4", "prefill_g8_d64", "prefill_g16", "chunked", "ragged_tails",
+               "prefill_bs256", "mixed"]
+
+
+@pytest.mark.parametrize("rows", [128, 256])
+@pytest.mark.parametrize("name", FORCED_ROWS)
+def test_both_q_block_shapes_match_oracle(name, rows):
+    # bf16 Q-block kernel with 4 waves (128 rows, two workgroups per CU) and
+    # 8 waves (256 rows), whichever the tuned rule would pick
+    seqs, Hq, Hkv, d, kv, bs, extra = SMALL[name]
+    w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=seed_of(name),
+                     name=f"{name}_rows{rows}", **extra)
+    with qblock_rows(rows):
+        att = attention_for(w)
+    assert att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]))["block_m"] == rows
+    out = run_gpu(w, att)
+    T = valid_token_count(w)
+    check_close(out[:T], oracle_full(w)[:T], w.kv_fp8, w.name)
+    assert (out[T:].float() == SENTINEL).all()
 
 
 def test_shuffled_mixed_order():
