@@ -87,7 +87,9 @@ typedef struct pa_config {
   int32_t num_q_heads;     /* Hq */
   int32_t num_kv_heads;    /* Hkv; Hq % Hkv == 0; G = Hq / Hkv must divide 128 and be <= 16 */
   int32_t head_dim;        /* d: 64 or 128 */
-  int32_t block_size;      /* tokens per KV-cache block: a power of two >= 16 */
+  int32_t block_size;      /* tokens per KV-cache block: any multiple of 16 in [16, 2^20]
+                              (powers of two, and the large non-power-of-two sizes
+                              of hybrid attention / state-space models, Sec. 4.6) */
   int32_t kv_dtype;        /* PA_DTYPE_BF16 or PA_DTYPE_FP8_E4M3 */
   float k_scale;           /* fp8 dequantisation: K = decode(k_cache) * k_scale (1 for bf16) */
   float v_scale;           /* V = decode(v_cache) * v_scale (1 for bf16) */

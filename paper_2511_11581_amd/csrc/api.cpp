@@ -114,8 +114,8 @@ pa_status check_config(const pa_config* c) {
     return fail(PA_ERR_UNSUPPORTED, "query heads per kv head must be 1, 2, 4, 8 or 16 (got %d)", G);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PA_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
-  if (c->block_size < 16 || (c->block_size & (c->block_size - 1)) != 0 || c->block_size > (1 << 20))
-    return fail(PA_ERR_UNSUPPORTED, "block_size must be a power of two >= 16 (got %d)",
+  if (c->block_size < 16 || c->block_size % 16 != 0 || c->block_size > (1 << 20))
+    return fail(PA_ERR_UNSUPPORTED, "block_size must be a multiple of 16 in [16, 2^20] (got %d)",
                 c->block_size);
   if (c->kv_dtype != PA_DTYPE_BF16 && c->kv_dtype != PA_DTYPE_FP8_E4M3)
     return fail(PA_ERR_UNSUPPORTED, "kv_dtype must be bf16 or fp8 e4m3 (got %d)", c->kv_dtype);
@@ -327,7 +327,7 @@ pa_status check_batch(const pa_config& c, const pa_tensor* q, const pa_tensor* k
     return fail(PA_ERR_INVALID_ARG, "out must have the shape of q");
   if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
   if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences per call (got %lld)", (long long)S);
-  if (MB * c.block_size > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
+  if (MB * c.block_size > INT32_MAX - 65536) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
   for (const pa_tensor* kv : {k, v})
     if ((int64_t)c.block_size * kv->stride[1] * elem_bytes(kv->dtype) >= INT32_MAX ||
         kv->stride[2] * elem_bytes(kv->dtype) >= INT32_MAX)
@@ -370,6 +370,17 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   pp->list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
   pp->count = reinterpret_cast<int32_t*>(ws + wl.count);
   pp->rec = reinterpret_cast<int4*>(ws + wl.rec);
+}
+
+// floor(p / bs) by multiply-high and shift (see pa::BlockDiv).
+pa::BlockDiv block_div(int bs) {
+  int l = 0;
+  while ((1 << l) < bs) ++l;   // ceil(log2 bs), bs >= 16
+  pa::BlockDiv d;
+  d.mul = (uint32_t)((((uint64_t)1 << (31 + l)) + (uint64_t)bs - 1) / (uint64_t)bs);
+  d.shr = l - 1;
+  d.bs = bs;
+  return d;
 }
 
 pa::KvGeom geom(const pa_tensor* t) {
@@ -662,7 +673,7 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   a.num_tokens = (int32_t)sh.T;
   a.num_blocks = (int32_t)std::min<int64_t>(sh.NB, INT32_MAX);
   a.block_size = c.block_size;
-  a.bs_log2 = __builtin_ctz(c.block_size);
+  a.bdiv = block_div(c.block_size);
   a.num_q_heads = c.num_q_heads;
   a.num_kv_heads = c.num_kv_heads;
   a.group = c.num_q_heads / c.num_kv_heads;
@@ -761,7 +772,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
     return fail(PA_ERR_INVALID_ARG, "k_dense and v_dense must share strides");
   if (S > 65535) return fail(PA_ERR_UNSUPPORTED, "at most 65535 sequences");
   if (S > 0 && NB < 1) return fail(PA_ERR_INVALID_ARG, "the cache holds no blocks");
-  if (MB * c.block_size > INT32_MAX) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
+  if (MB * c.block_size > INT32_MAX - 65536) return fail(PA_ERR_UNSUPPORTED, "block table too wide");
   for (const pa_tensor* kv : {k_cache, v_cache})
     if ((int64_t)c.block_size * kv->stride[1] * elem_bytes(kv->dtype) >= INT32_MAX ||
         kv->stride[2] * elem_bytes(kv->dtype) >= INT32_MAX ||
@@ -798,7 +809,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   a.num_tokens = (int32_t)num_tokens;
   a.num_blocks = (int32_t)std::min<int64_t>(NB, INT32_MAX);
   a.block_size = c.block_size;
-  a.bs_log2 = __builtin_ctz(c.block_size);
+  a.bdiv = block_div(c.block_size);
   a.num_q_heads = c.num_q_heads;
   a.num_kv_heads = c.num_kv_heads;
   a.group = c.num_q_heads / c.num_kv_heads;
@@ -872,7 +883,7 @@ pa_status pa_cache_write(pa_handle* h, const pa_tensor* key, const pa_tensor* va
   a.num_kv_heads = c.num_kv_heads;
   a.head_dim = c.head_dim;
   a.block_size = c.block_size;
-  a.bs_log2 = __builtin_ctz(c.block_size);
+  a.bdiv = block_div(c.block_size);
   a.fp8 = c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 0;
   a.k_scale = c.k_scale;
   a.v_scale = c.v_scale;

@@ -52,7 +52,7 @@ __global__ __launch_bounds__(64) void baseline_kernel(BatchArgs a) {
   float m = -__builtin_inff(), l = 0.f;
   const int32_t* btr = a.bt + (int64_t)s * a.bt_row;
   for (int p0 = 0; p0 < nkeys; p0 += a.block_size) {   // one page per tile
-    const int blk = page_of(btr, p0, a.bs_log2, a.num_blocks);
+    const int blk = page_of(btr, p0, a.bdiv, a.num_blocks);
     const int nk = min(a.block_size, nkeys - p0);
     const uint8_t* kb = a.k + (int64_t)blk * a.kg.blk + (int64_t)g * a.kg.head;
     const uint8_t* vb = a.v + (int64_t)blk * a.vg.blk + (int64_t)g * a.vg.head;

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void cache_write_kernel(CacheWriteArgs a) {
   if (t >= a.num_tokens) return;
   const int slot = uniform(a.slots[t]);
   if (slot < 0 || (int64_t)slot >= a.num_slots) return;
-  const int blk = slot >> a.bs_log2, off = slot & (a.block_size - 1);
+  const int blk = a.bdiv.block(slot), off = slot - a.block_size * blk;
   const int cpr = a.head_dim / 8;   // 16-byte input chunks per head row
   const int nch = a.num_kv_heads * cpr;
   uint8_t* krow = a.kc + (int64_t)blk * a.kg.blk + (int64_t)off * a.kg.slot;

@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.h"
+
 namespace pa {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
@@ -94,8 +96,8 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 // Physical block holding logical key position p of a sequence, read from its
 // block-table row and clamped into [0, num_blocks) so that a corrupt table
 // can never address memory outside the cache.
-__device__ __forceinline__ int page_of(const int32_t* bt_row, int p, int bs_log2, int num_blocks) {
-  int b = bt_row[p >> bs_log2];
+__device__ __forceinline__ int page_of(const int32_t* bt_row, int p, const BlockDiv& bd, int num_blocks) {
+  int b = bt_row[bd.block(p)];
   b = b < 0 ? 0 : b;
   return b >= num_blocks ? num_blocks - 1 : b;
 }

@@ -124,7 +124,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
   const int lq = lane & 3, lc = lane >> 2;     // loading coordinates
   const int hl = lc / LPH, ci = lc % LPH;      // head of the unit and chunk of its row this lane loads
-  const int Hkv = a.num_kv_heads, G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
+  const int Hkv = a.num_kv_heads, G = a.group;
+  const BlockDiv bd = a.bdiv;   // block size: a multiple of 16, so no 16-key block straddles two
 
   const int J = p.meta[0], Wn = p.meta[1];
   const int w = blockIdx.x * kDecodeWaves + wave;
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   auto load_window = [&](const Piece& pc, int first, int (&win)[NWIN]) {
     const int32_t* bt_row = a.bt + (int64_t)pc.s * a.bt_row;
 #pragma unroll
-    for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(((first + 64 * i + lane) * 16) >> bsl, a.mb - 1)];
+    for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(bd.block((first + 64 * i + lane) * 16), a.mb - 1)];
   };
   auto make_piece = [&](int jj, int gu, int k0, int64_t budget) {
     if (jj + 1 - base > 63) reload(jj);
@@ -237,7 +238,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   // the window registers; refill() must have made the step's blocks resident).
   auto issue = [&](const uint8_t* base, const KvGeom& geo, uint32_t off, int k, LT (&rows)[R]) {
     const int blk0 = uniform(k * BPS - cb);
-    const int kb0 = (k * KS) & bsm;
 #pragma unroll
     for (int b = 0; b < BPS; ++b) {
       const int bi = blk0 + b;   // never straddles registers: 64 % BPS == 0
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
 #pragma unroll
       for (int i = 1; i < NWIN; ++i) pg = (bi >> 6) == i ? lane_i(win[i], bi & 63) : pg;
       pg = pg < 0 ? 0 : (pg >= a.num_blocks ? a.num_blocks - 1 : pg);
-      const int sb = (kb0 + 16 * b) & bsm;
+      const int sb = bd.slot(k * KS + 16 * b);   // slot of the 16-key block's first key
       const uint8_t* bp = base + (int64_t)pg * geo.blk + (int64_t)cur.g * geo.head + (int64_t)sb * geo.slot;
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) rows[4 * b + r4] = ldn<LB>(bp + 4 * r4 * geo.slot + off);

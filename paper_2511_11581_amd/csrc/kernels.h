@@ -20,6 +20,23 @@ constexpr int kQblockWaveRows = 32;
 // measured no faster than one wave per SIMD with one step in flight.
 constexpr int kDecodeWaves = 4;
 
+// Division of a key position (0 <= p < 2^31) by the block size, any
+// multiple of 16 up to 2^20: floor(p / bs) = mulhi(p, mul) >> shr with
+// l = ceil(log2 bs), mul = ceil(2^(31 + l) / bs) < 2^32, shr = l - 1
+// (division by invariant integers using multiplication, Granlund and
+// Montgomery 1994, Thm. 4.2 for 31-bit numerators).
+struct BlockDiv {
+  uint32_t mul;
+  int32_t shr;
+  int32_t bs;
+  __host__ __device__ int block(int p) const { return (int)(__umulhi_u32((uint32_t)p, mul) >> shr); }
+  __host__ __device__ int slot(int p) const { return p - bs * block(p); }
+  // mulhi of 32-bit operands on host and device
+  __host__ __device__ static uint32_t __umulhi_u32(uint32_t a, uint32_t b) {
+    return (uint32_t)(((uint64_t)a * b) >> 32);
+  }
+};
+
 struct KvGeom {
   int64_t blk;   // bytes between physical blocks
   int64_t slot;  // bytes between token slots of one block
@@ -40,7 +57,7 @@ struct BatchArgs {
   uint8_t* out;
   int64_t o_tok, o_head;        // out strides (bytes)
   int32_t num_seqs, num_tokens, num_blocks, block_size;
-  int32_t bs_log2;              // block_size = 1 << bs_log2
+  BlockDiv bdiv;                // key position -> (block, slot)
   int32_t num_q_heads, num_kv_heads, group;  // group = Hq / Hkv
   float sl2;                    // softmax scale * log2(e) * k_scale
   float v_scale;
@@ -135,7 +152,8 @@ struct CacheWriteArgs {
   uint8_t* vc;
   KvGeom kg, vg;
   int64_t num_slots;       // NB * block_size
-  int32_t num_tokens, num_kv_heads, head_dim, block_size, bs_log2;
+  int32_t num_tokens, num_kv_heads, head_dim, block_size;
+  BlockDiv bdiv;
   int32_t fp8;
   float k_scale, v_scale;  // fp8: stored code = e4m3fn(value / scale)
 };

@@ -56,7 +56,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
   const int Hkv = a.num_kv_heads;
   const int g = blockIdx.x % Hkv;
   const int wi = blockIdx.x / Hkv;
-  const int G = a.group, BQ = pp.block_q, bsl = a.bs_log2, bsm = a.block_size - 1;
+  const int G = a.group, BQ = pp.block_q;
+  const BlockDiv bd = a.bdiv;   // block size: a multiple of 16
 
   if (wi >= pp.count[0]) return;
   const int seq = uniform(pp.list_seq[wi]);
@@ -95,9 +96,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
   // ---- loader geometry.  Tile t covers keys [64t, 64t + 64).  K load i of
   // this thread reads key kk_i = (tid + 256 i) / CH, 16-byte chunk tid % CH;
   // all keys of one wave's K load fall in one 16-key block, so its block-table
-  // lookup is wave-uniform (scalar).  V: thread (m = vt & 15, c = vt >> 4)
-  // reads keys 4m..4m+3, chunk c (one lookup per thread).  Keys past kv_len
-  // read clamped block-table entries and are zeroed when written to LDS.
+  // lookup is wave-uniform (scalar): the page and the slot of the group's
+  // first key, the lanes' rows at fixed offsets from it.  V: thread (m = vt &
+  // 15, c = vt >> 4) reads keys 4m..4m+3, chunk c (one lookup per thread).
+  // Keys past kv_len read clamped block-table entries (at in-block slots) and
+  // are zeroed when written to LDS.
   const int vtask = tid % VTASKS;
   const int vm = vtask & 15, vc = vtask >> 4;
   // (Offsets inside one block fit in 32 bits: the host checks
@@ -107,34 +110,41 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 #pragma unroll
   for (int i = 0; i < KLD; ++i) {
     const int kk = (tid + kThreads * i) / CH;
-    kkw[i] = uniform(kk);
-    koff[i] = (kk & bsm) * (int)a.kg.slot + 16 * ((tid + kThreads * i) % CH);
+    kkw[i] = uniform(kk);   // the wave's first key of load i (lane 0's)
+    koff[i] = (kk - kkw[i]) * (int)a.kg.slot + 16 * ((tid + kThreads * i) % CH);
   }
-  const int voff = ((4 * vm) & bsm) * (int)a.vg.slot + 16 * vc;
+  const int voff = 16 * vc;
   const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
   const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
-  const int last_blk = (kv_len - 1) >> bsl;
+  const int last_blk = bd.block(kv_len - 1);
+  auto page = [&](int bi) {   // table entry bi (<= the last needed block), clamped into the cache
+    const int b = bt_row[min(bi, last_blk)];
+    return b < 0 ? 0 : (b >= a.num_blocks ? a.num_blocks - 1 : b);
+  };
 
-  int pg_k[KLD], pg_v;
-  auto load_pages = [&](int tile, int (&pk)[KLD], int& pv) {
+  // Pages and in-block slots of the first keys of this thread's loads.
+  int pg_k[KLD], sl_k[KLD], pg_v, sl_v;
+  auto load_pages = [&](int tile) {
     const int tb = tile * kTileN;
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
-      const int bi = min((tb + kkw[i]) >> bsl, last_blk);
-      pk[i] = uniform(page_of(bt_row, bi << bsl, bsl, a.num_blocks));
+      const int key0 = uniform(tb + kkw[i]), bi = uniform(bd.block(key0));
+      pg_k[i] = uniform(page(bi));
+      sl_k[i] = uniform(key0 - a.block_size * bi);
     }
-    pv = page_of(bt_row, min((tb + 4 * vm) >> bsl, last_blk) << bsl, bsl, a.num_blocks);
+    const int kv0 = tb + 4 * vm, bv = bd.block(kv0);
+    pg_v = page(bv);
+    sl_v = kv0 - a.block_size * bv;
   };
   u32x4 kreg[KLD];
   u32x4 vreg[4];
-  auto load_tile = [&](int tile, const int (&pk)[KLD], int pv) {
-    const int64_t toff = (int64_t)((tile * kTileN) & bsm);   // slot of the tile start when bs > 64
+  auto load_tile = [&]() {   // the tile whose pages load_pages found last
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
-      const uint8_t* base = kbase + (int64_t)pk[i] * a.kg.blk + toff * a.kg.slot;
+      const uint8_t* base = kbase + (int64_t)pg_k[i] * a.kg.blk + (int64_t)sl_k[i] * a.kg.slot;
       kreg[i] = ld16_cached(base + koff[i]);   // K/V are reused by other Q-blocks
     }
-    const uint8_t* vb = vbase + (int64_t)pv * a.vg.blk + toff * a.vg.slot + voff;
+    const uint8_t* vb = vbase + (int64_t)pg_v * a.vg.blk + (int64_t)sl_v * a.vg.slot + voff;
 #pragma unroll
     for (int r = 0; r < 4; ++r) vreg[r] = ld16_cached(vb + r * (int)a.vg.slot);
   };
@@ -299,8 +309,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     const int64_t d0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
     for (int tile = 0; tile < ntiles; ++tile) {
       const int tb = tile * kTileN;
-      load_pages(tile, pg_k, pg_v);
-      load_tile(tile, pg_k, pg_v);
+      load_pages(tile);
+      load_tile();
 #pragma unroll
       for (int i = 0; i < KLD; ++i) {
         const int flat = tid + kThreads * i;
@@ -317,9 +327,9 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     return;
   }
 
-  load_pages(0, pg_k, pg_v);
-  load_tile(0, pg_k, pg_v);
-  load_pages(min(1, ntiles - 1), pg_k, pg_v);
+  load_pages(0);
+  load_tile();
+  load_pages(min(1, ntiles - 1));
   store_tile(0);
   __syncthreads();
 
@@ -331,8 +341,8 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
     const int tb = tile * kTileN;
     // Unconditional (clamped) prefetch keeps the waits exact: the store of
     // tile + 1 waits only for its own loads, not the younger page lookups.
-    load_tile(min(tile + 1, ntiles - 1), pg_k, pg_v);
-    load_pages(min(tile + 2, ntiles - 1), pg_k, pg_v);
+    load_tile();                              // tile + 1 (clamped): pages found last iteration
+    load_pages(min(tile + 2, ntiles - 1));
     __builtin_amdgcn_sched_barrier(0);
     if (tb <= wave_pos_max) attend(tile, uniform(tile >= nfull) != 0);
     if (tile + 1 < ntiles) store_tile(tile + 1);

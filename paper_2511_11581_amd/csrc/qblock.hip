@@ -140,7 +140,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   const int tid = __builtin_amdgcn_workitem_id_x(), lane = tid & 63, wave = uniform(tid >> 6);
   const int n = lane & 31, hf = lane >> 5;
   const int Hkv = a.num_kv_heads;
-  const int G = a.group, bsl = a.bs_log2, bsm = a.block_size - 1;
+  const int G = a.group;
+  const BlockDiv bd = a.bdiv;   // block size: a multiple of 16
   const float c = a.sl2, inv_c = 1.f / a.sl2;   // scale * log2(e) (* k_scale)
   // One workgroup per (Q-block, kv head) unit, kv head fastest: with
   // round-robin dispatch over the 8 XCDs, the units of one kv head (Hkv =
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   if (tok_hi <= 0) return;
   const int kv_len = ctx + tok_hi;                 // keys the block needs
   const int ntiles = (kv_len + kTile - 1) / kTile;
-  const int last_blk = (kv_len - 1) >> bsl;
+  const int last_blk = bd.block(kv_len - 1);
   const int32_t* bt_row = a.bt + (int64_t)seq * a.bt_row;
 
   // This lane's row and the wave's range of causal bounds.
@@ -210,7 +211,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   int twin;
   int tb = 0;
   auto load_twin = [&](int first) {
-    const int p = bt_row[min((kTile * (first + lane) + wrow) >> bsl, last_blk)];
+    const int p = bt_row[min(bd.block(kTile * (first + lane) + wrow), last_blk)];
     twin = p < 0 ? 0 : (p >= a.num_blocks ? a.num_blocks - 1 : p);
   };
   load_twin(0);
@@ -233,7 +234,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
       __builtin_amdgcn_s_waitcnt(0);
     }
     const uint32_t pg = (uint32_t)__builtin_amdgcn_readlane(twin, t - tb);
-    const int rb = (kTile * t + wrow) & bsm;   // first row inside the block
+    const int rb = bd.slot(kTile * t + wrow);   // first row inside the block
     kp = kbase + (uint64_t)pg * kblk + (uint32_t)(rb * (int)a.kg.slot);
     vp = vbase + (uint64_t)pg * vblk + (uint32_t)(rb * (int)a.vg.slot);
   };

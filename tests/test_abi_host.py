@@ -250,6 +250,10 @@ def test_plan_q_block_rows_can_be_forced(monkeypatch):
     (64, 2, 128, 16, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),   # G = 32
     (32, 8, 96, 16, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),
     (32, 8, 128, 8, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),
+    (32, 8, 128, 24, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),    # not a multiple of 16
+    (32, 8, 128, 48, pa.PA_DTYPE_BF16, pa.PA_OK),
+    (32, 8, 128, 528, pa.PA_DTYPE_FP8_E4M3, pa.PA_OK),
+    (32, 8, 128, (1 << 20) + 16, pa.PA_DTYPE_BF16, pa.PA_ERR_UNSUPPORTED),
     (30, 8, 128, 16, pa.PA_DTYPE_BF16, pa.PA_ERR_INVALID_ARG),
     (32, 8, 128, 16, pa.PA_DTYPE_F32, pa.PA_ERR_UNSUPPORTED),
     (32, 8, 128, 32, pa.PA_DTYPE_FP8_E4M3, pa.PA_OK),

@@ -81,6 +81,14 @@ def test_strided_views_and_block_size_32():
     _case(T=77, Hkv=4, d=128, bs=32, NB=9, kv="fp8", ks=0.02, vs=0.02, seed=4, strided=True)
 
 
+@pytest.mark.parametrize("bs,kv", [(48, "bf16"), (80, "fp8"), (400, "bf16"), (528, "fp8"),
+                                   (64, "bf16"), (256, "fp8")])
+def test_block_sizes_beyond_16(bs, kv):
+    # powers of two and the non-power-of-two sizes of hybrid models: slot ->
+    # (block, offset) by the invariant-divisor multiply
+    _case(T=200, Hkv=2, d=128, bs=bs, NB=7, kv=kv, ks=0.05, vs=0.03, seed=bs)
+
+
 def test_full_mixed_batch_token_count():
     # the mixed batch's 4216 new tokens, Hkv 8, d 128, into a 300-block pool
     _case(T=4216, Hkv=8, d=128, bs=16, NB=300, kv="bf16", seed=21)

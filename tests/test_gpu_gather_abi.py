@@ -70,6 +70,10 @@ GATHER_CASES = {
     "wide_table_padded_rows": ([(70, 1), (0, 40), (0, 0)], 8, 2, 128, "bf16", 16,
                                dict(token_pad=5, table_width=20, pool_blocks=64)),
     "strided_window_moves": ([(70000, 1), (300, 1)], 8, 8, 128, "bf16", 16, {}),
+    "bf16_d128_bs48": ([(37, 1), (0, 100), (250, 7), (1, 0), (4100, 1)], 8, 2, 128, "bf16", 48, {}),
+    "fp8_d128_bs80": ([(600, 1), (0, 300), (190, 66), (8000, 1)], 16, 2, 128, "fp8", 80, {}),
+    "bf16_d64_bs400": ([(999, 1), (0, 257), (300, 2), (20000, 1)], 8, 2, 64, "bf16", 400, {}),
+    "fp8_d64_bs528_hu4": ([(1500, 1), (0, 77), (33, 1)], 16, 8, 64, "fp8", 528, {}),
 }
 
 

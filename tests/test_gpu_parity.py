@@ -67,6 +67,19 @@ SMALL = {
     "prefill_fp8_g16": ([(0, 45), (100, 9)], 16, 1, 128, "fp8", 32, {}),
     "chunked_fp8_long": ([(2000, 200), (64, 64), (5000, 3)], 32, 8, 128, "fp8", 16, {}),
     "mixed_fp8": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1), (0, 2)], 32, 8, 128, "fp8", 16, {}),
+    # block sizes that are multiples of 16 but not powers of two (the large
+    # pages of hybrid attention / state-space models, Sec. 4.6)
+    "decode_bs48": ([(990, 1), (47, 1), (48, 1), (4000, 1)], 8, 2, 128, "bf16", 48, {}),
+    "decode_bs80_fp8": ([(1800, 1), (79, 1), (300, 1)], 8, 1, 128, "fp8", 80, {}),
+    "decode_bs400_d64": ([(1025, 1), (399, 1), (2600, 1)], 4, 2, 64, "bf16", 400, {}),
+    "decode_bs528_fp8_d64": ([(3000, 1), (527, 1), (528, 1)], 16, 4, 64, "fp8", 528, {}),
+    "prefill_bs48": ([(0, 150), (70, 64), (300, 9)], 8, 2, 128, "bf16", 48, {}),
+    "prefill_bs80_d64": ([(0, 77), (100, 40), (0, 300)], 16, 2, 64, "bf16", 80, {}),
+    "prefill_bs400": ([(0, 700), (500, 33), (399, 2)], 8, 2, 128, "bf16", 400, {}),
+    "prefill_fp8_bs48": ([(0, 150), (200, 70)], 8, 2, 128, "fp8", 48, {}),
+    "prefill_fp8_bs400_d64": ([(0, 500), (300, 20)], 8, 2, 64, "fp8", 400, {}),
+    "mixed_bs528": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1), (0, 2)], 32, 8, 128, "bf16", 528, {}),
+    "mixed_fp8_bs80": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1)], 32, 8, 128, "fp8", 80, {}),
 }
 
 
@@ -79,7 +92,7 @@ def test_small_batches_match_oracle(name):
 
 
 FORCED_ROWS = ["prefill_g4", "prefill_g8_d64", "prefill_g16", "chunked", "ragged_tails",
-               "prefill_bs256", "mixed"]
+               "prefill_bs256", "mixed", "prefill_bs48", "prefill_bs400"]
 
 
 @pytest.mark.parametrize("rows", [128, 256])
