@@ -92,12 +92,12 @@ def measured_traffic(kernel, workload):
     return (k["fetch_kib"] * 1024 * cal["fetch_scale"] + k["write_kib"] * 1024 * cal["write_scale"])
 
 
-def make_attention(w, profile=False):
+def make_attention(w, profile=False, no_split_kv=False):
     from paper_2511_11581_amd import pa
     return pa.PagedAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size,
                              w.k_cache.dtype, w.k_scale, w.v_scale, max_tokens=w.num_tokens,
                              max_seqs=w.num_seqs, max_blocks_per_seq=int(w.block_table.shape[1]),
-                             profile=profile)
+                             profile=profile, no_split_kv=no_split_kv)
 
 
 def time_steps(w, att, out, steps, warmup):
@@ -245,11 +245,13 @@ def measure_cache_write(kv, steps, warmup, T=4216, Hkv=8, d=128, bs=16):
 
 
 def measure_ladder(steps=3, warmup=1):
-    """The ablation of the paper's optimisation ladder on this GPU: the
-    baseline decomposition (one wave per (token, q head), one page per tile)
-    against the full path, for 16 sequences (ctx U[512, 4096], Hq 32 / Hkv 8,
-    d 128, bf16) whose decode share is 0, 50 or 100 % (decode rows q = 1,
-    the others chunked prefill q = 128).  Relative numbers only."""
+    """The paper's optimisation ladder (Sec. 7) on this GPU, three rungs: the
+    baseline decomposition (one wave per (token, q head), one page per tile),
+    Q-blocks without the split-KV decode kernel (single-token rows as
+    Q-blocks of one token, no split, no merge), and the full path; for 16
+    sequences (ctx U[512, 4096], Hq 32 / Hkv 8, d 128, bf16) whose decode
+    share is 0, 50 or 100 % (decode rows q = 1, the others chunked prefill
+    q = 128).  Relative numbers only."""
     import torch
     from paper_2511_11581_amd import workloads as W
     g = torch.Generator().manual_seed(805)
@@ -261,9 +263,11 @@ def measure_ladder(steps=3, warmup=1):
         w = W.make_batch(seqs, 32, 8, 128, seed=805 + share, name=f"ladder{share}", device="cuda",
                          poison=False)
         att = make_attention(w)
+        att_nosplit = make_attention(w, no_split_kv=True)
         out = torch.empty_like(w.q)
         timings = {}
-        for rung, fn in (("baseline", att.forward_baseline), ("full", att.forward)):
+        for rung, fn in (("baseline", att.forward_baseline), ("qblock", att_nosplit.forward),
+                         ("full", att.forward)):
             for _ in range(warmup):
                 fn(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc,
                    w.scale, out=out)
@@ -276,9 +280,13 @@ def measure_ladder(steps=3, warmup=1):
             e1.record()
             torch.cuda.synchronize()
             timings[rung + "_us"] = e0.elapsed_time(e1) * 1e3 / steps
+        timings["baseline_over_qblock"] = timings["baseline_us"] / timings["qblock_us"]
+        timings["qblock_over_full"] = timings["qblock_us"] / timings["full_us"]
         timings["speedup"] = timings["baseline_us"] / timings["full_us"]
         res[str(share)] = timings
-        del w, att, out
+        att.close()
+        att_nosplit.close()
+        del w, att, att_nosplit, out
         torch.cuda.empty_cache()
     return res
 
@@ -387,7 +395,8 @@ def main():
         ladder = measure_ladder()
         for share, r in ladder.items():
             print(f"# ladder, decode share {share}%: baseline decomposition {r['baseline_us']:.0f} us, "
-                  f"full path {r['full_us']:.0f} us ({r['speedup']:.1f}x)", file=sys.stderr)
+                  f"Q-blocks without split {r['qblock_us']:.0f} us, full path {r['full_us']:.0f} us "
+                  f"({r['speedup']:.1f}x)", file=sys.stderr)
 
     decode_like = args.config != 3
     h = headline

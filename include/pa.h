@@ -83,6 +83,14 @@ typedef struct pa_tensor {
  * durations.  Adds two event records per launch; off by default. */
 #define PA_FLAG_PROFILE 2u
 
+/* Ablation only (the middle rung of the optimisation ladder of Sec. 7):
+ * rows with one query token go through the Q-block kernel too, as Q-blocks
+ * of one token whose G heads are the rows (Sec. 4.4), with no split of
+ * their keys and no merge, instead of through the split-KV decode kernel
+ * (Sec. 4.5).  Same results within the tolerances; slower on small batches
+ * of long rows. */
+#define PA_FLAG_NO_SPLIT_KV 4u
+
 typedef struct pa_config {
   int32_t num_q_heads;     /* Hq */
   int32_t num_kv_heads;    /* Hkv; Hq % Hkv == 0; G = Hq / Hkv must divide 128 and be <= 16 */

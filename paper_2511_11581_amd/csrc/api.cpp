@@ -121,7 +121,7 @@ pa_status check_config(const pa_config* c) {
     return fail(PA_ERR_UNSUPPORTED, "kv_dtype must be bf16 or fp8 e4m3 (got %d)", c->kv_dtype);
   if (!(c->k_scale > 0.f) || !(c->v_scale > 0.f))
     return fail(PA_ERR_INVALID_ARG, "k_scale and v_scale must be positive");
-  if (c->flags & ~(PA_FLAG_VALIDATE | PA_FLAG_PROFILE))
+  if (c->flags & ~(PA_FLAG_VALIDATE | PA_FLAG_PROFILE | PA_FLAG_NO_SPLIT_KV))
     return fail(PA_ERR_INVALID_ARG, "unknown flags 0x%x", c->flags);
   if (c->workspace && (reinterpret_cast<uintptr_t>(c->workspace) & 255))
     return fail(PA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -129,7 +129,12 @@ pa_status check_config(const pa_config* c) {
 }
 
 // Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) + (#sequences with q_i >= 2).
-int64_t prefill_items(int64_t T, int64_t S, int64_t bq) { return cdiv(T, bq) + std::min<int64_t>(S, T / 2); }
+// Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) +
+// (#sequences with q_i >= qmin), qmin = 2 (1 when single-token rows also
+// take Q-blocks).
+int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin = 2) {
+  return cdiv(T, bq) + std::min<int64_t>(S, T / qmin);
+}
 
 int decode_unit_heads(const pa_config& c);
 int decode_step_keys(const pa_config& c) {
@@ -137,7 +142,7 @@ int decode_step_keys(const pa_config& c) {
   return pa::decode_step_keys(decode_unit_heads(c) * c.head_dim * eb, eb);
 }
 
-int64_t prefill_items(int64_t T, int64_t S, int64_t bq);
+int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 
 // Rows per Q-block.  fp8 caches: 128 (one kernel shape).  bf16 caches: 256
 // (8 waves, one workgroup per CU) or 128 (4 waves, two workgroups per CU),
@@ -155,7 +160,7 @@ int block_m(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int6
   if (T < 2 || S < 1) return 256;
   const int G = c.num_q_heads / c.num_kv_heads;
   const double waves256 =
-      (double)(prefill_items(T, S, 256 / G) * c.num_kv_heads) / (double)std::max(cus, 1);
+      (double)(prefill_items(T, S, 256 / G, 2) * c.num_kv_heads) / (double)std::max(cus, 1);
   const double tokens_per_seq = (double)T / (double)S;
   const int64_t max_keys = MB * c.block_size;
   if (tokens_per_seq <= 1536.0) return (max_keys <= 4736 || waves256 <= 1.33) ? 128 : 256;
@@ -245,9 +250,10 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
     p->merge_grid[0] = S;
     p->merge_grid[1] = (G + 3) / 4;
     p->merge_grid[2] = c.num_kv_heads;
-    if (T >= 2 && max_len >= 2) {
+    const int qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
+    if (T >= qmin && max_len >= qmin) {
       p->prefill_launch = 1;
-      items = prefill_items(T, S, p->block_q);
+      items = prefill_items(T, S, p->block_q, qmin);
       p->prefill_units = items * c.num_kv_heads;
       p->prefill_grid[0] = p->prefill_units;   // one workgroup per unit
       p->prefill_grid[1] = 1;
@@ -364,6 +370,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   dp->part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
   pp->block_m = p.block_m;
   pp->block_q = p.block_q;
+  pp->qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
   pp->work_items = (int32_t)items;
   pp->seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
   pp->list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
@@ -455,7 +462,8 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   uint64_t best = kHeader;
   if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
     const int64_t bq = kBlockMMin / (cfg->num_q_heads / cfg->num_kv_heads);   // most Q-blocks
-    const int64_t items = max_tokens >= 2 ? prefill_items(max_tokens, max_seqs, bq) : 0;
+    const int qmin = (cfg->flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
+    const int64_t items = max_tokens >= qmin ? prefill_items(max_tokens, max_seqs, bq, qmin) : 0;
     best = ws_layout(*cfg, decode_workers(kMaxCus), max_seqs, items).total;
   }
   *bytes = best;

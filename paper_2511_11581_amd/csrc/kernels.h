@@ -111,6 +111,7 @@ __host__ __device__ inline int active_workers(int64_t total, int64_t min_steps, 
 struct PrefillPlan {
   int32_t block_m;     // rows per Q-block (BLOCK_M; bf16: 256 or 128, i.e. 8 or 4 waves)
   int32_t block_q;     // query tokens per Q-block (BLOCK_M / group)
+  int32_t qmin;        // fewest query tokens of a Q-block row (2; 1: no split-KV decode rows)
   int32_t work_items;  // Q-block slots in the grid (upper bound)
   int32_t* seq_start;  // [num_seqs + 1] prefix sums of Q-blocks per sequence
   int32_t* list_seq;   // [work_items] sequence of the w-th Q-block (planned order)

@@ -86,10 +86,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
       t0 = a.qsl[i];
       const int q = a.qsl[i + 1] - t0;
       L = min(a.seq_lens[i], cap);
-      if (q == 1 && t0 >= 0 && t0 < a.num_tokens && L >= 1) {
+      if (q == 1 && pp.qmin == 2 && t0 >= 0 && t0 < a.num_tokens && L >= 1) {
         v[0] = 1;
         v[1] = (L + dp.step_keys - 1) / dp.step_keys;
-      } else if (with_prefill && q >= 2 && t0 >= 0 && t0 + q <= a.num_tokens && L >= q) {
+      } else if (with_prefill && q >= pp.qmin && t0 >= 0 && t0 + q <= a.num_tokens && L >= q) {
         v[2] = (q + bq - 1) / bq;
       }
     }

@@ -36,6 +36,7 @@ PA_DTYPE_I32 = 2
 PA_DTYPE_F32 = 3
 PA_FLAG_VALIDATE = 1
 PA_FLAG_PROFILE = 2
+PA_FLAG_NO_SPLIT_KV = 4
 PA_KERNEL_KINDS = 4
 KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
@@ -279,9 +280,12 @@ class PagedAttention:
                  kv_dtype: torch.dtype = torch.bfloat16, k_scale: float = 1.0,
                  v_scale: float = 1.0, max_tokens: int = 1, max_seqs: int = 1,
                  max_blocks_per_seq: int = 1, validate: bool = False, profile: bool = False,
-                 device="cuda"):
+                 no_split_kv: bool = False, device="cuda"):
+        """no_split_kv: ablation only, single-token rows through the Q-block
+        kernel (PA_FLAG_NO_SPLIT_KV)."""
         kvd = _DTYPES.get(kv_dtype, -1)
-        flags = (PA_FLAG_VALIDATE if validate else 0) | (PA_FLAG_PROFILE if profile else 0)
+        flags = ((PA_FLAG_VALIDATE if validate else 0) | (PA_FLAG_PROFILE if profile else 0)
+                 | (PA_FLAG_NO_SPLIT_KV if no_split_kv else 0))
         cfg = make_config(num_q_heads, num_kv_heads, head_dim, block_size, kvd, k_scale, v_scale,
                           flags)
         nbytes = pa_workspace_bytes(cfg, max_tokens, max_seqs, max_blocks_per_seq)

@@ -56,12 +56,14 @@ def decode_min_steps(n):
             os.environ["PA_DECODE_MIN_STEPS"] = old
 
 
-def attention_for(w, validate=False, max_tokens=None, max_seqs=None, max_blocks=None):
+def attention_for(w, validate=False, max_tokens=None, max_seqs=None, max_blocks=None,
+                  no_split_kv=False):
     return pa.PagedAttention(
         w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size, w.k_cache.dtype,
         w.k_scale, w.v_scale,
         max_tokens=max_tokens or max(1, w.num_tokens), max_seqs=max_seqs or max(1, w.num_seqs),
-        max_blocks_per_seq=max_blocks or max(1, int(w.block_table.shape[1])), validate=validate)
+        max_blocks_per_seq=max_blocks or max(1, int(w.block_table.shape[1])), validate=validate,
+        no_split_kv=no_split_kv)
 
 
 def run_gpu(w, att=None, out=None):
