@@ -1,9 +1,12 @@
 #!/usr/bin/env python3
 """Paged-attention benchmark on one MI355X.
 
-A step is one pa_forward call over one batch (every kernel of the path:
-decode split-KV + log-sum-exp merge for single-token rows, the Q-block
-kernel for the rest), inputs resident in HBM.  The headline workload is the
+A step is one pa_forward_hinted call over one batch (every kernel of the
+path: decode split-KV + log-sum-exp merge for single-token rows, the Q-block
+kernel for the rest; the hint is what the host knows of the batch, the
+number of single-token rows and the longest query, and only drops launches
+that would find no work), inputs resident in HBM.  The plain pa_forward
+time is reported next to it.  The headline workload is the
 Llama-3-8B-shaped decode batch (64 sequences, context U[512, 8192], Hq 32 /
 Hkv 8, d 128, bf16, block size 16); the other four benchmark batches are
 measured in the same run and reported under "configs".
@@ -100,24 +103,47 @@ def make_attention(w, profile=False, no_split_kv=False):
                              profile=profile, no_split_kv=no_split_kv)
 
 
-def time_steps(w, att, out, steps, warmup):
-    """Mean ms per step over `steps` calls, events on the launch stream."""
+def hint_of(w):
+    """What the host knows of the batch (pa_forward_hinted): the number of
+    single-token rows and the longest query."""
+    return (sum(1 for q in w.q_lens if q == 1), max(w.q_lens + [0]))
+
+
+def time_steps(w, att, out, steps, warmup, hint=None):
+    """Mean ms per step over `steps` back-to-back calls, events on the launch
+    stream around all of them."""
     import torch
     args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
     for _ in range(warmup):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record()
     for _ in range(steps):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     ev1.record()
     torch.cuda.synchronize()
     return ev0.elapsed_time(ev1) / steps
 
 
-def time_graph(w, att, out, steps, warmup):
+def per_call_ms(w, att, out, steps, hint=None):
+    """Per-call durations (an event pair around each call): median, min, max."""
+    import torch
+    args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record()
+        att.forward(*args, w.scale, out=out, hint=hint)
+        e1.record()
+    torch.cuda.synchronize()
+    t = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    return {"median": t[len(t) // 2], "min": t[0], "max": t[-1]}
+
+
+def time_graph(w, att, out, steps, warmup, hint=None):
     """Mean ms per replay of one pa_forward captured in a HIP graph (the
     launch overhead of the eager calls gone; the same kernels and work)."""
     import torch
@@ -125,12 +151,12 @@ def time_graph(w, att, out, steps, warmup):
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     for _ in range(warmup):
         g.replay()
     torch.cuda.synchronize()
@@ -145,43 +171,94 @@ def time_graph(w, att, out, steps, warmup):
     return ev0.elapsed_time(ev1) / steps
 
 
-def per_kernel_ms(w, out, steps, warmup):
+def per_kernel_ms(w, out, steps, warmup, hint=None):
     """Average duration of each kernel (HIP events recorded by the library
     around every launch on the same stream)."""
     import torch
     att = make_attention(w, profile=True)
     args = (w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc)
     for _ in range(warmup):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     torch.cuda.synchronize()
     att.profile(reset=True)
     for _ in range(steps):
-        att.forward(*args, w.scale, out=out)
+        att.forward(*args, w.scale, out=out, hint=hint)
     prof = att.profile(reset=True)
     att.close()
     return {k: (tot / n if n else 0.0) for k, (n, tot) in prof.items()}
 
 
-def measure(k, steps, warmup):
+def sampled_error(w, out, nrows=256, seed=0):
+    """Max / mean abs error of `out` against the fp64 oracle on sampled rows
+    (first and last token of every sequence plus random ones; every row of
+    every batch is compared in the GPU tests)."""
+    import numpy as np
+    import oracle
+    wc = w.to("cpu")
+    qsl = wc.query_start_loc.tolist()
+    rng = np.random.default_rng(seed)
+    rows = set()
+    for i in range(len(qsl) - 1):
+        if qsl[i + 1] > qsl[i]:
+            rows.add((qsl[i], int(rng.integers(w.num_q_heads))))
+            rows.add((qsl[i + 1] - 1, int(rng.integers(w.num_q_heads))))
+    nrows = min(nrows, qsl[-1] * w.num_q_heads)   # a batch may hold fewer rows
+    while len(rows) < nrows:
+        rows.add((int(rng.integers(qsl[-1])), int(rng.integers(w.num_q_heads))))
+    rows = sorted(rows)
+    import concurrent.futures as cf
+    nt = oracle.default_threads()
+    chunks = np.array_split(np.asarray(rows, dtype=np.int64), min(nt, len(rows)))
+
+    def one(ch):
+        return oracle.rows(wc.q, wc.k_cache, wc.v_cache, wc.block_table, wc.seq_lens,
+                           wc.query_start_loc, wc.scale, ch, k_scale=wc.k_scale, v_scale=wc.v_scale)
+
+    with cf.ThreadPoolExecutor(max_workers=len(chunks)) as ex:
+        ref = np.concatenate(list(ex.map(one, chunks)), 0)
+    got = out.cpu()
+    g = np.stack([got[t, h].double().numpy() for t, h in rows])
+    err = np.abs(g - ref)
+    return {"rows": len(rows), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean())}
+
+
+def measure(k, steps, warmup, block_size=None, with_error=True):
     import torch
     from paper_2511_11581_amd import workloads as W
-    w = W.make_config(k, device="cuda", poison=False)
+    if block_size is None:
+        w = W.make_config(k, device="cuda", poison=False)
+    else:   # the same batch on pages of another size
+        seqs, kw, gen, seed = W.config_seqs(k)
+        w = W.make_batch(seqs, seed=seed, device="cuda", poison=False, block_size=block_size,
+                         name=f"config{k}-bs{block_size}", _gen=gen, **kw)
     att = make_attention(w)
     out = torch.empty_like(w.q)
+    hint = hint_of(w)
     ms = time_steps(w, att, out, steps, warmup)
+    ms_h = time_steps(w, att, out, steps, warmup, hint)
+    calls = per_call_ms(w, att, out, steps, hint)
     gms = time_graph(w, att, out, steps, warmup)
-    kms = per_kernel_ms(w, out, steps, warmup)
+    gms_h = time_graph(w, att, out, steps, warmup, hint)
+    kms = per_kernel_ms(w, out, steps, warmup, hint)
     plan = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]))
+    err = sampled_error(w, out, seed=k) if with_error else None
     att.close()
     B, F = alg_bytes(w), alg_flops(w)
     res = {
         "config": k, "name": W.CONFIG_NAMES[k], "seed": w.seed, "sum_L": sum(w.seq_len_list),
-        "us_per_batch": ms * 1e3, "graph_us_per_batch": gms * 1e3, "alg_bytes": B, "alg_flops": F,
-        "GBps": B / (ms * 1e-3) / 1e9, "TFLOPs": F / (ms * 1e-3) / 1e12,
+        "block_size": w.block_size,
+        "us_per_batch": ms_h * 1e3, "us_per_batch_unhinted": ms * 1e3,
+        "us_median": calls["median"] * 1e3, "us_min": calls["min"] * 1e3, "us_max": calls["max"] * 1e3,
+        "graph_us_per_batch": gms_h * 1e3, "graph_us_per_batch_unhinted": gms * 1e3,
+        "hint": {"num_decode_seqs": hint[0], "max_query_len": hint[1]},
+        "alg_bytes": B, "alg_flops": F,
+        "GBps": B / (ms_h * 1e-3) / 1e9, "TFLOPs": F / (ms_h * 1e-3) / 1e12,
         "per_kernel_us": {kk: v * 1e3 for kk, v in kms.items() if v > 0},
         "plan": {kk: plan[kk] for kk in ("decode_step", "decode_workers", "decode_min_steps",
-                                         "block_q", "decode_grid", "prefill_grid")},
+                                         "block_m", "block_q", "decode_grid", "prefill_grid")},
     }
+    if err:
+        res["error_vs_oracle"] = err
     res["frac_hbm"] = res["GBps"] / HBM_PEAK_GBS
     res["frac_mfma"] = res["TFLOPs"] / BF16_PEAK_TFLOPS
     db, pf = decode_bytes(w), prefill_flops(w)
@@ -320,7 +397,14 @@ def cpu_baseline(w, budget_s=15.0, flops=False):
     s = sub(m)
     t = run(s) if m != probe.num_seqs else tp
     value, unit = (alg_flops(s) / t / 1e12, "TFLOP/s") if flops else (alg_bytes(s) / t / 1e9, "GB/s")
-    return {"value": value, "unit": unit, "cores": threads, "kind": "oracle",
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next(l.split(":", 1)[1].strip() for l in fh if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    return {"value": value, "unit": unit, "cores": threads, "kind": "oracle", "cpu_model": model,
+            "nproc": os.cpu_count(),
             "sample": f"first {m} of {w.num_seqs} sequences (sum_L={sum(s.seq_len_list)}), "
                       f"fp64 C oracle, {t:.1f} s"}
 
@@ -365,20 +449,41 @@ def main():
         return
 
     configs = {}
+
+    def report(k, r):
+        e = r.get("error_vs_oracle") or {}
+        print(f"# config {k}: {r['us_per_batch']:.1f} us/batch (median {r['us_median']:.1f}, min "
+              f"{r['us_min']:.1f}; {r['us_per_batch_unhinted']:.1f} without the hint; "
+              f"{r['graph_us_per_batch']:.1f} replayed from a HIP graph), {r['GBps']:.0f} GB/s "
+              f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
+              f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}, "
+              f"error vs oracle max {e.get('max_abs_err', float('nan')):.2e} "
+              f"mean {e.get('mean_abs_err', float('nan')):.2e} ({e.get('rows', 0)} rows)", file=sys.stderr,
+              flush=True)
+
     headline_w, headline = measure(args.config, args.steps, args.warmup)
     configs[args.config] = headline
+    report(args.config, headline)
     if not args.only:
         for k in (1, 2, 3, 4, 5):
             if k != args.config:
                 _, r = measure(k, args.steps, args.warmup)
                 configs[k] = r
+                report(k, r)
                 torch.cuda.empty_cache()
-    for k in sorted(configs):
-        r = configs[k]
-        print(f"# config {k}: {r['us_per_batch']:.1f} us/batch ({r['graph_us_per_batch']:.1f} replayed "
-              f"from a HIP graph), {r['GBps']:.0f} GB/s "
-              f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
-              f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}", file=sys.stderr)
+
+    # the decode and prefill batches on non-power-of-two pages (hybrid models)
+    block_sizes = {}
+    if not args.only:
+        for k, bs in ((2, 528), (3, 400)):
+            _, r = measure(k, args.steps, args.warmup, block_size=bs, with_error=False)
+            block_sizes[f"config{k}_bs{bs}"] = {kk: r[kk] for kk in (
+                "block_size", "us_per_batch", "us_median", "GBps", "frac_hbm", "TFLOPs", "frac_mfma",
+                "per_kernel_us")}
+            print(f"# config {k} at block size {bs}: {r['us_per_batch']:.1f} us/batch, "
+                  f"{r['GBps']:.0f} GB/s, {r['TFLOPs']:.1f} TFLOP/s, kernels {r['per_kernel_us']}",
+                  file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
 
     cache_write = {}
     if not args.only:
@@ -388,7 +493,7 @@ def main():
             print(f"# cache write ({cw['tokens']} tokens, Hkv {cw['kv_heads']}, d {cw['head_dim']}, "
                   f"{kv} cache): {cw['us']:.1f} us per call replayed from a HIP graph "
                   f"({cw['us_eager']:.1f} us eager), {cw['GBps']:.0f} GB/s "
-                  f"({100 * cw['frac_hbm']:.1f}% HBM)", file=sys.stderr)
+                  f"({100 * cw['frac_hbm']:.1f}% HBM)", file=sys.stderr, flush=True)
 
     ladder = None
     if not args.only:
@@ -396,7 +501,7 @@ def main():
         for share, r in ladder.items():
             print(f"# ladder, decode share {share}%: baseline decomposition {r['baseline_us']:.0f} us, "
                   f"Q-blocks without split {r['qblock_us']:.0f} us, full path {r['full_us']:.0f} us "
-                  f"({r['speedup']:.1f}x)", file=sys.stderr)
+                  f"({r['speedup']:.1f}x)", file=sys.stderr, flush=True)
 
     decode_like = args.config != 3
     h = headline
@@ -426,10 +531,14 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if not headline_w.kv_fp8 else "bf16/fp8-kv",
         "data": "synthetic (seeded N(0,1) bf16 Q/K/V, random block tables)",
         "config": {"workload": h["name"], "seq_lens_sum": h["sum_L"], "seed": h["seed"],
-                   "us_per_batch": h["us_per_batch"], "graph_us_per_batch": h["graph_us_per_batch"],
+                   "block_size": h["block_size"], "us_per_batch": h["us_per_batch"],
+                   "us_median": h["us_median"], "us_min": h["us_min"],
+                   "us_per_batch_unhinted": h["us_per_batch_unhinted"],
+                   "graph_us_per_batch": h["graph_us_per_batch"], "hint": h["hint"],
                    "parallelism": "single GPU"},
         "roofline": roof, "cpu_baseline": cpu,
         "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
+        "block_sizes": block_sizes,
         "cache_write": cache_write,
         "ladder": ladder,
     }

@@ -201,6 +201,25 @@ pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,
                      const pa_tensor *out, pa_stream stream);
 
+/* Facts about a batch that the host already has (the metadata step of
+ * Sec. 6.1 computes them from host-side lengths), so that pa_forward_hinted
+ * skips launches that would find no work.  -1 means unknown. */
+typedef struct pa_batch_hint {
+  int32_t num_decode_seqs;  /* sequences with exactly one query token */
+  int32_t max_query_len;    /* the longest query length in the batch */
+} pa_batch_hint;
+
+/* pa_forward with a hint: num_decode_seqs == 0 skips the split-KV decode
+ * and merge launches; 0 <= max_query_len <= 1 skips the Q-block launch and
+ * its work list.  hint == NULL, or -1 in both fields, is pa_forward.  The
+ * hint must hold: rows of a kind the hint rules out are left unwritten
+ * (with PA_FLAG_VALIDATE a violated hint is reported as PA_ERR_DEVICE). */
+pa_status pa_forward_hinted(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
+                            const pa_tensor *v_cache, const pa_tensor *block_table,
+                            const pa_tensor *seq_lens, const pa_tensor *query_start_loc,
+                            float scale, const pa_tensor *out, const pa_batch_hint *hint,
+                            pa_stream stream);
+
 /* For callers that cannot allocate device memory (code under HIP-graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same
  * attention, kernels and arguments as pa_forward, but the call's scratch

@@ -365,6 +365,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   dp->min_steps = p.decode_min_steps;
   dp->unit_heads = p.decode_unit_heads;
   dp->meta = reinterpret_cast<int32_t*>(ws + wl.meta);
+  dp->fused = 0;
   dp->dec = reinterpret_cast<int4*>(ws + wl.dec);
   dp->part_o = reinterpret_cast<float*>(ws + wl.part_o);
   dp->part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
@@ -620,10 +621,13 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
                               const pa_tensor* v_cache, const pa_tensor* block_table,
                               const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
                               float scale, const pa_tensor* out, pa_stream stream, bool baseline,
-                              uint8_t* ws, uint64_t ws_bytes, bool static_scratch) {
+                              uint8_t* ws, uint64_t ws_bytes, bool static_scratch,
+                              const pa_batch_hint* hint = nullptr) {
   if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
   const pa_config& c = h->cfg;
   if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
+  if (hint && (hint->num_decode_seqs < -1 || hint->max_query_len < -1))
+    return fail(PA_ERR_INVALID_ARG, "hint fields must be >= -1");
   Shapes sh;
   TRY(check_batch(c, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, &sh));
   if (!(scale > 0.f) || !(scale < 1e30f)) return fail(PA_ERR_INVALID_ARG, "scale must be positive and finite");
@@ -647,7 +651,9 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     pa::ValidateArgs va{static_cast<const int32_t*>(block_table->data), block_table->stride[0],
                         (int32_t)sh.MB, static_cast<const int32_t*>(seq_lens->data),
                         static_cast<const int32_t*>(query_start_loc->data), (int32_t)sh.S,
-                        (int32_t)sh.T, (int32_t)sh.NB, c.block_size, word};
+                        (int32_t)sh.T, (int32_t)sh.NB, c.block_size,
+                        hint && hint->num_decode_seqs == 0 ? 1 : 0, hint ? hint->max_query_len : -1,
+                        word};
     e = pa::launch_validate(va, st);
     if (e != hipSuccess) return hip_fail(e, "validate launch");
     uint32_t host_word = 0;
@@ -657,7 +663,7 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     if (host_word)
       return fail(PA_ERR_DEVICE, "metadata check failed (code 0x%x: 1 qsl[0]!=0, 2 qsl decreasing, "
                   "4 q_len>seq_len, 8 seq_len>table capacity, 16 block id out of range, "
-                  "32 qsl[S]>num_tokens)", host_word);
+                  "32 qsl[S]>num_tokens, 64 batch hint violated)", host_word);
   }
 
   const bool fp8 = c.kv_dtype == PA_DTYPE_FP8_E4M3;
@@ -699,16 +705,39 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   pa::DecodePlan dp;
   pa::PrefillPlan pp;
   device_plans(c, p, ws, sh.S, &dp, &pp);
+  // What the hint rules out (the single-token rows take Q-blocks under
+  // PA_FLAG_NO_SPLIT_KV, so then only the Q-block launch is needed).
+  const bool no_split = (c.flags & PA_FLAG_NO_SPLIT_KV) != 0;
+  const bool run_decode = !no_split && !(hint && hint->num_decode_seqs == 0);
+  const bool run_qblock = p.prefill_launch &&
+                          !(hint && hint->max_query_len >= 0 && hint->max_query_len < (no_split ? 1 : 2));
 
-  hipError_t e = timed_launch(h, PA_KERNEL_PLAN, st,
-                              [&] { return pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st); });
+  // A batch the hint says is decode-only, with a decode list that fits in the
+  // decode kernel's LDS: the decode kernel builds the list itself (no plan
+  // launch), then the merge.
+  const int eb = fp8 ? 1 : 2;
+  const bool fused = run_decode && !run_qblock && hint && hint->max_query_len >= 0 &&
+                     sh.S < pa::decode_list_cap(c.head_dim, eb, p.decode_unit_heads);
+  hipError_t e;
+  if (fused) {
+    dp.fused = 1;
+    e = timed_launch(h, PA_KERNEL_DECODE, st,
+                     [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    return PA_OK;
+  }
+  e = timed_launch(h, PA_KERNEL_PLAN, st, [&] { return pa::launch_plan(a, dp, pp, run_qblock, st); });
   if (e != hipSuccess) return hip_fail(e, "plan launch");
-  e = timed_launch(h, PA_KERNEL_DECODE, st,
-                   [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
-  if (e != hipSuccess) return hip_fail(e, "decode launch");
-  e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
-  if (e != hipSuccess) return hip_fail(e, "merge launch");
-  if (p.prefill_launch) {
+  if (run_decode) {
+    e = timed_launch(h, PA_KERNEL_DECODE, st,
+                     [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+    if (e != hipSuccess) return hip_fail(e, "merge launch");
+  }
+  if (run_qblock) {
     e = timed_launch(h, PA_KERNEL_PREFILL, st,
                      [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
@@ -724,6 +753,17 @@ pa_status pa_forward(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
   return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
                       stream, false, static_cast<uint8_t*>(h->cfg.workspace), h->cfg.workspace_bytes,
                       false);
+}
+
+pa_status pa_forward_hinted(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,
+                            const pa_tensor* v_cache, const pa_tensor* block_table,
+                            const pa_tensor* seq_lens, const pa_tensor* query_start_loc,
+                            float scale, const pa_tensor* out, const pa_batch_hint* hint,
+                            pa_stream stream) {
+  if (!h) return fail(PA_ERR_INVALID_ARG, "handle is NULL");
+  return forward_impl(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                      stream, false, static_cast<uint8_t*>(h->cfg.workspace), h->cfg.workspace_bytes,
+                      false, hint);
 }
 
 pa_status pa_forward_noalloc(pa_handle* h, const pa_tensor* q, const pa_tensor* k_cache,

@@ -102,4 +102,47 @@ __device__ __forceinline__ int page_of(const int32_t* bt_row, int p, const Block
   return b >= num_blocks ? num_blocks - 1 : b;
 }
 
+// Block-wide exclusive scan of NV values per thread (NT threads, a multiple
+// of 64), all in one pass; tot[] receives the block totals.  Every thread of
+// the block must call it (it synchronises the block).
+template <int NV, int NT>
+__device__ void block_scan(const int (&v)[NV], int (&ex)[NV], int (&tot)[NV]) {
+  __shared__ int wsum[NV][NT / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) x[i] = v[i];
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int y = __shfl_up(x[i], o);
+      if (lane >= o) x[i] += y;
+    }
+  }
+  if (lane == 63)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) wsum[i][w] = x[i];
+  __syncthreads();
+  if (w == 0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int t = lane < NT / 64 ? wsum[i][lane] : 0;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(t, o);
+        if (lane >= o) t += y;
+      }
+      if (lane < NT / 64) wsum[i][lane] = t;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    ex[i] = (w > 0 ? wsum[i][w - 1] : 0) + x[i] - v[i];
+    tot[i] = wsum[i][NT / 64 - 1];
+  }
+  __syncthreads();
+}
+
 }  // namespace pa

@@ -86,6 +86,70 @@ struct Piece {
   int head, tail;      // the pair starts before / continues after this worker
 };
 
+// The log-sum-exp merge of one query head's pieces (Sec. 4.5), by one wave:
+// M = max_k m_k, out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k, lanes
+// over d.  Piece k sits with worker w0 + k (slot 1 for the pair's first
+// worker, slot 0 for the others), head hu of its unit, query head hh of the
+// group; the result goes to row `tok`, query head g G + hh.  The pieces'
+// (m, l) are read one per lane, 64 at a time, and their weights reach the
+// lanes by readlane.
+template <int D>
+__device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePlan& p, int w0, int n,
+                                             int hu, int hh, int tok, int g) {
+  constexpr int DPT = D / 64;   // d values per lane
+  const int lane = threadIdx.x & 63;
+  const int HU = p.unit_heads, G = a.group;
+  auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
+  float M = kNegInf;
+  for (int k0 = 0; k0 < n; k0 += 64) {
+    const int k = k0 + lane;
+    const float m = k < n ? p.part_ml[row_of(k) * 2] : kNegInf;
+    M = fmaxf(M, m);
+  }
+  M = xor16_max(M);
+  M = xor32_max(M);
+  M = fmaxf(M, __shfl_xor(M, 8));
+  M = fmaxf(M, __shfl_xor(M, 4));
+  M = fmaxf(M, __shfl_xor(M, 2));
+  M = fmaxf(M, __shfl_xor(M, 1));
+  float num[DPT] = {}, den = 0.f;
+  for (int k0 = 0; k0 < n; k0 += 64) {
+    const int k = k0 + lane;
+    f32x2 ml = {kNegInf, 0.f};
+    if (k < n) ml = *(const f32x2*)(p.part_ml + row_of(k) * 2);
+    const float wk = k < n ? fast_exp2(ml[0] - M) : 0.f;
+    den += wk * ml[1];
+    const int kn = min(64, n - k0);
+    // 8 pieces per round: their loads are independent and in flight together
+    for (int i0 = 0; i0 < kn; i0 += 8) {
+      float v[8][DPT];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int kk = min(i0 + i, kn - 1);
+        const float* po = p.part_o + row_of(k0 + kk) * D + lane * DPT;
+#pragma unroll
+        for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float wi = i0 + i < kn ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk), i0 + i)) : 0.f;
+#pragma unroll
+        for (int x = 0; x < DPT; ++x) num[x] += wi * v[i][x];
+      }
+    }
+  }
+  den = xor16_sum(den);
+  den = xor32_sum(den);
+  den += __shfl_xor(den, 8);
+  den += __shfl_xor(den, 4);
+  den += __shfl_xor(den, 2);
+  den += __shfl_xor(den, 1);
+  const float inv = a.v_scale / den;
+  uint8_t* orow = a.out + (int64_t)tok * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
+  if constexpr (DPT == 2) *(uint32_t*)orow = pack_bf16(num[0] * inv, num[1] * inv);
+  else *(__bf16*)orow = (__bf16)(num[0] * inv);
+}
+
 // GATHER: the same partition, block-table walk and loads, but every loaded
 // row chunk of a valid key is stored into the dense outputs a.kd / a.vd
 // instead of being computed with (pa_debug_gather).
@@ -115,10 +179,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   constexpr int NWIN = 4;                  // block-id registers per lane (window of 64 NWIN blocks)
   static_assert(64 % BPS == 0, "steps must not straddle block-id registers");
 
-  // LDS sized so that one workgroup fills a CU (a second would not fit).
-  constexpr int kLdsBytes = kDecodeWaves * WB > 80 * 1024 + 1024 ? kDecodeWaves * WB : 80 * 1024 + 1024;
+  // LDS sized so that one workgroup fills a CU (a second would not fit),
+  // the rest of the CU's LDS for a decode list built here (fused launches).
+  constexpr int kLdsBytes = decode_tile_lds(D, EB, HU);
+  constexpr int kListCap = decode_list_cap(D, EB, HU);
+  static_assert(WB == decode_wave_lds(D, EB, HU) && kLdsBytes >= kDecodeWaves * WB, "tile LDS");
   static_assert(kLdsBytes <= 160 * 1024 && 2 * kLdsBytes > 160 * 1024, "one workgroup per CU");
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
+  __shared__ int4 list_lds[GATHER ? 1 : kListCap + 1];
 
   const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
   const int q4 = lane >> 4, c16 = lane & 15;   // MFMA operand coordinates
@@ -127,11 +195,53 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   const int Hkv = a.num_kv_heads, G = a.group;
   const BlockDiv bd = a.bdiv;   // block size: a multiple of 16, so no 16-key block straddles two
 
-  const int J = p.meta[0], Wn = p.meta[1];
   const int w = blockIdx.x * kDecodeWaves + wave;
   const int Hu = Hkv / HU;                     // units per sequence
+  // The decode list: built by the plan kernel, or (fused launches, decode-
+  // only batches) by this workgroup in LDS, the same pass over the
+  // sequences as the plan kernel's.
+  int J, Wn;
+  const int4* dec = p.dec;
+  if (!GATHER && p.fused) {
+    const int tid = threadIdx.x, S = a.num_seqs, cap = a.mb * a.block_size;
+    int nj = 0, nsteps = 0;
+    for (int b0 = 0; b0 < S; b0 += 64 * kDecodeWaves) {
+      const int i = b0 + tid;
+      int v[2] = {0, 0}, t0 = 0, L = 0;
+      if (i < S) {
+        t0 = a.qsl[i];
+        const int q = a.qsl[i + 1] - t0;
+        L = min(a.seq_lens[i], cap);
+        if (q == 1 && t0 >= 0 && t0 < a.num_tokens && L >= 1) {
+          v[0] = 1;
+          v[1] = (L + p.step_keys - 1) / p.step_keys;
+        }
+      }
+      int ex[2], tot[2];
+      block_scan<2, 64 * kDecodeWaves>(v, ex, tot);
+      if (v[0] && nj + ex[0] < kListCap) list_lds[nj + ex[0]] = make_int4(i, t0, L, nsteps + ex[1]);
+      nj += tot[0];
+      nsteps += tot[1];
+    }
+    nj = min(nj, kListCap);   // (the host launches fused only for S < kListCap)
+    if (tid == 0) list_lds[nj] = make_int4(0, 0, 0, nsteps);
+    __syncthreads();
+    J = nj;
+    Wn = active_workers((int64_t)Hu * nsteps, p.min_steps, p.workers);
+    dec = list_lds;
+    if (blockIdx.x == 0) {   // the merge kernel, launched next, reads the list from the workspace
+      for (int i = tid; i <= nj; i += 64 * kDecodeWaves) p.dec[i] = list_lds[i];
+      if (tid == 0) {
+        p.meta[0] = J;
+        p.meta[1] = Wn;
+      }
+    }
+  } else {
+    J = p.meta[0];
+    Wn = p.meta[1];
+  }
   if (w >= Wn || J <= 0) return;
-  const int64_t Ttot = (int64_t)Hu * p.dec[J].w;
+  const int64_t Ttot = (int64_t)Hu * dec[J].w;
   int64_t t = worker_begin(w, Ttot, Wn);
   const int64_t t_end = worker_begin(w + 1, Ttot, Wn);
   if (t >= t_end) return;
@@ -142,13 +252,13 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   while (hi - lo > 63) {
     const int step = (hi - lo + 63) / 64;
     const int idx = lo + lane * step;
-    const int64_t P = (int64_t)Hu * p.dec[min(idx, J)].w;
+    const int64_t P = (int64_t)Hu * dec[min(idx, J)].w;
     const bool ok = idx < hi && P <= t;
     lo += (63 - __builtin_clzll(__ballot(ok))) * step;
     hi = min(hi, lo + step);
   }
   int base = lo;
-  int4 ent = p.dec[min(base + lane, J)];
+  int4 ent = dec[min(base + lane, J)];
   {
     const bool ok = base + lane < hi && (int64_t)Hu * ent.w <= t;
     lo = base + (63 - __builtin_clzll(__ballot(ok)));
@@ -156,7 +266,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   // Entry jj of the list (jj + 1 - base <= 63 must hold): fields by readlane.
   auto reload = [&](int jj) {   // rare: the wait below drains everything in flight
     base = jj;
-    ent = p.dec[min(base + lane, J)];
+    ent = dec[min(base + lane, J)];
     __builtin_amdgcn_s_waitcnt(0);
   };
 
@@ -540,15 +650,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
 }
 
 // Log-sum-exp merge of the pieces of every (sequence, kv head) pair that
-// spans several workers: M = max_k m_k, out = sum_k 2^(m_k - M) acc_k /
-// sum_k 2^(m_k - M) l_k (Sec. 4.5).  One wave per (pair, query head of the
-// group), lanes over d; the pair's first worker holds its piece in slot 1,
-// later workers in slot 0.  The pieces' (m, l) are read one per lane, 64 at
-// a time, and their weights reach the lanes by readlane.
+// spans several workers (Sec. 4.5), for launches without fused merges.  One
+// wave per (pair, query head of the group); pairs one worker finished exit.
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
-  constexpr int DPT = D / 64;   // d values per lane
-  const int lane = threadIdx.x & 63;
   const int jj = blockIdx.x, G = a.group;
   const int hh = uniform(blockIdx.y * 4 + (threadIdx.x >> 6));   // head within the group
   const int g = blockIdx.z;
@@ -562,57 +667,7 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
   const int64_t ta = (int64_t)Hu * e.w + (int64_t)gu * nt;
   const int w0 = worker_of(ta, Ttot, Wn), w1 = worker_of(ta + nt - 1, Ttot, Wn);
   if (w0 == w1) return;
-  const int n = w1 - w0 + 1;
-  // piece k of the pair sits with wave w0 + k, head hu of its unit
-  auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
-  float M = kNegInf;
-  for (int k0 = 0; k0 < n; k0 += 64) {
-    const int k = k0 + lane;
-    const float m = k < n ? p.part_ml[row_of(k) * 2] : kNegInf;
-    M = fmaxf(M, m);
-  }
-  M = xor16_max(M);
-  M = xor32_max(M);
-  M = fmaxf(M, __shfl_xor(M, 8));
-  M = fmaxf(M, __shfl_xor(M, 4));
-  M = fmaxf(M, __shfl_xor(M, 2));
-  M = fmaxf(M, __shfl_xor(M, 1));
-  float num[DPT] = {}, den = 0.f;
-  for (int k0 = 0; k0 < n; k0 += 64) {
-    const int k = k0 + lane;
-    f32x2 ml = {kNegInf, 0.f};
-    if (k < n) ml = *(const f32x2*)(p.part_ml + row_of(k) * 2);
-    const float wk = k < n ? fast_exp2(ml[0] - M) : 0.f;
-    den += wk * ml[1];
-    const int kn = min(64, n - k0);
-    // 8 pieces per round: their loads are independent and in flight together
-    for (int i0 = 0; i0 < kn; i0 += 8) {
-      float v[8][DPT];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int kk = min(i0 + i, kn - 1);
-        const float* po = p.part_o + row_of(k0 + kk) * D + lane * DPT;
-#pragma unroll
-        for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float wi = i0 + i < kn ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk), i0 + i)) : 0.f;
-#pragma unroll
-        for (int x = 0; x < DPT; ++x) num[x] += wi * v[i][x];
-      }
-    }
-  }
-  den = xor16_sum(den);
-  den = xor32_sum(den);
-  den += __shfl_xor(den, 8);
-  den += __shfl_xor(den, 4);
-  den += __shfl_xor(den, 2);
-  den += __shfl_xor(den, 1);
-  const float inv = a.v_scale / den;
-  uint8_t* orow = a.out + (int64_t)e.y * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
-  if constexpr (DPT == 2) *(uint32_t*)orow = pack_bf16(num[0] * inv, num[1] * inv);
-  else *(__bf16*)orow = (__bf16)(num[0] * inv);
+  merge_pieces<D>(a, p, w0, w1 - w0 + 1, hu, hh, e.y, g);
 }
 
 template <bool GATHER>

@@ -68,6 +68,26 @@ struct BatchArgs {
   int64_t d_seq, d_tok, d_head;  // dense strides (bytes)
 };
 
+// LDS of the decode kernel (kDecodeWaves waves of HU heads of head size d,
+// cache element bytes eb): per wave and head a K tile of 32 rows of 2d + 32
+// bytes and a V^T tile of d rows of 64 bytes plus 64 bytes of padding every
+// 2^dpl rows (dpl = log2 of the d values one lane loads per row); at least
+// 81 KB, so that one workgroup fills a CU.  Fused launches build the decode
+// list in the rest of the CU's 160 KB, decode_list_cap entries.
+__host__ __device__ constexpr int decode_dpl_log2(int d, int eb, int hu) {
+  return (hu * d * eb / 16) / eb == 16 ? 4 : ((hu * d * eb / 16) / eb == 8 ? 3 : 2);
+}
+__host__ __device__ constexpr int decode_wave_lds(int d, int eb, int hu) {
+  return hu * (32 * (2 * d + 32) + 16 * (4 * d + 4 * (d >> decode_dpl_log2(d, eb, hu))));
+}
+__host__ __device__ constexpr int decode_tile_lds(int d, int eb, int hu) {
+  return kDecodeWaves * decode_wave_lds(d, eb, hu) > 81 * 1024 ? kDecodeWaves * decode_wave_lds(d, eb, hu)
+                                                                : 81 * 1024;
+}
+__host__ __device__ constexpr int decode_list_cap(int d, int eb, int hu) {
+  return (160 * 1024 - decode_tile_lds(d, eb, hu) - 1024) / 16 - 1;
+}
+
 struct DecodePlan {
   int32_t workers;     // decode waves in the static grid
   int32_t step_keys;   // keys per decode step (KS)
@@ -75,6 +95,10 @@ struct DecodePlan {
   int32_t unit_heads;  // HU: adjacent kv heads one worker computes together
   int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
   int4* dec;           // [J + 1] {sequence, token row, length, prefix P(j) of step counts}
+  // fused = 1 (decode-only batches): each workgroup builds the decode list
+  // in LDS itself, the plan kernel's pass over the sequences, and workgroup
+  // 0 also stores it (and meta) for the merge kernel: no plan launch.
+  int32_t fused;
   float* part_o;       // [workers, 2, HU, G, head_dim] unnormalised piece results
   float* part_ml;      // [workers, 2, HU, G, 2] (max in log2 units, sum)
 };
@@ -127,6 +151,8 @@ struct ValidateArgs {
   const int32_t* seq_lens;
   const int32_t* qsl;
   int32_t num_seqs, num_tokens, num_blocks, block_size;
+  int32_t hint_no_decode;   // 1: no sequence may have query length 1
+  int32_t hint_max_q;       // >= 0: no query length may exceed it
   uint32_t* error_word;
 };
 

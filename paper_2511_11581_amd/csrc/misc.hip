@@ -18,6 +18,7 @@ enum : uint32_t {
   kErrCapacity = 8u,      // seq_len > table width * block_size
   kErrBlock = 16u,        // block id outside [0, num_blocks)
   kErrTokens = 32u,       // query_start_loc[S] > num_tokens
+  kErrHint = 64u,         // the batch hint does not hold
 };
 
 // grid: (S), block 256.
@@ -32,6 +33,7 @@ __global__ __launch_bounds__(256) void validate_kernel(ValidateArgs a) {
     if (L < 0 || q1 - q0 > L) err |= kErrQLen;
     if ((int64_t)L > (int64_t)a.mb * a.block_size) err |= kErrCapacity;
     if (s == a.num_seqs - 1 && q1 > a.num_tokens) err |= kErrTokens;
+    if ((a.hint_no_decode && q1 - q0 == 1) || (a.hint_max_q >= 0 && q1 - q0 > a.hint_max_q)) err |= kErrHint;
   }
   const int64_t nb = min((int64_t)(L > 0 ? L : 0), (int64_t)a.mb * a.block_size);
   const int nblk = (int)((nb + a.block_size - 1) / a.block_size);

@@ -24,48 +24,6 @@ constexpr int kPlanSortCap = 8192;   // larger Q-block lists keep the natural or
 constexpr int kPlanBuckets = 2048;   // key-tile counts are clamped to this
 
 
-// Block-wide exclusive scan of NV values per thread (kPlanThreads threads),
-// all in one pass; tot[] receives the block totals.
-template <int NV>
-__device__ void block_scan(const int (&v)[NV], int (&ex)[NV], int (&tot)[NV]) {
-  __shared__ int wsum[NV][kPlanThreads / 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x[NV];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) x[i] = v[i];
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int y = __shfl_up(x[i], o);
-      if (lane >= o) x[i] += y;
-    }
-  }
-  if (lane == 63)
-#pragma unroll
-    for (int i = 0; i < NV; ++i) wsum[i][w] = x[i];
-  __syncthreads();
-  if (w == 0) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      int t = lane < kPlanThreads / 64 ? wsum[i][lane] : 0;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(t, o);
-        if (lane >= o) t += y;
-      }
-      if (lane < kPlanThreads / 64) wsum[i][lane] = t;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    ex[i] = (w > 0 ? wsum[i][w - 1] : 0) + x[i] - v[i];
-    tot[i] = wsum[i][kPlanThreads / 64 - 1];
-  }
-  __syncthreads();
-}
-
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodePlan dp, PrefillPlan pp,
                                                             int with_prefill) {
   __shared__ int hist[kPlanBuckets];
@@ -94,7 +52,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
       }
     }
     int ex[3], tot[3];
-    block_scan<3>(v, ex, tot);
+    block_scan<3, kPlanThreads>(v, ex, tot);
     if (v[0]) dp.dec[njs + ex[0]] = make_int4(i, t0, L, nsteps + ex[1]);
     if (with_prefill && i < S) {
       pp.seq_start[i] = nqb + ex[2];
@@ -171,7 +129,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     const int b = kPlanBuckets - 1 - (base + tid);
     const int v[1] = {hist[b]};
     int ex[1], tot[1];
-    block_scan<1>(v, ex, tot);
+    block_scan<1, kPlanThreads>(v, ex, tot);
     hist[b] = hcarry + ex[0];  // bucket b is read and written by this thread only
     hcarry += tot[0];
   }

@@ -42,7 +42,7 @@ KERNEL_NAMES = ("decode", "merge", "prefill", "plan")
 PA_MAX_DIMS = 4
 
 # Every function declared in include/pa.h.
-EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_noalloc",
+EXPORTS = ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_hinted", "pa_forward_noalloc",
            "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
            "pa_decode_pieces", "pa_profile_read", "pa_destroy", "pa_last_error")
 
@@ -77,6 +77,10 @@ class pa_plan_info(ctypes.Structure):
             v = getattr(self, name)
             d[name] = list(v) if hasattr(v, "__len__") else int(v)
         return d
+
+
+class pa_batch_hint(ctypes.Structure):
+    _fields_ = [("num_decode_seqs", ctypes.c_int32), ("max_query_len", ctypes.c_int32)]
 
 
 class pa_decode_piece(ctypes.Structure):
@@ -114,6 +118,8 @@ def load_library(path: str = LIB_PATH):
     lib.pa_create.argtypes = [C, ctypes.POINTER(P)]
     lib.pa_forward.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_forward_noalloc.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
+    lib.pa_forward_hinted.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T,
+                                      ctypes.POINTER(pa_batch_hint), P]
     lib.pa_forward_baseline.argtypes = [P, T, T, T, T, T, T, ctypes.c_float, T, P]
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, ctypes.c_int64, T, T, P]
     lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
@@ -129,7 +135,7 @@ def load_library(path: str = LIB_PATH):
     lib.pa_destroy.restype = None
     lib.pa_last_error.argtypes = []
     lib.pa_last_error.restype = ctypes.c_char_p
-    for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_noalloc",
+    for name in ("pa_workspace_bytes", "pa_create", "pa_forward", "pa_forward_hinted", "pa_forward_noalloc",
                  "pa_forward_baseline", "pa_cache_write", "pa_debug_gather", "pa_plan",
                  "pa_decode_pieces", "pa_profile_read"):
         getattr(lib, name).restype = ctypes.c_int
@@ -244,6 +250,17 @@ def pa_forward(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, s
                                      ctypes.byref(ds[6]), _stream(stream)))
 
 
+def pa_forward_hinted(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
+                      num_decode_seqs=-1, max_query_len=-1, stream=None) -> None:
+    """pa_forward with the host's knowledge of the batch (-1: unknown): no
+    decode rows skips the decode + merge launches, max_query_len <= 1 the
+    Q-block launch."""
+    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
+    hint = pa_batch_hint(int(num_decode_seqs), int(max_query_len))
+    _check(load_library().pa_forward_hinted(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
+                                            ctypes.byref(ds[6]), ctypes.byref(hint), _stream(stream)))
+
+
 def pa_forward_noalloc(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
                        stream=None) -> None:
     """pa_forward with the library's static device scratch instead of a
@@ -300,13 +317,20 @@ class PagedAttention:
         return pa_plan(self.handle, None, 0, num_tokens, num_seqs, max_blocks_per_seq)
 
     def forward(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
-                scale: Optional[float] = None, out: Optional[torch.Tensor] = None, stream=None):
+                scale: Optional[float] = None, out: Optional[torch.Tensor] = None, stream=None,
+                hint=None):
+        """hint: optional (num_decode_seqs, max_query_len) known on the host
+        (pa_forward_hinted); None calls pa_forward."""
         if out is None:
             out = torch.empty_like(q)
         if scale is None:
             scale = q.shape[-1] ** -0.5
-        pa_forward(self.handle, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
-                   scale, out, stream)
+        if hint is None:
+            pa_forward(self.handle, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
+                       scale, out, stream)
+        else:
+            pa_forward_hinted(self.handle, q, k_cache, v_cache, block_table, seq_lens,
+                              query_start_loc, scale, out, hint[0], hint[1], stream)
         return out
 
     def forward_baseline(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
