@@ -421,6 +421,9 @@ def main():
                     help="only measure pa_cache_write (mixed batch's 4216 tokens, bf16 and fp8 caches)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--trace", action="store_true",
+                    help="only run the headline batch's timed steps (warm-up + steps, hinted calls): "
+                         "what a profiler attached to this command records")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this path has no multi-GPU mode (asked for {args.gpus}).",
@@ -442,6 +445,15 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": max(1, args.steps)}))
+        return
+
+    if args.trace:
+        from paper_2511_11581_amd import workloads as W
+        w = W.make_config(args.config, device="cuda", poison=False)
+        att = make_attention(w)
+        out = torch.empty_like(w.q)
+        ms = time_steps(w, att, out, args.steps, args.warmup, hint_of(w))
+        print(json.dumps({"trace_config": args.config, "ms_per_step": ms, "steps": args.steps}))
         return
 
     if args.cache_write:
