@@ -222,15 +222,19 @@ def sampled_error(w, out, nrows=256, seed=0):
     return {"rows": len(rows), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean())}
 
 
-def measure(k, steps, warmup, block_size=None, with_error=True):
+def measure(k, steps, warmup, block_size=None, with_error=True, kv_dtype=None):
     import torch
     from paper_2511_11581_amd import workloads as W
-    if block_size is None:
+    if block_size is None and kv_dtype is None:
         w = W.make_config(k, device="cuda", poison=False)
-    else:   # the same batch on pages of another size
+    else:   # the same batch on pages of another size, or in a cache of another dtype
         seqs, kw, gen, seed = W.config_seqs(k)
-        w = W.make_batch(seqs, seed=seed, device="cuda", poison=False, block_size=block_size,
-                         name=f"config{k}-bs{block_size}", _gen=gen, **kw)
+        kw = dict(kw)
+        if kv_dtype is not None:
+            kw["kv_dtype"] = kv_dtype
+        bs = block_size if block_size is not None else 16
+        w = W.make_batch(seqs, seed=seed, device="cuda", poison=False, block_size=bs,
+                         name=f"config{k}-bs{bs}-{kw.get('kv_dtype', 'bf16')}", _gen=gen, **kw)
     att = make_attention(w)
     out = torch.empty_like(w.q)
     hint = hint_of(w)
@@ -424,6 +428,8 @@ def main():
     ap.add_argument("--trace", action="store_true",
                     help="only run the headline batch's timed steps (warm-up + steps, hinted calls): "
                          "what a profiler attached to this command records")
+    ap.add_argument("--kv", choices=("bf16", "fp8"), default=None,
+                    help="with --trace: the batch with caches of this dtype")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this path has no multi-GPU mode (asked for {args.gpus}).",
@@ -449,11 +455,17 @@ def main():
 
     if args.trace:
         from paper_2511_11581_amd import workloads as W
-        w = W.make_config(args.config, device="cuda", poison=False)
+        if args.kv is None:
+            w = W.make_config(args.config, device="cuda", poison=False)
+        else:
+            seqs, kw, gen, seed = W.config_seqs(args.config)
+            kw = dict(kw, kv_dtype=args.kv)
+            w = W.make_batch(seqs, seed=seed, device="cuda", poison=False, name=f"config{args.config}-{args.kv}",
+                             _gen=gen, **kw)
         att = make_attention(w)
         out = torch.empty_like(w.q)
         ms = time_steps(w, att, out, args.steps, args.warmup, hint_of(w))
-        print(json.dumps({"trace_config": args.config, "ms_per_step": ms, "steps": args.steps}))
+        print(json.dumps({"trace_config": args.config, "kv": args.kv, "ms_per_step": ms, "steps": args.steps}))
         return
 
     if args.cache_write:
@@ -495,6 +507,24 @@ def main():
             print(f"# config {k} at block size {bs}: {r['us_per_batch']:.1f} us/batch, "
                   f"{r['GBps']:.0f} GB/s, {r['TFLOPs']:.1f} TFLOP/s, kernels {r['per_kernel_us']}",
                   file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
+
+    # the prefill and mixed batches with fp8 e4m3 caches
+    kv_fp8 = {}
+    if not args.only:
+        for k in (3, 4):
+            _, r = measure(k, args.steps, args.warmup, kv_dtype="fp8")
+            kv_fp8[f"config{k}_fp8"] = {kk: r[kk] for kk in (
+                "us_per_batch", "us_median", "GBps", "frac_hbm", "TFLOPs", "frac_mfma",
+                "per_kernel_us", "error_vs_oracle") if kk in r}
+            for kk in ("prefill_kernel_TFLOPs", "decode_kernel_GBps"):
+                if kk in r:
+                    kv_fp8[f"config{k}_fp8"][kk] = r[kk]
+            e = r.get("error_vs_oracle") or {}
+            print(f"# config {k} with fp8 caches: {r['us_per_batch']:.1f} us/batch, "
+                  f"{r['GBps']:.0f} GB/s, {r['TFLOPs']:.1f} TFLOP/s, kernels {r['per_kernel_us']}, "
+                  f"error vs oracle max {e.get('max_abs_err', float('nan')):.2e} "
+                  f"mean {e.get('mean_abs_err', float('nan')):.2e}", file=sys.stderr, flush=True)
             torch.cuda.empty_cache()
 
     cache_write = {}
@@ -551,6 +581,7 @@ def main():
         "roofline": roof, "cpu_baseline": cpu,
         "configs": {str(k): {kk: v for kk, v in r.items() if kk != "name"} for k, r in configs.items()},
         "block_sizes": block_sizes,
+        "kv_fp8": kv_fp8,
         "cache_write": cache_write,
         "ladder": ladder,
     }

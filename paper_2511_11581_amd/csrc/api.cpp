@@ -11,8 +11,9 @@
 //      split the key tiles of all single-token rows evenly (Sec. 4.5);
 //   3. the log-sum-exp merge of pairs that span several workers;
 //   4. the Q-block kernel for rows with two or more query tokens (Sec. 4.4),
-//      BLOCK_M = 256 or 128 rows (bf16 caches, chosen from the batch shape)
-//      or 128 (fp8 caches), i.e. BLOCK_Q = BLOCK_M / G tokens.
+//      BLOCK_M = 256 or 128 rows (bf16 caches, chosen from the batch shape),
+//      256 (fp8 caches, d = 128) or 128 (fp8, d = 64), i.e. BLOCK_Q =
+//      BLOCK_M / G tokens.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -144,7 +145,9 @@ int decode_step_keys(const pa_config& c) {
 
 int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 
-// Rows per Q-block.  fp8 caches: 128 (one kernel shape).  bf16 caches: 256
+// Rows per Q-block.  fp8 caches: 256 for d = 128 (the bf16 kernel's 8-wave
+// shape, widening its copies to bf16 in LDS), 128 for d = 64 (a
+// register-staged kernel).  bf16 caches: 256
 // (8 waves, one workgroup per CU) or 128 (4 waves, two workgroups per CU),
 // chosen from host-visible sizes by a decision tree fitted offline to the
 // faster of the two on 47 prefill-heavy shapes (1-64 sequences, 16-4096 new
@@ -155,7 +158,7 @@ int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 // PA_QBLOCK_ROWS (128 or 256, read when a handle is created) forces one.
 constexpr int kBlockMMin = 128;
 int block_m(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S, int64_t MB) {
-  if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return 128;
+  if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return c.head_dim == 128 ? 256 : 128;
   if (tun.qblock_rows) return tun.qblock_rows;
   if (T < 2 || S < 1) return 256;
   const int G = c.num_q_heads / c.num_kv_heads;

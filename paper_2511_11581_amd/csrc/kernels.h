@@ -166,8 +166,8 @@ hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPl
                        bool with_prefill, hipStream_t st);
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st, bool gather = false);
-hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st,
-                         bool gather = false);
+hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
+                         hipStream_t st, bool gather = false);
 
 // KV-cache write (csrc/cache.hip).
 struct CacheWriteArgs {

@@ -371,7 +371,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(BatchArgs a, Prefi
 
 hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                           hipStream_t st, bool gather) {
-  if (!fp8) return launch_qblock(a, p, head_dim, st, gather);
+  if (!fp8 || head_dim == 128) return launch_qblock(a, p, head_dim, fp8, st, gather);
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   dim3 grid((unsigned)blocks), block(kThreads);

@@ -13,10 +13,10 @@
 // the scores of tile t + 1, then O += V^T P^T of tile t with the softmax of
 // tile t + 1 (one exp, one pack and one dot2 per weight) placed between its
 // products, so that the VALU work runs under the wave's own products; the
-// second wave on the SIMD does the same.  The score products start from
-// -m / c (c = scale * log2(e)), so one multiply by c precedes each exp; Q
-// enters the products unchanged (rounding Q * c to bf16 would add a relative
-// error of 2^-9 to every score, which grows with the logit).
+// second wave on the SIMD does the same.  Each weight takes one fma (c S -
+// m, c = scale * log2(e)) before its exp; Q enters the products unchanged
+// (rounding Q * c to bf16 would add a relative error of 2^-9 to every
+// score, which grows with the logit).
 //
 // K/V tiles of 64 keys move from HBM into a ring of 4 LDS stages with
 // global_load_lds_dwordx4 (no staging registers, no VALU), three tiles
@@ -103,6 +103,17 @@ __device__ __forceinline__ void wait_vm_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
 }
+// Vector-memory count bounded by N, LDS operations left in flight; a
+// compiler memory barrier too, so that no LDS access moves across it.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+// Every LDS operation drained, vector-memory operations left in flight.
+__device__ __forceinline__ void wait_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");
+}
 
 // GATHER: only the last Q-block of each sequence runs; it walks the block
 // table and copies every tile into the ring with the same loads, then
@@ -115,9 +126,21 @@ __device__ __forceinline__ void wait_vm_lds() {
 // 4: two workgroups per CU (80 KB each: a K ring of 3 stages and a V ring of
 // 2; period t loads V of tile t + 1 and K of tile t + 3), so that one
 // workgroup's barrier waits and start-up run under the other's products.
-template <int D, int W, bool GATHER>
+//
+// FP8 (e4m3 caches; W = 8, d = 128): the copies land in a staging area
+// private to each wave (3 stages of its 8 K rows and 8 V rows, 2 KB a
+// stage), and the wave itself widens its rows to bf16 into the K and V
+// rings (3 stages each), exactly: every e4m3 value is a bf16 value, and the
+// per-tensor scales act on the scores (k_scale, folded into c) and on the
+// output (v_scale).  Period t widens tile t + 2, which landed during
+// periods t - 2 and t - 1, and copies tile t + 4 into the staging stage
+// that tile t + 1 left; V rows at or past the end are widened to zeros.
+// Since a wave widens only what it copied, its own vmcnt wait orders the
+// two; the barrier of the next period publishes the bf16 rows.  The
+// products are those of the bf16 kernel.
+template <int D, int W, bool FP8, bool GATHER>
 __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, PrefillPlan pp) {
-  constexpr int RB = 2 * D;                        // bytes per cached row
+  constexpr int RB = 2 * D;                        // bytes per row in the rings (bf16)
   constexpr int CPR = D / 8;                       // 16-byte chunks per row
   constexpr int TB = kTile * RB;                   // bytes per K (or V) tile
   constexpr int RPI = 1024 / RB;                   // rows per load instruction
@@ -125,15 +148,25 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   constexpr int KRW = 256 / RB;                    // K rows per 256-byte bank window
   constexpr int NT = D / 16;                       // k-steps of K Q^T
   constexpr int NDB = D / 32;                      // 32-row d blocks of O^T
-  constexpr int KSTG = W == 8 ? 4 : 3;             // K ring stages
-  constexpr int VSTG = W == 8 ? 4 : 2;             // V ring stages
+  constexpr int KSTG = FP8 ? 3 : W == 8 ? 4 : 3;   // K ring stages
+  constexpr int VSTG = FP8 ? 3 : W == 8 ? 4 : 2;   // V ring stages
   constexpr bool kSplit = W != 8;                  // K and V of one period from different tiles
-  constexpr int VBASE = KSTG * TB;                 // V ring after the K ring
+  // fp8 staging: per wave and stage, its K rows then its V rows (kTile / W
+  // rows of D bytes each, one 16-byte copy per lane and tensor)
+  constexpr int SROW = kTile / W;                  // rows per wave and tile
+  constexpr int SCH = D / 16;                      // 16-byte chunks per fp8 row
+  constexpr int SSTG = 3;                          // staging stages
+  constexpr int SWB = 2 * 1024;                    // staging bytes per wave and stage
+  constexpr int SBYTES = FP8 ? SSTG * W * SWB : 0;
+  constexpr int SBASE = KSTG * TB;                 // staging after the K ring
+  constexpr int VBASE = KSTG * TB + SBYTES;        // V ring after the K ring (and the staging)
   static_assert(kQblockWaveRows == 32 && (W == 8 || W == 4), "8 or 4 waves x 32 rows");
   static_assert(NLD >= 1 && NLD * RPI * W == kTile, "tile loads");
   static_assert(RPI <= 16, "one instruction stays inside one 16-key block");
-  static_assert((KSTG + VSTG) * TB * (8 / W) <= 160 * 1024, "workgroups per CU fit the LDS");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[(KSTG + VSTG) * TB];
+  static_assert(!FP8 || (W == 8 && D == 128 && SROW * SCH == 64), "fp8: 8 waves, d = 128");
+  static_assert(((KSTG + VSTG) * TB + SBYTES) * (8 / W) <= 160 * 1024, "workgroups per CU fit the LDS");
+  static_assert(kQblockWaveRows * W * RB <= KSTG * TB + SBYTES, "output staging below the V ring");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[(KSTG + VSTG) * TB + SBYTES];
   auto kst = [](int t) { return t % KSTG; };   // ring stage of tile t's K
   auto vst = [](int t) { return t % VSTG; };   // ring stage of tile t's V
 
@@ -142,7 +175,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   const int Hkv = a.num_kv_heads;
   const int G = a.group;
   const BlockDiv bd = a.bdiv;   // block size: a multiple of 16
-  const float c = a.sl2, inv_c = 1.f / a.sl2;   // scale * log2(e) (* k_scale)
+  const float c = a.sl2;   // scale * log2(e) (* k_scale)
   // One workgroup per (Q-block, kv head) unit, kv head fastest: with
   // round-robin dispatch over the 8 XCDs, the units of one kv head (Hkv =
   // 8) share an XCD and its L2, which serves the K/V re-reads of a
@@ -196,11 +229,17 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   auto fK = [](int r) { return (r / KRW) & (CPR - 1); };
   auto fV = [](int r) { return (CPR / 4) * (r & 3) + (CPR / 8) * ((r >> 2) & 1); };
   int koff[NLD], voff[NLD];
+  if constexpr (FP8) {
+    // lane i copies chunk i % SCH of row wrow + i / SCH (16 fp8 values)
+    koff[0] = (lane / SCH) * (int)a.kg.slot + 16 * (lane % SCH);
+    voff[0] = (lane / SCH) * (int)a.vg.slot + 16 * (lane % SCH);
+  } else {
 #pragma unroll
-  for (int k = 0; k < NLD; ++k) {
-    const int rr = RPI * k + lane / CPR, r = wrow + rr, s = lane % CPR;
-    koff[k] = rr * (int)a.kg.slot + 16 * (s ^ fK(r));
-    voff[k] = rr * (int)a.vg.slot + 16 * (s ^ fV(r));
+    for (int k = 0; k < NLD; ++k) {
+      const int rr = RPI * k + lane / CPR, r = wrow + rr, s = lane % CPR;
+      koff[k] = rr * (int)a.kg.slot + 16 * (s ^ fK(r));
+      voff[k] = rr * (int)a.vg.slot + 16 * (s ^ fV(r));
+    }
   }
   const uint8_t* kbase = a.k + (int64_t)g * a.kg.head;
   const uint8_t* vbase = a.v + (int64_t)g * a.vg.head;
@@ -262,6 +301,47 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
       issue_vpart(t, k);
     }
   };
+  // fp8: the wave's staging stage of tile t (K rows, then V rows at + 1 KB)
+  auto stg = [&](int t) { return SBASE + ((t % SSTG) * W + wave) * SWB; };
+  auto issue8_k = [&](int t) { dma16(kp + koff[0], lds_addr(lds + stg(t))); };
+  auto issue8_v = [&](int t) { dma16(vp + voff[0], lds_addr(lds + stg(t) + 1024)); };
+  auto issue8 = [&](int t) {
+    issue_prep(t);
+    issue8_k(t);
+    issue8_v(t);
+  };
+  // fp8: widen the wave's staged rows of tile t to bf16 in the K and V
+  // rings, at the places the bf16 copies would have put them (its copies
+  // of tile t have landed).  Lane i: row r8 = wrow + i / SCH, fp8 chunk
+  // c8 = i % SCH, i.e. bf16 chunks 2 c8 and 2 c8 + 1, whose swizzled
+  // slots differ in bit 0 (both swizzles keep it or flip it for the pair).
+  // read8 fetches the 16 codes, put8_k / put8_v write the bf16 values.
+  const int r8 = wrow + lane / SCH;
+  const int w8k = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fK(r8));
+  const int w8v = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fV(r8));
+  auto read8 = [&](int t, int tensor) -> u32x4 {
+    return *(const u32x4*)(lds + stg(t) + 1024 * tensor + 16 * lane);
+  };
+  auto put8_k = [&](int t, const u32x4& raw) {
+    bf16x8 lo, hi;
+    fp8x16_to_bf16(raw, lo, hi);
+    uint8_t* base = lds + kst(t) * TB;
+    *(bf16x8*)(base + w8k) = lo;
+    *(bf16x8*)(base + (w8k ^ 16)) = hi;
+  };
+  auto put8_v = [&](int t, const u32x4& raw) {
+    bf16x8 lo, hi;
+    fp8x16_to_bf16(raw, lo, hi);
+    if (t * kTile + r8 >= kv_len) {   // past the end: zeros (the bytes may be NaN codes)
+      lo = bf16x8{};
+      hi = bf16x8{};
+    }
+    uint8_t* base = lds + VBASE + vst(t) * TB;
+    *(bf16x8*)(base + w8v) = lo;
+    *(bf16x8*)(base + (w8v ^ 16)) = hi;
+  };
+  auto widen8_k = [&](int t) { put8_k(t, read8(t, 0)); };
+  auto widen8_v = [&](int t) { put8_v(t, read8(t, 1)); };
   // V rows at or past kv_len (last tile only) may hold anything, NaN
   // included, and would poison P V even with zero weights: each lane zeroes
   // the chunks it loaded, after its own loads have landed.
@@ -291,8 +371,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   }
 
   f32x16 o[NDB];     // O^T accumulators
-  f32x16 s[2];       // S^T of one tile (two 32-key halves), relative to m_run
-  f32x16 nm;         // -m_run / c in every element: the score products start from it
+  f32x16 s[2];       // S^T of one tile (two 32-key halves)
   bf16x8 pb[4];      // P^T operands (four 16-key steps)
   float m_run = 0.f, l_run = 0.f;
   float psum = 0.f;                   // row sum of the tile in progress
@@ -303,9 +382,9 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
 
-  // ---- softmax pieces.  A score product started from nm = -m_run / c
-  //      leaves s = S - m_run / c (S = q . k, c = scale * log2(e)), and the
-  //      weight is 2^(c s) = 2^(c S - m_run).  Element e is s[e / 16][e % 16],
+  // ---- softmax pieces.  s = S = q . k; with c = scale * log2(e) the
+  //      weight is 2^(c S - m_run), one fma and one exp (the fma rounds
+  //      once, after the exact product).  Element e is s[e / 16][e % 16],
   //      key 8(e % 16 / 4) + 4 hf + e % 4 + 32 (e / 16) of the tile.  Causal
   //      mask of tile t (tiles crossing a diagonal only):
   auto mask = [&](int t) {
@@ -316,17 +395,17 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
       for (int i = 0; i < 16; ++i)
         s[kb][i] = (32 * kb + 8 * (i >> 2) + (i & 3)) <= lim ? s[kb][i] : kNegInf;
   };
-  // Weights of elements 8u .. 8u + 7, 2^(c s - d), to the bf16 operand pb[u];
-  // the row sum adds the rounded weights (the ones the products use) with
-  // dot2.  (Used where the reference moves; the products' schedule splits
-  // the d = 0 case into exp_pair and pack_group below.)
-  auto group = [&](int u, float d) {
+  // Weights of elements 8u .. 8u + 7, 2^(c s - m), to the bf16 operand
+  // pb[u]; the row sum adds the rounded weights (the ones the products use)
+  // with dot2.  (Used for the first tile and where the reference moves; the
+  // products' schedule splits the work into exp_pair and pack_group below.)
+  auto group = [&](int u, float m) {
     const int kb = u >> 1, i0 = 8 * (u & 1);
     u32x4 pw;
 #pragma unroll
     for (int h = 0; h < 4; ++h)
-      pw[h] = pack_bf16(fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h], c, -d)),
-                        fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h + 1], c, -d)));
+      pw[h] = pack_bf16(fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h], c, -m)),
+                        fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h + 1], c, -m)));
     pb[u] = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
     for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
@@ -337,8 +416,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   float ex[8];
   auto exp_pair = [&](int u, int h) {
     const int kb = u >> 1, i0 = 8 * (u & 1);
-    ex[2 * h] = fast_exp2(s[kb][i0 + 2 * h] * c);
-    ex[2 * h + 1] = fast_exp2(s[kb][i0 + 2 * h + 1] * c);
+    ex[2 * h] = fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h], c, -m_run));
+    ex[2 * h + 1] = fast_exp2(__builtin_fmaf(s[kb][i0 + 2 * h + 1], c, -m_run));
   };
   auto pack_group = [&](int u) {
     u32x4 pw;
@@ -348,7 +427,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
 #pragma unroll
     for (int h = 0; h < 4; ++h) psum = dot2_bf16(pw[h], kOnesBf16x2, psum);
   };
-  // Row max of the tile in log2 units relative to m_run, across the lane pair.
+  // Row max of the tile in log2 units (c S), across the lane pair.
   auto tile_max = [&]() {
     float mA = kNegInf, mB = kNegInf;
 #pragma unroll
@@ -365,16 +444,14 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   // and never above it.
   auto finish = [&]() {
     if (__ballot(psum > 4096.f)) {
-      const float d = fmaxf(tile_max(), 0.f);
+      const float d = fmaxf(tile_max() - m_run, 0.f);
       m_run += d;
       alpha = fast_exp2(-d);
       resc = 1;
       l_run *= alpha;
       psum = 0.f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) group(u, d);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) nm[i] = -m_run * inv_c;
+      for (int u = 0; u < 4; ++u) group(u, m_run);
     }
     l_run += psum;
     psum = 0.f;
@@ -400,6 +477,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   // LDS operands are read kAhead products ahead into a small register ring;
   // a scheduling fence after every product keeps each step's work in place.
   constexpr int kAhead = 4;
+  static_assert(!FP8 || 14 < NS, "fp8: widening and copies between the score products");
   static_assert(kSplit ? 3 + 4 * NLD <= NS + NP : 2 + 3 * ND <= NS + 1,
                 "tile loads fit between the products");
   auto period = [&](int t, auto full_tag) {
@@ -418,19 +496,39 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     };
     constexpr int I0 = kFullP ? 0 : NS;
     bf16x8 ring[kAhead];
+    u32x4 raw8;   // fp8: staged codes between their read and their widening
 #pragma unroll
     for (int i = 0; i < kAhead; ++i) ring[i] = rd(I0 + i);
 #pragma unroll
     for (int i = I0; i < NS + NP; ++i) {
       const bf16x8 op = ring[(i - I0) % kAhead];
       if (i < NS) {
-        s[i & 1] = mfma32(op, qt[i >> 1], (i >> 1) == 0 ? nm : s[i & 1]);
+        s[i & 1] = mfma32(op, qt[i >> 1], (i >> 1) == 0 ? f32x16{} : s[i & 1]);
       } else {
         const int p = i - NS;
         o[p % NDB] = mfma32(op, pb[p / NDB], o[p % NDB]);
       }
       if (i + kAhead < NS + NP) ring[(i - I0) % kAhead] = rd(i + kAhead);
-      if constexpr (kFullP && !kSplit) {
+      if constexpr (kFullP && FP8) {
+        // widen tile t + 2 (copied two periods ago; tile t + 3's copies may
+        // still fly), then copy tile t + 4 into the staging stage of t + 1
+        if (t + 2 < ntiles) {
+          if (i == 0) {
+            if (t + 3 < ntiles) wait_vm<2>();
+            else wait_vm<0>();
+            raw8 = read8(t + 2, 0);
+          }
+          if (i == 3) put8_k(t + 2, raw8);
+          if (i == 6) raw8 = read8(t + 2, 1);
+          if (i == 9) put8_v(t + 2, raw8);
+        }
+        if (t + 4 < ntiles) {
+          if (i == 11) issue_prep(t + 4);
+          if (i == 12) issue8_k(t + 4);
+          if (i == 14) issue8_v(t + 4);
+        }
+      }
+      if constexpr (kFullP && !kSplit && !FP8) {
         // K and V of tile t + 3 between the score products, alternating
         if (t + 3 < ntiles) {
           if (i == 1) issue_prep(t + 3);
@@ -468,6 +566,22 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   if constexpr (GATHER) {
     if (ctx + tok_hi != min(a.seq_lens[seq], a.mb * a.block_size)) return;   // not the last Q-block
     const int64_t kd0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
+    if constexpr (FP8) {
+      // each wave stores the raw codes of its staged rows
+      const int r = wrow + lane / SCH, c8 = lane % SCH;
+      for (int t = 0; t < ntiles; ++t) {
+        issue8(t);
+        wait_vm<0>();
+        const u32x4 kw = *(const u32x4*)(lds + stg(t) + 16 * lane);
+        const u32x4 vw = *(const u32x4*)(lds + stg(t) + 1024 + 16 * lane);
+        const int key = t * kTile + r;
+        if (key < kv_len) {
+          *(u32x4*)(a.kd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = kw;
+          *(u32x4*)(a.vd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = vw;
+        }
+      }
+      return;
+    }
     for (int t = 0; t < ntiles; ++t) {
       issue(t);
       wait_vm_lds<0>();
@@ -500,7 +614,26 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   // ---- prologue: tiles 0, 1, 2 in flight (split rings: K of tiles 0, 1,
   //      V of tile 0, K of tile 2, in that order); scores and weights of
   //      tile 0, whose row max becomes the first reference
-  if constexpr (!kSplit) {
+  if constexpr (FP8) {
+    // tiles 0 .. 2 copied; 0 and 1 widened (2 may still fly), then tile 3
+    // copied over tile 0's staging once its reads are done
+    issue8(0);
+    if (ntiles > 1) issue8(1);
+    if (ntiles > 2) issue8(2);
+    if (ntiles > 2) wait_vm<4>();
+    else if (ntiles == 2) wait_vm<2>();
+    else wait_vm<0>();
+    widen8_k(0);
+    widen8_v(0);
+    if (ntiles > 1) {
+      if (ntiles > 2) wait_vm<2>();
+      else wait_vm<0>();
+      widen8_k(1);
+      widen8_v(1);
+    }
+    wait_lds();
+    if (ntiles > 3) issue8(3);
+  } else if constexpr (!kSplit) {
     issue(0);
     if (ntiles > 1) issue(1);
     if (ntiles > 2) issue(2);
@@ -521,9 +654,13 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
       else wait_vm_lds<0>();
     }
   };
-  wait_first();
-  if (ntiles == 1) zero_tail(0);
-  wait_first();
+  if constexpr (FP8) {
+    wait_lds();
+  } else {
+    wait_first();
+    if (ntiles == 1) zero_tail(0);
+    wait_first();
+  }
   __builtin_amdgcn_s_barrier();
   {
     const uint8_t* ks = lds;
@@ -539,8 +676,6 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   for (int u = 0; u < 4; ++u) group(u, m_run);
   l_run = psum;
   psum = 0.f;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) nm[i] = -m_run * inv_c;
 
   // ---- tile periods.  sync(t): K of tile t + 1 and V of tile t have
   //      landed for every wave and every wave has finished period t - 1, so
@@ -548,7 +683,9 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   //      this period's loads.  The O rescale owed by the softmax of tile t is
   //      applied before the products of tile t.
   auto sync = [&](int t) {
-    if constexpr (!kSplit) {
+    if constexpr (FP8) {
+      wait_lds();   // the rows this wave widened are written
+    } else if constexpr (!kSplit) {
       // this wave's loads of tile t + 1 have landed (those of t + 2, if it
       // exists, may still fly)
       auto wait_next = [&]() {
@@ -572,7 +709,15 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     __builtin_amdgcn_s_barrier();
   };
   auto load_next = [&](int t) {   // period t's loads, outside the products
-    if constexpr (!kSplit) {
+    if constexpr (FP8) {
+      if (t + 2 < ntiles) {
+        if (t + 3 < ntiles) wait_vm<2>();
+        else wait_vm<0>();
+        widen8_k(t + 2);
+        widen8_v(t + 2);
+      }
+      if (t + 4 < ntiles) issue8(t + 4);
+    } else if constexpr (!kSplit) {
       if (t + 3 < ntiles) issue(t + 3);
     } else {
       if (t + 1 < ntiles) issue_v(t + 1);
@@ -636,13 +781,19 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
 
 }  // namespace
 
-hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, hipStream_t st,
-                         bool gather) {
+hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
+                         hipStream_t st, bool gather) {
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   const int W = p.block_m / kQblockWaveRows;
   const dim3 grid((unsigned)blocks), block(64 * W);
-#define PA_QB(DD, WW, GG) qblock_kernel<DD, WW, GG><<<grid, block, 0, st>>>(a, p)
+  if (fp8) {
+    if (W != 8 || head_dim != 128) return hipErrorInvalidValue;
+    if (gather) qblock_kernel<128, 8, true, true><<<grid, block, 0, st>>>(a, p);
+    else qblock_kernel<128, 8, true, false><<<grid, block, 0, st>>>(a, p);
+    return hipGetLastError();
+  }
+#define PA_QB(DD, WW, GG) qblock_kernel<DD, WW, false, GG><<<grid, block, 0, st>>>(a, p)
   if (W == 8) {
     if (head_dim == 128) gather ? PA_QB(128, 8, true) : PA_QB(128, 8, false);
     else if (head_dim == 64) gather ? PA_QB(64, 8, true) : PA_QB(64, 8, false);

@@ -11,11 +11,13 @@ batches force them, in two ways:
     the tiles before it.
 Each case first shows, from the oracle's per-key scores (log2 units), that
 its inputs cross the threshold of the kernel that computes them:
-  * bf16 Q-block kernel: the reference is the first 64-key tile's row max and
-    moves when a weight exceeds 2^12, so some later tile's max must exceed the
-    first tile's max by more than 12;
-  * fp8 Q-block kernel and decode kernel: the running max moves when a tile
-    (or decode step) max exceeds it by more than 8;
+  * MFMA Q-block kernel (bf16 caches, and fp8 caches with d = 128): the
+    reference is the first 64-key tile's row max and moves when a weight
+    exceeds 2^12, so some later tile's max must exceed the first tile's max
+    by more than 12;
+  * register-staged fp8 Q-block kernel (d = 64) and decode kernel: the
+    running max moves when a tile (or decode step) max exceeds it by more
+    than 8;
   * merge: the pieces of one split row must have maxima more than 20 apart.
 Then every row is compared with the oracle at the usual tolerances.
 """
@@ -113,8 +115,9 @@ def test_prefill_rescale(name):
     seqs, Hq, Hkv, d, kv, bs, qs, spikes, toks = PREFILL[name]
     w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=seed_of(name), name=name,
                      q_scale=qs, spikes=spikes)
-    jump = _prefill_jump(w, _rows_of_tokens(w, toks), first_tile_reference=(kv == "bf16"))
-    need = 12.0 if kv == "bf16" else 8.0
+    mfma_kernel = kv == "bf16" or d == 128
+    jump = _prefill_jump(w, _rows_of_tokens(w, toks), first_tile_reference=mfma_kernel)
+    need = 12.0 if mfma_kernel else 8.0
     assert jump > need, f"{name}: inputs rise only {jump:.1f} log2 units (need > {need})"
     _full(w, attention_for(w))
 
