@@ -139,7 +139,11 @@ typedef struct pa_profile {
  * segments of 8 steps (the example of Fig. 4).  The default minimum share is
  * 1 step (environment PA_DECODE_MIN_STEPS, read when a handle is created):
  * for batches too small to fill the grid, the serial steps of one worker
- * cost more than the merge of more segments. */
+ * cost more than the merge of more segments.  Where no sequence can be
+ * longer than PA_DECODE_WHOLE_STEPS steps (default 8; from the table width,
+ * max_blocks_per_seq x block_size keys), the shares are whole pairs
+ * instead (decode_whole_units): every segment covers its pair and the
+ * merge launch is skipped. */
 typedef struct pa_plan_info {
   int32_t decode_launch;     /* 1 if the decode kernels are launched */
   int32_t decode_step;       /* keys per decode step (32, 64 or 128) */
@@ -147,6 +151,9 @@ typedef struct pa_plan_info {
   int32_t decode_workers;    /* waves in the static decode grid */
   int32_t decode_min_steps;  /* fewest steps per active worker group, batch permitting */
   int32_t decode_unit_heads; /* kv heads per decode unit (HU, see above) */
+  int32_t decode_whole_units; /* 1: no sequence can exceed PA_DECODE_WHOLE_STEPS decode steps
+                                 (default 8; max_blocks_per_seq x block_size keys), so each
+                                 worker takes whole (sequence, unit) pairs and no merge runs */
   int32_t merge_launch;      /* 1 if the log-sum-exp merge kernel is launched */
   int32_t prefill_launch;    /* 1 if the Q-block (q_len >= 2) kernel is launched */
   int32_t block_m;           /* rows per Q-block (BLOCK_M, Sec. 4.4) */

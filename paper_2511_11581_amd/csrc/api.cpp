@@ -39,6 +39,7 @@ struct pa_event_ring {
 // is created.
 struct pa_tunables {
   int decode_min_steps;
+  int decode_whole_steps;
   int qblock_rows;   // 0: chosen from the batch shape; else 128 or 256 (bf16 caches)
 };
 
@@ -85,6 +86,10 @@ constexpr int kMaxCus = 256;
 // sweep over 15 decode shapes (1..128 sequences, 1K..32K keys; Sec. 5's
 // tuning exported as a rule): 1 was best or within noise in all but one.
 constexpr int kMinStepsDefault = 1;
+// Whole (sequence, unit) pairs per decode worker, with no merge launch, when
+// no sequence can exceed this many steps (table width x block size): below
+// it the merge launch costs more than splitting the keys saves.
+constexpr int kWholeStepsDefault = 8;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
 constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel
@@ -218,10 +223,14 @@ WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
 }
 
 pa_tunables tunables_from_env() {
-  pa_tunables t{kMinStepsDefault, 0};
+  pa_tunables t{kMinStepsDefault, kWholeStepsDefault, 0};
   if (const char* e = std::getenv("PA_DECODE_MIN_STEPS")) {
     const int v = std::atoi(e);
     if (v >= 1) t.decode_min_steps = std::min(v, 4096);
+  }
+  if (const char* e = std::getenv("PA_DECODE_WHOLE_STEPS")) {
+    const int v = std::atoi(e);
+    if (v >= 0) t.decode_whole_steps = std::min(v, 4096);
   }
   if (const char* e = std::getenv("PA_QBLOCK_ROWS")) {
     const int v = std::atoi(e);
@@ -249,10 +258,13 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
     p->decode_grid[0] = p->decode_workers / p->decode_waves;
     p->decode_grid[1] = 1;
     p->decode_grid[2] = 1;
-    p->merge_launch = 1;
-    p->merge_grid[0] = S;
-    p->merge_grid[1] = (G + 3) / 4;
-    p->merge_grid[2] = c.num_kv_heads;
+    p->decode_whole_units = cdiv(max_len, p->decode_step) <= tun.decode_whole_steps ? 1 : 0;
+    if (!p->decode_whole_units) {
+      p->merge_launch = 1;
+      p->merge_grid[0] = S;
+      p->merge_grid[1] = (G + 3) / 4;
+      p->merge_grid[2] = c.num_kv_heads;
+    }
     const int qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
     if (T >= qmin && max_len >= qmin) {
       p->prefill_launch = 1;
@@ -366,6 +378,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   dp->workers = p.decode_workers;
   dp->step_keys = p.decode_step;
   dp->min_steps = p.decode_min_steps;
+  dp->whole_units = p.decode_whole_units;
   dp->unit_heads = p.decode_unit_heads;
   dp->meta = reinterpret_cast<int32_t*>(ws + wl.meta);
   dp->fused = 0;
@@ -514,10 +527,38 @@ pa_status pa_decode_pieces(const pa_handle* h, const pa_config* cfg, int32_t num
     }
   }
   const int64_t total = (int64_t)Hu * P;
+  int64_t n = 0;
+  auto put = [&](int64_t jj, int64_t gu, int w, int64_t k0, int64_t k1, int slot) {
+    for (int hu = 0; hu < HU; ++hu, ++n) {
+      if (n >= cap) continue;
+      pa_decode_piece& pc = pieces[n];
+      pc.seq = dec[jj].s;
+      pc.kv_head = (int32_t)(gu * HU + hu);
+      pc.worker = w;
+      pc.first_key = (int32_t)(k0 * KS);
+      pc.end_key = (int32_t)std::min<int64_t>(k1 * KS, dec[jj].L);
+      pc.slot = slot;
+    }
+  };
+  if (cdiv(cap_keys, KS) <= tun.decode_whole_steps) {
+    // Whole pairs per workgroup, their steps split over its waves (the
+    // pieces merged inside the workgroup).
+    const int64_t U = (int64_t)Hu * (int64_t)dec.size();
+    const int64_t B = std::min<int64_t>(U, decode_workers(cus) / pa::kDecodeWaves);
+    for (int64_t b = 0; b < B; ++b)
+      for (int64_t u = U * b / B; u < U * (b + 1) / B; ++u) {
+        const int64_t jj = u / Hu, gu = u % Hu, nt = cdiv(dec[jj].L, KS);
+        const int64_t np = std::min<int64_t>(pa::kDecodeWaves, nt);
+        for (int64_t i = 0; i < np; ++i)
+          put(jj, gu, (int)(b * pa::kDecodeWaves + i), i * nt / np, (i + 1) * nt / np,
+              np == 1 ? -1 : (i == 0 ? 1 : 0));
+      }
+    *count = n;
+    return PA_OK;
+  }
   const int W = pa::active_workers(total, tun.decode_min_steps, decode_workers(cus));
   // Walk every worker's range of the unit step space, unit by unit; a unit
   // piece is one piece per head of the unit.
-  int64_t n = 0;
   size_t j = 0;
   for (int w = 0; w < W; ++w) {
     int64_t t = pa::worker_begin(w, total, W);
@@ -528,16 +569,7 @@ pa_status pa_decode_pieces(const pa_handle* h, const pa_config* cfg, int32_t num
       const int64_t off = t - (int64_t)Hu * dec[j].P;
       const int64_t gu = off / nt, k0 = off % nt, k1 = std::min(nt, k0 + (te - t));
       const bool head = k0 > 0, tail = k1 < nt;
-      for (int hu = 0; hu < HU; ++hu, ++n) {
-        if (n >= cap) continue;
-        pa_decode_piece& pc = pieces[n];
-        pc.seq = dec[j].s;
-        pc.kv_head = (int32_t)(gu * HU + hu);
-        pc.worker = w;
-        pc.first_key = (int32_t)(k0 * KS);
-        pc.end_key = (int32_t)std::min<int64_t>(k1 * KS, dec[j].L);
-        pc.slot = (!head && !tail) ? -1 : (head ? 0 : 1);
-      }
+      put(j, gu, w, k0, k1, (!head && !tail) ? -1 : (head ? 0 : 1));
       t += k1 - k0;
     }
   }
@@ -727,8 +759,10 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     e = timed_launch(h, PA_KERNEL_DECODE, st,
                      [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "decode launch");
-    e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
-    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    if (p.merge_launch) {
+      e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+      if (e != hipSuccess) return hip_fail(e, "merge launch");
+    }
     return PA_OK;
   }
   e = timed_launch(h, PA_KERNEL_PLAN, st, [&] { return pa::launch_plan(a, dp, pp, run_qblock, st); });
@@ -737,8 +771,10 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     e = timed_launch(h, PA_KERNEL_DECODE, st,
                      [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "decode launch");
-    e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
-    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    if (p.merge_launch) {
+      e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+      if (e != hipSuccess) return hip_fail(e, "merge launch");
+    }
   }
   if (run_qblock) {
     e = timed_launch(h, PA_KERNEL_PREFILL, st,

@@ -24,6 +24,11 @@
 // and merge_kernel combines the pieces of every pair that spans several
 // workers.  A worker has at most one head and one tail unit piece, so
 // partial slot (w, 0) holds the head pieces and (w, 1) tail-only pieces.
+// Batches of short sequences (every pair within a few steps, known from the
+// table width) take whole pairs instead: worker w computes pairs
+// [w U / W, (w + 1) U / W) of the U pairs, W = min(U, workers), every piece
+// covers its pair, and no merge follows (one launch fewer where the launch,
+// not the keys, sets the time).
 //
 // Per wave and step: the G query heads of kv head g are the columns of one
 // 16-wide MFMA tile, so every K/V row is read from HBM once.  K and V rows
@@ -229,7 +234,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
     J = nj;
     Wn = active_workers((int64_t)Hu * nsteps, p.min_steps, p.workers);
     dec = list_lds;
-    if (blockIdx.x == 0) {   // the merge kernel, launched next, reads the list from the workspace
+    if (blockIdx.x == 0 && !p.whole_units) {   // the merge kernel, launched next, reads the list from the workspace
       for (int i = tid; i <= nj; i += 64 * kDecodeWaves) p.dec[i] = list_lds[i];
       if (tid == 0) {
         p.meta[0] = J;
@@ -240,412 +245,449 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
     J = p.meta[0];
     Wn = p.meta[1];
   }
-  if (w >= Wn || J <= 0) return;
+  if (J <= 0) return;
   const int64_t Ttot = (int64_t)Hu * dec[J].w;
-  int64_t t = worker_begin(w, Ttot, Wn);
-  const int64_t t_end = worker_begin(w + 1, Ttot, Wn);
-  if (t >= t_end) return;
 
-  // ---- first unit: largest j with Hu * P(j) <= t, by a 64-ary search; the
-  //      wave then holds entries base .. base + 63 of the list, one per lane.
-  int lo = 0, hi = J;
-  while (hi - lo > 63) {
-    const int step = (hi - lo + 63) / 64;
-    const int idx = lo + lane * step;
-    const int64_t P = (int64_t)Hu * dec[min(idx, J)].w;
-    const bool ok = idx < hi && P <= t;
-    lo += (63 - __builtin_clzll(__ballot(ok))) * step;
-    hi = min(hi, lo + step);
-  }
-  int base = lo;
-  int4 ent = dec[min(base + lane, J)];
-  {
-    const bool ok = base + lane < hi && (int64_t)Hu * ent.w <= t;
-    lo = base + (63 - __builtin_clzll(__ballot(ok)));
-  }
-  // Entry jj of the list (jj + 1 - base <= 63 must hold): fields by readlane.
-  auto reload = [&](int jj) {   // rare: the wait below drains everything in flight
-    base = jj;
-    ent = dec[min(base + lane, J)];
-    __builtin_amdgcn_s_waitcnt(0);
-  };
+  // Steps [t, t_end) of the step space, piece by piece.
+  auto run = [&](int64_t t, const int64_t t_end) {
 
-  // Block-table entries of the 64 * NWIN 16-key blocks starting at `first`
-  // (register i, lane l: block first + 64 i + l), loaded from clamped
-  // indices; entries past the sequence end are never used for a valid key,
-  // and every entry is clamped into [0, num_blocks) at its use.
-  auto load_window = [&](const Piece& pc, int first, int (&win)[NWIN]) {
-    const int32_t* bt_row = a.bt + (int64_t)pc.s * a.bt_row;
-#pragma unroll
-    for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(bd.block((first + 64 * i + lane) * 16), a.mb - 1)];
-  };
-  auto make_piece = [&](int jj, int gu, int k0, int64_t budget) {
-    if (jj + 1 - base > 63) reload(jj);
-    Piece pc;
-    jj = uniform(jj);
-    pc.j = jj;
-    pc.gu = uniform(gu);
-    pc.s = lane_i(ent.x, jj - base);
-    pc.t0 = lane_i(ent.y, jj - base);
-    pc.L = min(lane_i(ent.z, jj - base), a.mb * a.block_size);
-    const int nt = lane_i(ent.w, jj + 1 - base) - lane_i(ent.w, jj - base);
-    pc.g = uniform(gu * HU);
-    pc.k0 = uniform(k0);
-    pc.k1 = uniform((int)min((int64_t)nt, (int64_t)k0 + budget));
-    pc.head = pc.k0 > 0;
-    pc.tail = pc.k1 < nt;
-    return pc;
-  };
-  // Q^T of a piece as MFMA B operands, per head hu of the unit: column c16
-  // = query head (g + hu) G + c16 (zero if c16 >= G), k-step st covers
-  // d = 32 st + 8 q4 + j.
-  auto load_q = [&](const Piece& pc, bf16x8 (&qt)[HU][NSTEP]) {
-    const bool hv = c16 < G;
-#pragma unroll
+    // ---- first unit: largest j with Hu * P(j) <= t, by a 64-ary search; the
+    //      wave then holds entries base .. base + 63 of the list, one per lane.
+    int lo = 0, hi = J;
+    while (hi - lo > 63) {
+      const int step = (hi - lo + 63) / 64;
+      const int idx = lo + lane * step;
+      const int64_t P = (int64_t)Hu * dec[min(idx, J)].w;
+      const bool ok = idx < hi && P <= t;
+      lo += (63 - __builtin_clzll(__ballot(ok))) * step;
+      hi = min(hi, lo + step);
+    }
+    int base = lo;
+    int4 ent = dec[min(base + lane, J)];
+    {
+      const bool ok = base + lane < hi && (int64_t)Hu * ent.w <= t;
+      lo = base + (63 - __builtin_clzll(__ballot(ok)));
+    }
+    // Entry jj of the list (jj + 1 - base <= 63 must hold): fields by readlane.
+    auto reload = [&](int jj) {   // rare: the wait below drains everything in flight
+      base = jj;
+      ent = dec[min(base + lane, J)];
+      __builtin_amdgcn_s_waitcnt(0);
+    };
+
+    // Block-table entries of the 64 * NWIN 16-key blocks starting at `first`
+    // (register i, lane l: block first + 64 i + l), loaded from clamped
+    // indices; entries past the sequence end are never used for a valid key,
+    // and every entry is clamped into [0, num_blocks) at its use.
+    auto load_window = [&](const Piece& pc, int first, int (&win)[NWIN]) {
+      const int32_t* bt_row = a.bt + (int64_t)pc.s * a.bt_row;
+  #pragma unroll
+      for (int i = 0; i < NWIN; ++i) win[i] = bt_row[min(bd.block((first + 64 * i + lane) * 16), a.mb - 1)];
+    };
+    auto make_piece = [&](int jj, int gu, int k0, int64_t budget) {
+      if (jj + 1 - base > 63) reload(jj);
+      Piece pc;
+      jj = uniform(jj);
+      pc.j = jj;
+      pc.gu = uniform(gu);
+      pc.s = lane_i(ent.x, jj - base);
+      pc.t0 = lane_i(ent.y, jj - base);
+      pc.L = min(lane_i(ent.z, jj - base), a.mb * a.block_size);
+      const int nt = lane_i(ent.w, jj + 1 - base) - lane_i(ent.w, jj - base);
+      pc.g = uniform(gu * HU);
+      pc.k0 = uniform(k0);
+      pc.k1 = uniform((int)min((int64_t)nt, (int64_t)k0 + budget));
+      pc.head = pc.k0 > 0;
+      pc.tail = pc.k1 < nt;
+      return pc;
+    };
+    // Q^T of a piece as MFMA B operands, per head hu of the unit: column c16
+    // = query head (g + hu) G + c16 (zero if c16 >= G), k-step st covers
+    // d = 32 st + 8 q4 + j.
+    auto load_q = [&](const Piece& pc, bf16x8 (&qt)[HU][NSTEP]) {
+      const bool hv = c16 < G;
+  #pragma unroll
+      for (int hu = 0; hu < HU; ++hu) {
+        const uint8_t* qrow = a.q + (int64_t)pc.t0 * a.q_tok + (int64_t)((pc.g + hu) * G + (hv ? c16 : 0)) * a.q_head;
+  #pragma unroll
+        for (int st = 0; st < NSTEP; ++st) {
+          u32x4 v = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
+          qt[hu][st] = __builtin_bit_cast(bf16x8, v);
+        }
+      }
+    };
+
+    Piece cur;
+    {
+      const int64_t Pj = lane_i(ent.w, lo - base);
+      const int nt = lane_i(ent.w, lo + 1 - base) - (int)Pj;
+      const int64_t off = t - (int64_t)Hu * Pj;
+      cur = make_piece(lo, (int)(off / nt), (int)(off % nt), t_end - t);
+    }
+    bf16x8 qc[HU][NSTEP];
+    int win[NWIN];
+    int cb = 0;   // first 16-key block of the window held in win
+
+    float m_run[HU], l_run[HU];
+    f32x4 o[HU][NDB];
+  #pragma unroll
     for (int hu = 0; hu < HU; ++hu) {
-      const uint8_t* qrow = a.q + (int64_t)pc.t0 * a.q_tok + (int64_t)((pc.g + hu) * G + (hv ? c16 : 0)) * a.q_head;
-#pragma unroll
-      for (int st = 0; st < NSTEP; ++st) {
-        u32x4 v = hv ? ld16_cached(qrow + 2 * (32 * st + 8 * q4)) : u32x4{0, 0, 0, 0};
-        qt[hu][st] = __builtin_bit_cast(bf16x8, v);
-      }
-    }
-  };
-
-  Piece cur;
-  {
-    const int64_t Pj = lane_i(ent.w, lo - base);
-    const int nt = lane_i(ent.w, lo + 1 - base) - (int)Pj;
-    const int64_t off = t - (int64_t)Hu * Pj;
-    cur = make_piece(lo, (int)(off / nt), (int)(off % nt), t_end - t);
-  }
-  bf16x8 qc[HU][NSTEP];
-  int win[NWIN];
-  int cb = 0;   // first 16-key block of the window held in win
-
-  float m_run[HU], l_run[HU];
-  f32x4 o[HU][NDB];
-#pragma unroll
-  for (int hu = 0; hu < HU; ++hu) {
-    m_run[hu] = kNegInf;
-    l_run[hu] = 0.f;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) o[hu][db] = f32x4{0, 0, 0, 0};
-  }
-  // Per head of the unit: a K tile (natural rows) and a V^T tile.
-  uint8_t* const wl = lds + wave * WB;
-  auto kl = [&](int hu) { return wl + hu * HT; };
-  auto vt = [&](int hu) { return wl + hu * HT + KT; };
-
-  // Issue the K/V loads of step k of a pair (kv head g, block cache `cache`
-  // starting at 16-key block cb); live = 0 issues harmless loads of one row.
-  // Addresses: a wave-uniform (scalar) base per 4-row group and a fixed
-  // 32-bit per-lane offset (row lq of the group, head hl of the unit, chunk
-  // ci of that head's row).
-  const uint32_t koff = (uint32_t)(lq * a.kg.slot + hl * a.kg.head + ci * LB);
-  const uint32_t voff = (uint32_t)(lq * a.vg.slot + hl * a.vg.head + ci * LB);
-  // Issue the K (or V) loads of step k of the current piece (block ids from
-  // the window registers; refill() must have made the step's blocks resident).
-  auto issue = [&](const uint8_t* base, const KvGeom& geo, uint32_t off, int k, LT (&rows)[R]) {
-    const int blk0 = uniform(k * BPS - cb);
-#pragma unroll
-    for (int b = 0; b < BPS; ++b) {
-      const int bi = blk0 + b;   // never straddles registers: 64 % BPS == 0
-      int pg = lane_i(win[0], bi & 63);
-#pragma unroll
-      for (int i = 1; i < NWIN; ++i) pg = (bi >> 6) == i ? lane_i(win[i], bi & 63) : pg;
-      pg = pg < 0 ? 0 : (pg >= a.num_blocks ? a.num_blocks - 1 : pg);
-      const int sb = bd.slot(k * KS + 16 * b);   // slot of the 16-key block's first key
-      const uint8_t* bp = base + (int64_t)pg * geo.blk + (int64_t)cur.g * geo.head + (int64_t)sb * geo.slot;
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) rows[4 * b + r4] = ldn<LB>(bp + 4 * r4 * geo.slot + off);
-    }
-  };
-  // bf16 words of one loaded row chunk (DPL values of one key).
-  auto to_bf16 = [&](const LT& v, uint32_t (&wd)[NW]) {
-    if constexpr (FP8) {
-#pragma unroll
-      for (int q = 0; q < LB / 4; ++q) {
-        const u32x2 cv = fp8x4_to_bf16x4(dw<LB>(v, q));
-        wd[2 * q] = cv[0];
-        wd[2 * q + 1] = cv[1];
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < NW; ++q) wd[q] = dw<LB>(v, q);
-    }
-  };
-  // Scores and online-softmax update for step k of the current piece; the
-  // probabilities P^T of sub-tile u (as MFMA B operands) go to pt[u].
-  auto consume_k = [&](int k, LT (&kr)[R], bf16x8 (&pt)[HU][NSUB]) {
-    f32x4 sacc[HU][NSUB][2];
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      // ---- K rows -> LDS (bf16, natural layout), into the tile of head hl
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        uint32_t wd[NW];
-        to_bf16(kr[8 * u + r], wd);
-        uint8_t* dst = kl(hl) + (4 * r + lq) * KRB + ci * (2 * DPL);
-        if constexpr (NW == 8) {
-          *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
-          *(u32x4*)(dst + 16) = u32x4{wd[4], wd[5], wd[6], wd[7]};
-        } else if constexpr (NW == 4) {
-          *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
-        } else {
-          *(u32x2*)dst = u32x2{wd[0], wd[1]};
-        }
-      }
-      // ---- S^T = K Q^T per head; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
-#pragma unroll
-      for (int hu = 0; hu < HU; ++hu)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          f32x4 acc = {0, 0, 0, 0};
-          const uint8_t* kp = kl(hu) + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
-#pragma unroll
-          for (int st = 0; st < NSTEP; ++st)
-            acc = mfma16(*(const bf16x8*)(kp + 64 * st), qc[hu][st], acc);
-          sacc[hu][u][kb] = acc;
-        }
-    }
-    // ---- online softmax (log2 domain); lane holds keys 32u + 16kb + q4 + 4r of head c16
-    const int kend = uniform(cur.L - k * KS);   // keys of this step inside the sequence
-    if (kend < KS) {   // last step of the pair: mask keys >= L (compare with immediates)
-      const int lim = kend - q4;
-#pragma unroll
-      for (int hu = 0; hu < HU; ++hu)
-#pragma unroll
-        for (int u = 0; u < NSUB; ++u)
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              sacc[hu][u][kb][r] = kSub * u + 16 * kb + 4 * r < lim ? sacc[hu][u][kb][r] : kNegInf;
-    }
-#pragma unroll
-    for (int hu = 0; hu < HU; ++hu) {
-      float mx = kNegInf;
-#pragma unroll
-      for (int u = 0; u < NSUB; ++u)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[hu][u][kb][r]);
-      mx = xor16_max(mx);
-      mx = xor32_max(mx) * a.sl2;
-      // The reference max m_run is only raised when some query head's step
-      // max exceeds it by more than 8 (log2 units): the weights then stay
-      // below 2^8, and l, O and the stored partials all use the same
-      // reference, so the result is unchanged while O is rescaled on few
-      // steps only.
-      if (__ballot(mx > m_run[hu] + 8.f)) {
-        const float m_new = fmaxf(m_run[hu], mx);
-        const float alpha = fast_exp2(m_run[hu] - m_new);
-        m_run[hu] = m_new;
-        l_run[hu] *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[hu][db] *= alpha;
-      }
-      float psum = 0.f;
-#pragma unroll
-      for (int u = 0; u < NSUB; ++u) {
-        float x[2][4];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            x[kb][r] = fast_exp2(__builtin_fmaf(sacc[hu][u][kb][r], a.sl2, -m_run[hu]));
-            psum += x[kb][r];
-          }
-        const u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
-                          pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
-        pt[hu][u] = __builtin_bit_cast(bf16x8, pw);
-      }
-      l_run[hu] += psum;
-    }
-  };
-  // V^T column group of sub-tile u for d value e of this lane's chunk: the
-  // bf16 pairs (row 2jj, row 2jj + 1) for jj = 0..3, taken straight from the
-  // loaded row chunks (v_perm pairs the 16-bit halves, or the fp8 bytes,
-  // which one conversion then widens); with MASK, rows of keys >= kend
-  // (lim = kend - lq) read as zero, as their slots may hold NaN.
-  auto vt_col = [&](LT (&vr)[R], int u, int e, int lim, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    u32x4 col;
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int r0 = 8 * u + 2 * jj, r1 = r0 + 1;
-      uint32_t w0, w1;
-      if constexpr (FP8) {
-        w0 = dw<LB>(vr[r0], e >> 2);
-        w1 = dw<LB>(vr[r1], e >> 2);
-      } else {
-        w0 = dw<LB>(vr[r0], e >> 1);
-        w1 = dw<LB>(vr[r1], e >> 1);
-      }
-      if constexpr (MASK) {
-        w0 = kSub * u + 4 * (2 * jj) < lim ? w0 : 0u;
-        w1 = kSub * u + 4 * (2 * jj + 1) < lim ? w1 : 0u;
-      }
-      if constexpr (FP8) {
-        const uint32_t bsel = (uint32_t)(e & 3);
-        const uint32_t pair = __builtin_amdgcn_perm(w1, w0, bsel | ((4u + bsel) << 8) | 0x0C0C0000u);
-        col[jj] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(pair, 1.0f, false));
-      } else {
-        col[jj] = __builtin_amdgcn_perm(w1, w0, (e & 1) ? 0x07060302u : 0x05040100u);
-      }
-    }
-    return col;
-  };
-  // O^T += V^T P^T for step k of the current piece.
-  auto consume_v = [&](int k, LT (&vr)[R], const bf16x8 (&pt)[HU][NSUB]) {
-    const int kend = uniform(cur.L - k * KS);
-    const int lim = kend - lq;
-#pragma unroll
-    for (int u = 0; u < NSUB; ++u) {
-      // ---- V -> V^T: this lane's 8 keys (4r + lq, r = 0..7) are the 8
-      //      consecutive positions of column group lq.
-      if (kend < KS) {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e)
-          *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::true_type{});
-      } else {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e)
-          *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::false_type{});
-      }
-      // ---- O^T += V^T P^T per head
-#pragma unroll
-      for (int hu = 0; hu < HU; ++hu)
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const u32x4 va = *(const u32x4*)(vt(hu) + vt_off<PSH>(16 * db + c16, q4));
-          o[hu][db] = mfma16(__builtin_bit_cast(bf16x8, va), pt[hu][u], o[hu][db]);
-        }
-    }
-  };
-  // End of a piece: bf16 output if the piece is its whole pair, else
-  // partials (rows [wave, slot, head of the unit, query head]).
-  auto finalize = [&]() {
-#pragma unroll
-    for (int hu = 0; hu < HU; ++hu) {
-      float l_tot = xor16_sum(l_run[hu]);
-      l_tot = xor32_sum(l_tot);
-      if (c16 < G) {
-        if (!cur.head && !cur.tail) {
-          const float inv = a.v_scale / l_tot;
-          uint8_t* orow = a.out + (int64_t)cur.t0 * a.o_tok + (int64_t)((cur.g + hu) * G + c16) * a.o_head;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) {
-            const u32x2 v2 = {pack_bf16(o[hu][db][0] * inv, o[hu][db][1] * inv),
-                              pack_bf16(o[hu][db][2] * inv, o[hu][db][3] * inv)};
-            *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
-          }
-        } else {
-          const int64_t row = (((int64_t)w * 2 + (cur.head ? 0 : 1)) * HU + hu) * G + c16;
-          float* po = p.part_o + row * D;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[hu][db];
-          if (q4 == 0) *(f32x2*)(p.part_ml + row * 2) = f32x2{m_run[hu], l_tot};
-        }
-      }
       m_run[hu] = kNegInf;
       l_run[hu] = 0.f;
-#pragma unroll
+  #pragma unroll
       for (int db = 0; db < NDB; ++db) o[hu][db] = f32x4{0, 0, 0, 0};
     }
-  };
+    // Per head of the unit: a K tile (natural rows) and a V^T tile.
+    uint8_t* const wl = lds + wave * WB;
+    auto kl = [&](int hu) { return wl + hu * HT; };
+    auto vt = [&](int hu) { return wl + hu * HT + KT; };
 
-  // Software pipeline over the worker's steps (two register sets, loop
-  // unrolled by two).  Every half issues the loads of the next step (of the
-  // current piece, else the first step of the next piece) unconditionally,
-  // so that each wait covers only the older set; sched_barrier keeps the
-  // compiler from hoisting the consumer's first instructions above them.
-  // Make the blocks of step k resident in the window registers (a new window
-  // starts at the step's first block; the load is waited for at its use).
-  auto refill = [&](int k) {
-    if (k * BPS >= cb + 64 * NWIN) {   // rare: drains the loads in flight
-      cb = uniform(k * BPS);
-      load_window(cur, cb, win);
-      __builtin_amdgcn_s_waitcnt(0);
-    }
-  };
-
-  // Per piece: block ids and query rows, then a software pipeline over its
-  // steps with one step in flight, skewed by half a step: while step k is
-  // consumed, the K loads of step k + 1 are issued before its scores and the
-  // V loads before its P V product, so that step k's K registers are free
-  // before step k + 1's V registers fill.  Two register sets, loop unrolled
-  // by two with an exact tail; every issue in the loop body is
-  // unconditional so that each wait covers only the older set, and
-  // sched_barrier keeps the compiler from hoisting consumers above the loads.
-  LT krA[R], vrA[R], krB[R], vrB[R];
-  auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&kz)[R], LT (&vz)[R]) {
-    bf16x8 pt[HU][NSUB];
-    if (more) {
-      refill(k + 1);
-      issue(a.k, a.kg, koff, k + 1, kz);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    consume_k(k, kx, pt);
-    if (more) {
-      __builtin_amdgcn_sched_barrier(0);
-      issue(a.v, a.vg, voff, k + 1, vz);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    consume_v(k, vx, pt);
-  };
-  // Gather-only: the rows of step k go straight from the load registers
-  // to the dense outputs (keys < L only).
-  auto store_rows = [&](int k, LT (&kx)[R], LT (&vx)[R]) {
-    const int64_t base = (int64_t)cur.s * a.d_seq + (int64_t)(cur.g + hl) * a.d_head + ci * LB;
-#pragma unroll
-    for (int b = 0; b < BPS; ++b)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int key = k * KS + 16 * b + 4 * r4 + lq;
-        if (key < cur.L) {
-          *(LT*)(a.kd + base + (int64_t)key * a.d_tok) = kx[4 * b + r4];
-          *(LT*)(a.vd + base + (int64_t)key * a.d_tok) = vx[4 * b + r4];
+    // Issue the K/V loads of step k of a pair (kv head g, block cache `cache`
+    // starting at 16-key block cb); live = 0 issues harmless loads of one row.
+    // Addresses: a wave-uniform (scalar) base per 4-row group and a fixed
+    // 32-bit per-lane offset (row lq of the group, head hl of the unit, chunk
+    // ci of that head's row).
+    const uint32_t koff = (uint32_t)(lq * a.kg.slot + hl * a.kg.head + ci * LB);
+    const uint32_t voff = (uint32_t)(lq * a.vg.slot + hl * a.vg.head + ci * LB);
+    // Issue the K (or V) loads of step k of the current piece (block ids from
+    // the window registers; refill() must have made the step's blocks resident).
+    auto issue = [&](const uint8_t* base, const KvGeom& geo, uint32_t off, int k, LT (&rows)[R]) {
+      const int blk0 = uniform(k * BPS - cb);
+  #pragma unroll
+      for (int b = 0; b < BPS; ++b) {
+        const int bi = blk0 + b;   // never straddles registers: 64 % BPS == 0
+        int pg = lane_i(win[0], bi & 63);
+  #pragma unroll
+        for (int i = 1; i < NWIN; ++i) pg = (bi >> 6) == i ? lane_i(win[i], bi & 63) : pg;
+        pg = pg < 0 ? 0 : (pg >= a.num_blocks ? a.num_blocks - 1 : pg);
+        const int sb = bd.slot(k * KS + 16 * b);   // slot of the 16-key block's first key
+        const uint8_t* bp = base + (int64_t)pg * geo.blk + (int64_t)cur.g * geo.head + (int64_t)sb * geo.slot;
+  #pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) rows[4 * b + r4] = ldn<LB>(bp + 4 * r4 * geo.slot + off);
+      }
+    };
+    // bf16 words of one loaded row chunk (DPL values of one key).
+    auto to_bf16 = [&](const LT& v, uint32_t (&wd)[NW]) {
+      if constexpr (FP8) {
+  #pragma unroll
+        for (int q = 0; q < LB / 4; ++q) {
+          const u32x2 cv = fp8x4_to_bf16x4(dw<LB>(v, q));
+          wd[2 * q] = cv[0];
+          wd[2 * q + 1] = cv[1];
+        }
+      } else {
+  #pragma unroll
+        for (int q = 0; q < NW; ++q) wd[q] = dw<LB>(v, q);
+      }
+    };
+    // Scores and online-softmax update for step k of the current piece; the
+    // probabilities P^T of sub-tile u (as MFMA B operands) go to pt[u].
+    auto consume_k = [&](int k, LT (&kr)[R], bf16x8 (&pt)[HU][NSUB]) {
+      f32x4 sacc[HU][NSUB][2];
+  #pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        // ---- K rows -> LDS (bf16, natural layout), into the tile of head hl
+  #pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          uint32_t wd[NW];
+          to_bf16(kr[8 * u + r], wd);
+          uint8_t* dst = kl(hl) + (4 * r + lq) * KRB + ci * (2 * DPL);
+          if constexpr (NW == 8) {
+            *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
+            *(u32x4*)(dst + 16) = u32x4{wd[4], wd[5], wd[6], wd[7]};
+          } else if constexpr (NW == 4) {
+            *(u32x4*)dst = u32x4{wd[0], wd[1], wd[2], wd[3]};
+          } else {
+            *(u32x2*)dst = u32x2{wd[0], wd[1]};
+          }
+        }
+        // ---- S^T = K Q^T per head; MFMA row c16 of block kb is key 16kb + (c16>>2) + 4(c16&3)
+  #pragma unroll
+        for (int hu = 0; hu < HU; ++hu)
+  #pragma unroll
+          for (int kb = 0; kb < 2; ++kb) {
+            f32x4 acc = {0, 0, 0, 0};
+            const uint8_t* kp = kl(hu) + (16 * kb + (c16 >> 2) + 4 * (c16 & 3)) * KRB + 16 * q4;
+  #pragma unroll
+            for (int st = 0; st < NSTEP; ++st)
+              acc = mfma16(*(const bf16x8*)(kp + 64 * st), qc[hu][st], acc);
+            sacc[hu][u][kb] = acc;
+          }
+      }
+      // ---- online softmax (log2 domain); lane holds keys 32u + 16kb + q4 + 4r of head c16
+      const int kend = uniform(cur.L - k * KS);   // keys of this step inside the sequence
+      if (kend < KS) {   // last step of the pair: mask keys >= L (compare with immediates)
+        const int lim = kend - q4;
+  #pragma unroll
+        for (int hu = 0; hu < HU; ++hu)
+  #pragma unroll
+          for (int u = 0; u < NSUB; ++u)
+  #pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+  #pragma unroll
+              for (int r = 0; r < 4; ++r)
+                sacc[hu][u][kb][r] = kSub * u + 16 * kb + 4 * r < lim ? sacc[hu][u][kb][r] : kNegInf;
+      }
+  #pragma unroll
+      for (int hu = 0; hu < HU; ++hu) {
+        float mx = kNegInf;
+  #pragma unroll
+        for (int u = 0; u < NSUB; ++u)
+  #pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[hu][u][kb][r]);
+        mx = xor16_max(mx);
+        mx = xor32_max(mx) * a.sl2;
+        // The reference max m_run is only raised when some query head's step
+        // max exceeds it by more than 8 (log2 units): the weights then stay
+        // below 2^8, and l, O and the stored partials all use the same
+        // reference, so the result is unchanged while O is rescaled on few
+        // steps only.
+        if (__ballot(mx > m_run[hu] + 8.f)) {
+          const float m_new = fmaxf(m_run[hu], mx);
+          const float alpha = fast_exp2(m_run[hu] - m_new);
+          m_run[hu] = m_new;
+          l_run[hu] *= alpha;
+  #pragma unroll
+          for (int db = 0; db < NDB; ++db) o[hu][db] *= alpha;
+        }
+        float psum = 0.f;
+  #pragma unroll
+        for (int u = 0; u < NSUB; ++u) {
+          float x[2][4];
+  #pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              x[kb][r] = fast_exp2(__builtin_fmaf(sacc[hu][u][kb][r], a.sl2, -m_run[hu]));
+              psum += x[kb][r];
+            }
+          const u32x4 pw = {pack_bf16(x[0][0], x[0][1]), pack_bf16(x[0][2], x[0][3]),
+                            pack_bf16(x[1][0], x[1][1]), pack_bf16(x[1][2], x[1][3])};
+          pt[hu][u] = __builtin_bit_cast(bf16x8, pw);
+        }
+        l_run[hu] += psum;
+      }
+    };
+    // V^T column group of sub-tile u for d value e of this lane's chunk: the
+    // bf16 pairs (row 2jj, row 2jj + 1) for jj = 0..3, taken straight from the
+    // loaded row chunks (v_perm pairs the 16-bit halves, or the fp8 bytes,
+    // which one conversion then widens); with MASK, rows of keys >= kend
+    // (lim = kend - lq) read as zero, as their slots may hold NaN.
+    auto vt_col = [&](LT (&vr)[R], int u, int e, int lim, auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+      u32x4 col;
+  #pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int r0 = 8 * u + 2 * jj, r1 = r0 + 1;
+        uint32_t w0, w1;
+        if constexpr (FP8) {
+          w0 = dw<LB>(vr[r0], e >> 2);
+          w1 = dw<LB>(vr[r1], e >> 2);
+        } else {
+          w0 = dw<LB>(vr[r0], e >> 1);
+          w1 = dw<LB>(vr[r1], e >> 1);
+        }
+        if constexpr (MASK) {
+          w0 = kSub * u + 4 * (2 * jj) < lim ? w0 : 0u;
+          w1 = kSub * u + 4 * (2 * jj + 1) < lim ? w1 : 0u;
+        }
+        if constexpr (FP8) {
+          const uint32_t bsel = (uint32_t)(e & 3);
+          const uint32_t pair = __builtin_amdgcn_perm(w1, w0, bsel | ((4u + bsel) << 8) | 0x0C0C0000u);
+          col[jj] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(pair, 1.0f, false));
+        } else {
+          col[jj] = __builtin_amdgcn_perm(w1, w0, (e & 1) ? 0x07060302u : 0x05040100u);
         }
       }
-  };
-  for (;;) {
-    cb = uniform(cur.k0 * BPS);
-    load_window(cur, cb, win);
-    if constexpr (GATHER) {
-      __builtin_amdgcn_s_waitcnt(0);
-      for (int k = cur.k0; k < cur.k1; ++k) {
-        refill(k);
-        issue(a.k, a.kg, koff, k, krA);
-        issue(a.v, a.vg, voff, k, vrA);
-        store_rows(k, krA, vrA);
+      return col;
+    };
+    // O^T += V^T P^T for step k of the current piece.
+    auto consume_v = [&](int k, LT (&vr)[R], const bf16x8 (&pt)[HU][NSUB]) {
+      const int kend = uniform(cur.L - k * KS);
+      const int lim = kend - lq;
+  #pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        // ---- V -> V^T: this lane's 8 keys (4r + lq, r = 0..7) are the 8
+        //      consecutive positions of column group lq.
+        if (kend < KS) {
+  #pragma unroll
+          for (int e = 0; e < DPL; ++e)
+            *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::true_type{});
+        } else {
+  #pragma unroll
+          for (int e = 0; e < DPL; ++e)
+            *(u32x4*)(vt(hl) + vt_off<PSH>(ci * DPL + e, lq)) = vt_col(vr, u, e, lim, std::false_type{});
+        }
+        // ---- O^T += V^T P^T per head
+  #pragma unroll
+        for (int hu = 0; hu < HU; ++hu)
+  #pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const u32x4 va = *(const u32x4*)(vt(hu) + vt_off<PSH>(16 * db + c16, q4));
+            o[hu][db] = mfma16(__builtin_bit_cast(bf16x8, va), pt[hu][u], o[hu][db]);
+          }
       }
-    } else {
-    load_q(cur, qc);
-    __builtin_amdgcn_s_waitcnt(0);
-    int k = cur.k0;
-    const int k1 = cur.k1;
-    issue(a.k, a.kg, koff, k, krA);
-    issue(a.v, a.vg, voff, k, vrA);
-    for (; k + 2 < k1; k += 2) {   // A holds step k
-      step(k, true, krA, vrA, krB, vrB);
-      step(k + 1, true, krB, vrB, krA, vrA);
+    };
+    // End of a piece: bf16 output if the piece is its whole pair, else
+    // partials (rows [wave, slot, head of the unit, query head]).
+    auto finalize = [&]() {
+  #pragma unroll
+      for (int hu = 0; hu < HU; ++hu) {
+        float l_tot = xor16_sum(l_run[hu]);
+        l_tot = xor32_sum(l_tot);
+        if (c16 < G) {
+          if (!cur.head && !cur.tail) {
+            const float inv = a.v_scale / l_tot;
+            uint8_t* orow = a.out + (int64_t)cur.t0 * a.o_tok + (int64_t)((cur.g + hu) * G + c16) * a.o_head;
+  #pragma unroll
+            for (int db = 0; db < NDB; ++db) {
+              const u32x2 v2 = {pack_bf16(o[hu][db][0] * inv, o[hu][db][1] * inv),
+                                pack_bf16(o[hu][db][2] * inv, o[hu][db][3] * inv)};
+              *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
+            }
+          } else {
+            const int64_t row = (((int64_t)w * 2 + (cur.head ? 0 : 1)) * HU + hu) * G + c16;
+            float* po = p.part_o + row * D;
+  #pragma unroll
+            for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[hu][db];
+            if (q4 == 0) *(f32x2*)(p.part_ml + row * 2) = f32x2{m_run[hu], l_tot};
+          }
+        }
+        m_run[hu] = kNegInf;
+        l_run[hu] = 0.f;
+  #pragma unroll
+        for (int db = 0; db < NDB; ++db) o[hu][db] = f32x4{0, 0, 0, 0};
+      }
+    };
+
+    // Software pipeline over the worker's steps (two register sets, loop
+    // unrolled by two).  Every half issues the loads of the next step (of the
+    // current piece, else the first step of the next piece) unconditionally,
+    // so that each wait covers only the older set; sched_barrier keeps the
+    // compiler from hoisting the consumer's first instructions above them.
+    // Make the blocks of step k resident in the window registers (a new window
+    // starts at the step's first block; the load is waited for at its use).
+    auto refill = [&](int k) {
+      if (k * BPS >= cb + 64 * NWIN) {   // rare: drains the loads in flight
+        cb = uniform(k * BPS);
+        load_window(cur, cb, win);
+        __builtin_amdgcn_s_waitcnt(0);
+      }
+    };
+
+    // Per piece: block ids and query rows, then a software pipeline over its
+    // steps with one step in flight, skewed by half a step: while step k is
+    // consumed, the K loads of step k + 1 are issued before its scores and the
+    // V loads before its P V product, so that step k's K registers are free
+    // before step k + 1's V registers fill.  Two register sets, loop unrolled
+    // by two with an exact tail; every issue in the loop body is
+    // unconditional so that each wait covers only the older set, and
+    // sched_barrier keeps the compiler from hoisting consumers above the loads.
+    LT krA[R], vrA[R], krB[R], vrB[R];
+    auto step = [&](int k, bool more, LT (&kx)[R], LT (&vx)[R], LT (&kz)[R], LT (&vz)[R]) {
+      bf16x8 pt[HU][NSUB];
+      if (more) {
+        refill(k + 1);
+        issue(a.k, a.kg, koff, k + 1, kz);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      consume_k(k, kx, pt);
+      if (more) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue(a.v, a.vg, voff, k + 1, vz);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      consume_v(k, vx, pt);
+    };
+    // Gather-only: the rows of step k go straight from the load registers
+    // to the dense outputs (keys < L only).
+    auto store_rows = [&](int k, LT (&kx)[R], LT (&vx)[R]) {
+      const int64_t base = (int64_t)cur.s * a.d_seq + (int64_t)(cur.g + hl) * a.d_head + ci * LB;
+  #pragma unroll
+      for (int b = 0; b < BPS; ++b)
+  #pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int key = k * KS + 16 * b + 4 * r4 + lq;
+          if (key < cur.L) {
+            *(LT*)(a.kd + base + (int64_t)key * a.d_tok) = kx[4 * b + r4];
+            *(LT*)(a.vd + base + (int64_t)key * a.d_tok) = vx[4 * b + r4];
+          }
+        }
+    };
+    for (;;) {
+      cb = uniform(cur.k0 * BPS);
+      load_window(cur, cb, win);
+      if constexpr (GATHER) {
+        __builtin_amdgcn_s_waitcnt(0);
+        for (int k = cur.k0; k < cur.k1; ++k) {
+          refill(k);
+          issue(a.k, a.kg, koff, k, krA);
+          issue(a.v, a.vg, voff, k, vrA);
+          store_rows(k, krA, vrA);
+        }
+      } else {
+      load_q(cur, qc);
+      __builtin_amdgcn_s_waitcnt(0);
+      int k = cur.k0;
+      const int k1 = cur.k1;
+      issue(a.k, a.kg, koff, k, krA);
+      issue(a.v, a.vg, voff, k, vrA);
+      for (; k + 2 < k1; k += 2) {   // A holds step k
+        step(k, true, krA, vrA, krB, vrB);
+        step(k + 1, true, krB, vrB, krA, vrA);
+      }
+      if (k + 1 < k1) {
+        step(k, true, krA, vrA, krB, vrB);
+        step(k + 1, false, krB, vrB, krB, vrB);
+      } else {
+        step(k, false, krA, vrA, krA, vrA);
+      }
+      finalize();
+      }
+      t += cur.k1 - cur.k0;
+      if (t >= t_end) break;
+      const int jj = cur.gu + 1 < Hu ? cur.j : cur.j + 1;
+      const int gu = cur.gu + 1 < Hu ? cur.gu + 1 : 0;
+      cur = make_piece(jj, gu, 0, t_end - t);
     }
-    if (k + 1 < k1) {
-      step(k, true, krA, vrA, krB, vrB);
-      step(k + 1, false, krB, vrB, krB, vrB);
-    } else {
-      step(k, false, krA, vrA, krA, vrA);
+  };
+
+  if (p.whole_units) {
+    // Whole pairs: workgroup b takes pairs [b U / B, (b + 1) U / B), B =
+    // min(U, workgroups); the n = min(4, nt) waves split each pair's nt
+    // steps evenly, store their pieces' partials (slot 1 for the first, 0
+    // for the others) and, after a workgroup barrier, merge them (one wave
+    // per (unit head, query head)).  A pair of one step is one piece and
+    // writes its rows itself.
+    const int64_t U = (int64_t)J * Hu;
+    const int B = (int)min(U, (int64_t)gridDim.x);
+    if ((int)blockIdx.x >= B) return;
+    const int64_t ua = U * blockIdx.x / B, ub = U * (blockIdx.x + 1) / B;
+    for (int64_t u = ua; u < ub; ++u) {
+      const int j = (int)(u / Hu), gu = (int)(u % Hu);
+      const int64_t Pj = dec[j].w;
+      const int nt = dec[j + 1].w - (int)Pj;
+      const int n = min(kDecodeWaves, nt);
+      const int64_t s0 = (int64_t)Hu * Pj + (int64_t)gu * nt;
+      if (wave < n) run(s0 + (int64_t)wave * nt / n, s0 + (int64_t)(wave + 1) * nt / n);
+      if constexpr (!GATHER) {
+        if (n > 1) {
+          __syncthreads();   // the pieces' partials are stored
+          const int tok = dec[j].y;
+          for (int x = wave; x < HU * G; x += kDecodeWaves)
+            merge_pieces<D>(a, p, (int)blockIdx.x * kDecodeWaves, n, x / G, x % G, tok, gu * HU + x / G);
+          __syncthreads();   // read before the next pair's pieces reuse the slots
+        }
+      }
     }
-    finalize();
-    }
-    t += cur.k1 - cur.k0;
-    if (t >= t_end) break;
-    const int jj = cur.gu + 1 < Hu ? cur.j : cur.j + 1;
-    const int gu = cur.gu + 1 < Hu ? cur.gu + 1 : 0;
-    cur = make_piece(jj, gu, 0, t_end - t);
+    return;
+  }
+  if (w >= Wn) return;
+  {
+    const int64_t t = worker_begin(w, Ttot, Wn), t_end = worker_begin(w + 1, Ttot, Wn);
+    if (t < t_end) run(t, t_end);
   }
 }
 

@@ -92,6 +92,10 @@ struct DecodePlan {
   int32_t workers;     // decode waves in the static grid
   int32_t step_keys;   // keys per decode step (KS)
   int32_t min_steps;   // fewest steps per active worker when the batch allows
+  // whole_units = 1 (short sequences): worker w takes the whole units
+  // [w U / W, (w + 1) U / W) of the U = J Hu units, W = min(U, workers);
+  // no unit is split and no merge follows.
+  int32_t whole_units;
   int32_t unit_heads;  // HU: adjacent kv heads one worker computes together
   int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
   int4* dec;           // [J + 1] {sequence, token row, length, prefix P(j) of step counts}

@@ -64,6 +64,7 @@ class pa_plan_info(ctypes.Structure):
     _fields_ = [("decode_launch", ctypes.c_int32), ("decode_step", ctypes.c_int32),
                 ("decode_waves", ctypes.c_int32), ("decode_workers", ctypes.c_int32),
                 ("decode_min_steps", ctypes.c_int32), ("decode_unit_heads", ctypes.c_int32),
+                ("decode_whole_units", ctypes.c_int32),
                 ("merge_launch", ctypes.c_int32),
                 ("prefill_launch", ctypes.c_int32), ("block_m", ctypes.c_int32),
                 ("block_q", ctypes.c_int32), ("prefill_tile", ctypes.c_int32),

@@ -132,7 +132,23 @@ def check_partition(c, cus, seq_lens, qsl, T, MB):
     for w in steps:   # per unit piece (its HU heads share the slot, one row each)
         slots = [x["slot"] for x in pcs[::HU] if x["worker"] == w and x["slot"] >= 0]
         assert len(slots) == len(set(slots))
-    if steps:
+    if steps and p["decode_whole_units"]:
+        # whole pairs: workgroup b takes pairs [b U / B, (b + 1) U / B) in
+        # order, B = min(U, workgroups); a pair of nt steps is cut evenly
+        # over the first min(4, nt) waves of its workgroup
+        nw = p["decode_waves"]
+        firsts = [x for x in pcs[::HU] if x["first_key"] == 0]   # one per pair, in order
+        U = len(firsts)
+        B = min(U, p["decode_workers"] // nw)
+        for u, x in enumerate(firsts):
+            b = next(b for b in range(B) if b * U // B <= u < (b + 1) * U // B)
+            assert x["worker"] == b * nw
+            row = rows[(x["seq"], x["kv_head"])]
+            nt = -(-row[-1]["end_key"] // KS)
+            n = min(nw, nt)
+            assert [(y["first_key"] // KS, -(-y["end_key"] // KS)) for y in row] == \
+                [(i * nt // n, (i + 1) * nt // n) for i in range(n)]
+    elif steps:
         assert sorted(steps) == list(range(len(steps)))
         assert max(steps.values()) - min(steps.values()) <= 1
         total = sum(steps.values())   # steps of the unit space
@@ -171,7 +187,9 @@ def test_decode_partition_of_the_benchmark_decode_batch():
 def test_plan_decode_grid_is_static():
     for S, MB in [(1, 1), (64, 513), (16, 8193)]:
         p = plan(cfg(), cus=256, T=S, S=S, MB=MB)
-        assert p["decode_launch"] == 1 and p["merge_launch"] == 1
+        whole = -(-MB * 16 // p["decode_step"]) <= 8
+        assert p["decode_launch"] == 1 and p["merge_launch"] == (0 if whole else 1)
+        assert p["decode_whole_units"] == (1 if whole else 0)
         assert p["decode_workers"] == 256 * 4
         assert p["decode_grid"] == [p["decode_workers"] // p["decode_waves"], 1, 1]
     assert plan(cfg(), cus=80, T=4, S=4, MB=4)["decode_workers"] == 80 * 4
@@ -179,6 +197,33 @@ def test_plan_decode_grid_is_static():
     assert plan(cfg(64, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3))["decode_workers"] == 256 * 4
     assert plan(cfg(8, 2, 64))["decode_step"] == 32   # two heads per unit: 256-byte runs
     assert plan(cfg(8, 2, 64, 16, pa.PA_DTYPE_FP8_E4M3))["decode_step"] == 32  # two 64-byte heads per unit: 128-byte runs of fp8
+
+
+def test_short_sequences_take_whole_pairs_without_merge(monkeypatch):
+    # the tiny decode batch (contexts up to 255, table width 16 blocks of 16):
+    # at most 8 steps per pair, so whole pairs per worker and no merge launch
+    from paper_2511_11581_amd import workloads as W
+    w = W.make_config(1, device="cpu", poison=False)
+    c = cfg(8, 2, 64)
+    MB = int(w.block_table.shape[1])
+    p = plan(c, cus=256, T=w.num_tokens, S=w.num_seqs, MB=MB)
+    assert p["decode_whole_units"] == 1 and p["merge_launch"] == 0
+    pcs = check_partition(c, 256, w.seq_lens.tolist(), w.query_start_loc.tolist(), w.num_tokens, MB)
+    # lengths 18, 65, 101, 256 (context + the new token) = 1, 3, 4, 8 steps of
+    # 32 keys: one workgroup per sequence (Hkv 2 in one unit), its pieces on
+    # 1, 3, 4, 4 waves
+    assert w.seq_lens.tolist() == [18, 65, 101, 256]
+    assert [sum(1 for x in pcs if x["seq"] == i and x["kv_head"] == 0) for i in range(4)] == [1, 3, 4, 4]
+    assert {x["worker"] // 4 for x in pcs if x["seq"] == 3} == {3}
+    # one step more than the limit (a wider table) splits again
+    p = plan(c, cus=256, T=w.num_tokens, S=w.num_seqs, MB=8 * p["decode_step"] // 16 + 1)
+    assert p["decode_whole_units"] == 0 and p["merge_launch"] == 1
+    # PA_DECODE_WHOLE_STEPS=0 turns it off
+    monkeypatch.setenv("PA_DECODE_WHOLE_STEPS", "0")
+    p = plan(c, cus=256, T=w.num_tokens, S=w.num_seqs, MB=MB)
+    assert p["decode_whole_units"] == 0 and p["merge_launch"] == 1
+    pcs = check_partition(c, 256, w.seq_lens.tolist(), w.query_start_loc.tolist(), w.num_tokens, MB)
+    assert len({x["worker"] for x in pcs}) == 16   # 16 steps in all, one per worker
 
 
 def test_decode_unit_heads_make_runs_of_256_bytes():
