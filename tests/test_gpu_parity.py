@@ -80,6 +80,13 @@ SMALL = {
     "prefill_fp8_bs400_d64": ([(0, 500), (300, 20)], 8, 2, 64, "fp8", 400, {}),
     "mixed_bs528": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1), (0, 2)], 32, 8, 128, "bf16", 528, {}),
     "mixed_fp8_bs80": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1)], 32, 8, 128, "fp8", 80, {}),
+    # short sequences only (table width <= 8 decode steps): whole (sequence,
+    # unit) pairs per workgroup, merged inside it; more pairs than
+    # workgroups, so a workgroup runs several pairs in turn
+    "decode_many_short": ([((37 * i) % 207, 1) for i in range(300)], 32, 8, 128, "bf16", 16, {}),
+    "decode_many_short_fp8_g8": ([((53 * i) % 250 + 1, 1) for i in range(100)], 64, 8, 128, "fp8", 16, {}),
+    "mixed_short_g16_d64": ([((29 * i) % 120, 1) for i in range(40)] + [(0, 60), (50, 30), (3, 2)],
+                            32, 2, 64, "bf16", 16, {}),
 }
 
 
