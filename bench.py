@@ -325,14 +325,16 @@ def measure_cache_write(kv, steps, warmup, T=4216, Hkv=8, d=128, bs=16):
             "GBps": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
 
 
-def measure_ladder(steps=3, warmup=1):
+def measure_ladder(steps=20, warmup=3):
     """The paper's optimisation ladder (Sec. 7) on this GPU, three rungs: the
     baseline decomposition (one wave per (token, q head), one page per tile),
     Q-blocks without the split-KV decode kernel (single-token rows as
-    Q-blocks of one token, no split, no merge), and the full path; for 16
-    sequences (ctx U[512, 4096], Hq 32 / Hkv 8, d 128, bf16) whose decode
-    share is 0, 50 or 100 % (decode rows q = 1, the others chunked prefill
-    q = 128).  Relative numbers only."""
+    Q-blocks of one token, no split, no merge), and the full path (the hinted
+    call: the launcher picks split-KV decode + merge + Q-blocks, or, for a
+    mixed batch whose Q-blocks fit one round of workgroups, every row as
+    Q-blocks); for 16 sequences (ctx U[512, 4096], Hq 32 / Hkv 8, d 128,
+    bf16) whose decode share is 0, 50 or 100 % (decode rows q = 1, the
+    others chunked prefill q = 128).  Relative numbers only."""
     import torch
     from paper_2511_11581_amd import workloads as W
     g = torch.Generator().manual_seed(805)
@@ -347,8 +349,10 @@ def measure_ladder(steps=3, warmup=1):
         att_nosplit = make_attention(w, no_split_kv=True)
         out = torch.empty_like(w.q)
         timings = {}
+        hint = hint_of(w)
+        full = lambda *a, **kw: att.forward(*a, hint=hint, **kw)
         for rung, fn in (("baseline", att.forward_baseline), ("qblock", att_nosplit.forward),
-                         ("full", att.forward)):
+                         ("full", full)):
             for _ in range(warmup):
                 fn(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.query_start_loc,
                    w.scale, out=out)
@@ -364,6 +368,15 @@ def measure_ladder(steps=3, warmup=1):
         timings["baseline_over_qblock"] = timings["baseline_us"] / timings["qblock_us"]
         timings["qblock_over_full"] = timings["qblock_us"] / timings["full_us"]
         timings["speedup"] = timings["baseline_us"] / timings["full_us"]
+        route = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]), hint)
+        if route["prefill_qmin"] == 1:
+            timings["full_route"] = "every row as Q-blocks, one launch"
+        elif hint[0] == 0:
+            timings["full_route"] = "Q-blocks"
+        elif hint[1] < 2:
+            timings["full_route"] = "split-KV decode"
+        else:
+            timings["full_route"] = "split-KV decode, then Q-blocks"
         res[str(share)] = timings
         att.close()
         att_nosplit.close()
@@ -543,7 +556,7 @@ def main():
         for share, r in ladder.items():
             print(f"# ladder, decode share {share}%: baseline decomposition {r['baseline_us']:.0f} us, "
                   f"Q-blocks without split {r['qblock_us']:.0f} us, full path {r['full_us']:.0f} us "
-                  f"({r['speedup']:.1f}x)", file=sys.stderr, flush=True)
+                  f"({r['speedup']:.1f}x; {r['full_route']})", file=sys.stderr, flush=True)
 
     decode_like = args.config != 3
     h = headline

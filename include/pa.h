@@ -145,7 +145,7 @@ typedef struct pa_profile {
  * instead (decode_whole_units): every segment covers its pair and the
  * merge launch is skipped. */
 typedef struct pa_plan_info {
-  int32_t decode_launch;     /* 1 if the decode kernels are launched */
+  int32_t decode_launch;     /* 1 if the decode kernel is launched (single-token rows on it) */
   int32_t decode_step;       /* keys per decode step (32, 64 or 128) */
   int32_t decode_waves;      /* waves per decode workgroup */
   int32_t decode_workers;    /* waves in the static decode grid */
@@ -155,6 +155,12 @@ typedef struct pa_plan_info {
                                  (default 8; max_blocks_per_seq x block_size keys), so each
                                  worker takes whole (sequence, unit) pairs and no merge runs */
   int32_t merge_launch;      /* 1 if the log-sum-exp merge kernel is launched */
+  int32_t prefill_qmin;      /* fewest query tokens of a Q-block row: 2 (single-token rows
+                                take the decode kernel), or 1 (every row as Q-blocks, no
+                                decode launch: PA_FLAG_NO_SPLIT_KV, or a hinted mixed batch
+                                whose Q-blocks, its single-token rows included, fill at most
+                                one round of workgroups and whose table width bounds every
+                                sequence to PA_UNIFY_MAX_KEYS keys, default 8192) */
   int32_t prefill_launch;    /* 1 if the Q-block (q_len >= 2) kernel is launched */
   int32_t block_m;           /* rows per Q-block (BLOCK_M, Sec. 4.4) */
   int32_t block_q;           /* query tokens per Q-block (BLOCK_Q = BLOCK_M / G) */
@@ -294,12 +300,13 @@ pa_status pa_cache_write(pa_handle *h, const pa_tensor *key, const pa_tensor *va
                          const pa_tensor *slot_mapping, const pa_tensor *k_cache,
                          const pa_tensor *v_cache, pa_stream stream);
 
-/* The launch plan pa_forward would use for a batch with these host-visible
- * sizes on a device with num_cus compute units (num_cus <= 0: the handle's
- * device, or 256 without a handle).  Host only; no HIP call.  h may be NULL,
- * then cfg is used. */
+/* The launch plan pa_forward (hint NULL) or pa_forward_hinted (hint given)
+ * would use for a batch with these host-visible sizes on a device with
+ * num_cus compute units (num_cus <= 0: the handle's device, or 256 without
+ * a handle).  Host only; no HIP call.  h may be NULL, then cfg is used. */
 pa_status pa_plan(const pa_handle *h, const pa_config *cfg, int32_t num_cus, int64_t num_tokens,
-                  int64_t num_seqs, int64_t max_blocks_per_seq, pa_plan_info *out);
+                  int64_t num_seqs, int64_t max_blocks_per_seq, const pa_batch_hint *hint,
+                  pa_plan_info *out);
 
 /* The decode partition pa_forward computes on the device, reproduced on
  * the host for metadata given in HOST memory (seq_lens [num_seqs],

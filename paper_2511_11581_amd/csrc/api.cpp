@@ -40,6 +40,7 @@ struct pa_event_ring {
 struct pa_tunables {
   int decode_min_steps;
   int decode_whole_steps;
+  int64_t unify_max_keys;
   int qblock_rows;   // 0: chosen from the batch shape; else 128 or 256 (bf16 caches)
 };
 
@@ -90,6 +91,15 @@ constexpr int kMinStepsDefault = 1;
 // no sequence can exceed this many steps (table width x block size): below
 // it the merge launch costs more than splitting the keys saves.
 constexpr int kWholeStepsDefault = 8;
+// A hinted batch mixing single-token rows with longer queries runs every row
+// as Q-blocks (one launch: no decode kernel, no merge) when all its Q-block
+// units, the single-token rows' included, fit in one round of workgroups
+// and no sequence can be longer than this many keys (table width x block
+// size): then the single-token rows run beside the prefill Q-blocks instead
+// of before them.  This is the paper's choice for mixed batches (Sec. 4.5:
+// the split kernel is for decode batches of long sequences); the key bound
+// keeps a long decode row from becoming the batch's longest Q-block.
+constexpr int64_t kUnifyMaxKeysDefault = 8192;
 constexpr int kPrefillTile = 64;
 constexpr uint64_t kHeader = 256;  // validation word + alignment
 constexpr uint64_t kMeta = 256;    // decode-list counters written by the plan kernel
@@ -162,6 +172,7 @@ int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 // sequences are short or the 256-row grid would not fill the CUs twice.
 // PA_QBLOCK_ROWS (128 or 256, read when a handle is created) forces one.
 constexpr int kBlockMMin = 128;
+constexpr int kBlockMMax = 256;   // one workgroup per CU; 128 rows: two
 int block_m(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S, int64_t MB) {
   if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return c.head_dim == 128 ? 256 : 128;
   if (tun.qblock_rows) return tun.qblock_rows;
@@ -223,7 +234,7 @@ WsLayout ws_layout(const pa_config& c, int workers, int64_t S, int64_t items) {
 }
 
 pa_tunables tunables_from_env() {
-  pa_tunables t{kMinStepsDefault, kWholeStepsDefault, 0};
+  pa_tunables t{kMinStepsDefault, kWholeStepsDefault, kUnifyMaxKeysDefault, 0};
   if (const char* e = std::getenv("PA_DECODE_MIN_STEPS")) {
     const int v = std::atoi(e);
     if (v >= 1) t.decode_min_steps = std::min(v, 4096);
@@ -231,6 +242,10 @@ pa_tunables tunables_from_env() {
   if (const char* e = std::getenv("PA_DECODE_WHOLE_STEPS")) {
     const int v = std::atoi(e);
     if (v >= 0) t.decode_whole_steps = std::min(v, 4096);
+  }
+  if (const char* e = std::getenv("PA_UNIFY_MAX_KEYS")) {
+    const long long v = std::atoll(e);
+    if (v >= 0) t.unify_max_keys = v;
   }
   if (const char* e = std::getenv("PA_QBLOCK_ROWS")) {
     const int v = std::atoi(e);
@@ -240,7 +255,7 @@ pa_tunables tunables_from_env() {
 }
 
 void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S,
-               int64_t MB, pa_plan_info* p) {
+               int64_t MB, pa_plan_info* p, const pa_batch_hint* hint = nullptr) {
   std::memset(p, 0, sizeof *p);
   const int G = c.num_q_heads / c.num_kv_heads;
   const int64_t max_len = MB * c.block_size;
@@ -254,18 +269,26 @@ void make_plan(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, i
   p->prefill_tile = kPrefillTile;
   int64_t items = 0;
   if (S >= 1 && T >= 1 && max_len >= 1) {
-    p->decode_launch = 1;
-    p->decode_grid[0] = p->decode_workers / p->decode_waves;
-    p->decode_grid[1] = 1;
-    p->decode_grid[2] = 1;
-    p->decode_whole_units = cdiv(max_len, p->decode_step) <= tun.decode_whole_steps ? 1 : 0;
-    if (!p->decode_whole_units) {
-      p->merge_launch = 1;
-      p->merge_grid[0] = S;
-      p->merge_grid[1] = (G + 3) / 4;
-      p->merge_grid[2] = c.num_kv_heads;
+    int qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
+    if (qmin == 2 && hint && hint->num_decode_seqs > 0 && hint->max_query_len >= 2 &&
+        max_len <= tun.unify_max_keys &&
+        prefill_items(T, S, p->block_q, 1) * c.num_kv_heads <=
+            (int64_t)cus * (kBlockMMax / p->block_m))
+      qmin = 1;   // a small mixed batch: every row as Q-blocks
+    p->prefill_qmin = qmin;
+    if (qmin == 2) {
+      p->decode_launch = 1;
+      p->decode_grid[0] = p->decode_workers / p->decode_waves;
+      p->decode_grid[1] = 1;
+      p->decode_grid[2] = 1;
+      p->decode_whole_units = cdiv(max_len, p->decode_step) <= tun.decode_whole_steps ? 1 : 0;
+      if (!p->decode_whole_units) {
+        p->merge_launch = 1;
+        p->merge_grid[0] = S;
+        p->merge_grid[1] = (G + 3) / 4;
+        p->merge_grid[2] = c.num_kv_heads;
+      }
     }
-    const int qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
     if (T >= qmin && max_len >= qmin) {
       p->prefill_launch = 1;
       items = prefill_items(T, S, p->block_q, qmin);
@@ -387,7 +410,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   dp->part_ml = reinterpret_cast<float*>(ws + wl.part_ml);
   pp->block_m = p.block_m;
   pp->block_q = p.block_q;
-  pp->qmin = (c.flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
+  pp->qmin = p.prefill_qmin;
   pp->work_items = (int32_t)items;
   pp->seq_start = reinterpret_cast<int32_t*>(ws + wl.seq_start);
   pp->list_seq = reinterpret_cast<int32_t*>(ws + wl.list_seq);
@@ -478,9 +501,10 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
   // largest on the largest device, so that batch and device bound all.
   uint64_t best = kHeader;
   if (max_seqs >= 1 && max_tokens >= 1 && max_blocks_per_seq * cfg->block_size >= 1) {
-    const int64_t bq = kBlockMMin / (cfg->num_q_heads / cfg->num_kv_heads);   // most Q-blocks
-    const int qmin = (cfg->flags & PA_FLAG_NO_SPLIT_KV) ? 1 : 2;
-    const int64_t items = max_tokens >= qmin ? prefill_items(max_tokens, max_seqs, bq, qmin) : 0;
+    // most Q-blocks: the smallest BLOCK_M, single-token rows included (the
+    // no-split flag, or a hinted small mixed batch)
+    const int64_t bq = kBlockMMin / (cfg->num_q_heads / cfg->num_kv_heads);
+    const int64_t items = prefill_items(max_tokens, max_seqs, bq, 1);
     best = ws_layout(*cfg, decode_workers(kMaxCus), max_seqs, items).total;
   }
   *bytes = best;
@@ -488,14 +512,16 @@ pa_status pa_workspace_bytes(const pa_config* cfg, int64_t max_tokens, int64_t m
 }
 
 pa_status pa_plan(const pa_handle* h, const pa_config* cfg, int32_t num_cus, int64_t num_tokens,
-                  int64_t num_seqs, int64_t max_blocks_per_seq, pa_plan_info* out) {
+                  int64_t num_seqs, int64_t max_blocks_per_seq, const pa_batch_hint* hint,
+                  pa_plan_info* out) {
   const pa_config* c = h ? &h->cfg : cfg;
   TRY(check_config(c));
   if (!out) return fail(PA_ERR_INVALID_ARG, "out is NULL");
   if (num_tokens < 0 || num_seqs < 0 || max_blocks_per_seq < 0)
     return fail(PA_ERR_INVALID_ARG, "negative size");
   int cus = num_cus > 0 ? num_cus : (h ? h->cus : kMaxCus);
-  make_plan(*c, h ? h->tun : tunables_from_env(), cus, num_tokens, num_seqs, max_blocks_per_seq, out);
+  make_plan(*c, h ? h->tun : tunables_from_env(), cus, num_tokens, num_seqs, max_blocks_per_seq, out,
+            hint);
   return PA_OK;
 }
 
@@ -667,7 +693,7 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   TRY(check_batch(c, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out, &sh));
   if (!(scale > 0.f) || !(scale < 1e30f)) return fail(PA_ERR_INVALID_ARG, "scale must be positive and finite");
   pa_plan_info p;
-  make_plan(c, h->tun, h->cus, sh.T, sh.S, sh.MB, &p);
+  make_plan(c, h->tun, h->cus, sh.T, sh.S, sh.MB, &p, hint);
   if (sh.S * cdiv(sh.MB * c.block_size, p.decode_step) * c.num_kv_heads > INT32_MAX)
     return fail(PA_ERR_UNSUPPORTED, "batch too large for 32-bit decode step indices");
   if (static_scratch && (!ws || p.workspace_bytes > ws_bytes))
@@ -736,14 +762,15 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     if (e != hipSuccess) return hip_fail(e, "baseline launch");
     return PA_OK;
   }
-  if (!p.decode_launch) return PA_OK;
+  if (!p.decode_launch && !p.prefill_launch) return PA_OK;
   pa::DecodePlan dp;
   pa::PrefillPlan pp;
   device_plans(c, p, ws, sh.S, &dp, &pp);
-  // What the hint rules out (the single-token rows take Q-blocks under
-  // PA_FLAG_NO_SPLIT_KV, so then only the Q-block launch is needed).
-  const bool no_split = (c.flags & PA_FLAG_NO_SPLIT_KV) != 0;
-  const bool run_decode = !no_split && !(hint && hint->num_decode_seqs == 0);
+  // What the hint rules out.  Single-token rows take Q-blocks under
+  // PA_FLAG_NO_SPLIT_KV and in a hinted small mixed batch (the plan's
+  // prefill_qmin 1); then only the Q-block launch is needed.
+  const bool no_split = p.prefill_qmin == 1;
+  const bool run_decode = p.decode_launch && !(hint && hint->num_decode_seqs == 0);
   const bool run_qblock = p.prefill_launch &&
                           !(hint && hint->max_query_len >= 0 && hint->max_query_len < (no_split ? 1 : 2));
 
@@ -879,7 +906,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   if (!c.workspace || c.workspace_bytes < p.workspace_bytes)
     return fail(PA_ERR_WORKSPACE, "workspace of %llu bytes needed, %llu given",
                 (unsigned long long)p.workspace_bytes, (unsigned long long)c.workspace_bytes);
-  if (S == 0 || num_tokens == 0 || !p.decode_launch) return PA_OK;
+  if (S == 0 || num_tokens == 0 || (!p.decode_launch && !p.prefill_launch)) return PA_OK;
   const int eb = elem_bytes(c.kv_dtype);
   pa::BatchArgs a;
   std::memset(&a, 0, sizeof a);
@@ -914,8 +941,10 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = pa::launch_plan(a, dp, pp, p.prefill_launch != 0, st);
   if (e != hipSuccess) return hip_fail(e, "plan launch");
-  e = pa::launch_decode(a, dp, c.head_dim, fp8, st, true);
-  if (e != hipSuccess) return hip_fail(e, "decode gather launch");
+  if (p.decode_launch) {
+    e = pa::launch_decode(a, dp, c.head_dim, fp8, st, true);
+    if (e != hipSuccess) return hip_fail(e, "decode gather launch");
+  }
   if (p.prefill_launch) {
     e = pa::launch_prefill(a, pp, c.head_dim, fp8, st, true);
     if (e != hipSuccess) return hip_fail(e, "Q-block gather launch");

@@ -65,7 +65,7 @@ class pa_plan_info(ctypes.Structure):
                 ("decode_waves", ctypes.c_int32), ("decode_workers", ctypes.c_int32),
                 ("decode_min_steps", ctypes.c_int32), ("decode_unit_heads", ctypes.c_int32),
                 ("decode_whole_units", ctypes.c_int32),
-                ("merge_launch", ctypes.c_int32),
+                ("merge_launch", ctypes.c_int32), ("prefill_qmin", ctypes.c_int32),
                 ("prefill_launch", ctypes.c_int32), ("block_m", ctypes.c_int32),
                 ("block_q", ctypes.c_int32), ("prefill_tile", ctypes.c_int32),
                 ("decode_grid", ctypes.c_int64 * 3), ("merge_grid", ctypes.c_int64 * 3),
@@ -125,7 +125,7 @@ def load_library(path: str = LIB_PATH):
     lib.pa_debug_gather.argtypes = [P, T, T, T, T, T, ctypes.c_int64, T, T, P]
     lib.pa_cache_write.argtypes = [P, T, T, T, T, T, P]
     lib.pa_plan.argtypes = [P, C, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
-                            ctypes.POINTER(pa_plan_info)]
+                            ctypes.POINTER(pa_batch_hint), ctypes.POINTER(pa_plan_info)]
     I32P = ctypes.POINTER(ctypes.c_int32)
     lib.pa_decode_pieces.argtypes = [P, C, ctypes.c_int32, I32P, I32P, ctypes.c_int64,
                                      ctypes.c_int64, ctypes.c_int64,
@@ -204,10 +204,12 @@ def pa_destroy(h) -> None:
 
 
 def pa_plan(h=None, cfg: Optional[pa_config] = None, num_cus: int = 0, num_tokens: int = 0,
-            num_seqs: int = 0, max_blocks_per_seq: int = 0) -> dict:
+            num_seqs: int = 0, max_blocks_per_seq: int = 0, hint=None) -> dict:
+    """hint: optional (num_decode_seqs, max_query_len), as for forward."""
     info = pa_plan_info()
+    hp = ctypes.byref(pa_batch_hint(int(hint[0]), int(hint[1]))) if hint is not None else None
     _check(load_library().pa_plan(h, ctypes.byref(cfg) if cfg is not None else None, num_cus,
-                                  num_tokens, num_seqs, max_blocks_per_seq, ctypes.byref(info)))
+                                  num_tokens, num_seqs, max_blocks_per_seq, hp, ctypes.byref(info)))
     return info.as_dict()
 
 
@@ -314,8 +316,8 @@ class PagedAttention:
         self.cfg = cfg
         self.handle = pa_create(cfg)
 
-    def plan(self, num_tokens: int, num_seqs: int, max_blocks_per_seq: int) -> dict:
-        return pa_plan(self.handle, None, 0, num_tokens, num_seqs, max_blocks_per_seq)
+    def plan(self, num_tokens: int, num_seqs: int, max_blocks_per_seq: int, hint=None) -> dict:
+        return pa_plan(self.handle, None, 0, num_tokens, num_seqs, max_blocks_per_seq, hint)
 
     def forward(self, q, k_cache, v_cache, block_table, seq_lens, query_start_loc,
                 scale: Optional[float] = None, out: Optional[torch.Tensor] = None, stream=None,

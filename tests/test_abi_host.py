@@ -226,6 +226,29 @@ def test_short_sequences_take_whole_pairs_without_merge(monkeypatch):
     assert len({x["worker"] for x in pcs}) == 16   # 16 steps in all, one per worker
 
 
+def test_small_mixed_batch_runs_every_row_as_q_blocks(monkeypatch):
+    # 8 single-token rows and 8 chunks of 128 tokens, contexts up to 4096
+    from paper_2511_11581_amd import workloads as W
+    c = cfg()
+    T, S, MB = 8 + 8 * 128, 16, (4096 + 128) // 16 + 1
+    p = plan(c, T=T, S=S, MB=MB)                     # pa_forward: split-KV decode + Q-blocks
+    assert p["prefill_qmin"] == 2 and p["decode_launch"] == 1 and p["merge_launch"] == 1
+    ph = pa.pa_plan(None, c, 256, T, S, MB, (8, 128))   # pa_forward_hinted: one Q-block launch
+    assert ph["prefill_qmin"] == 1 and ph["decode_launch"] == 0 and ph["merge_launch"] == 0
+    assert ph["prefill_units"] <= 256 * (256 // ph["block_m"])
+    assert ph["workspace_bytes"] <= pa.pa_workspace_bytes(c, T, S, MB)
+    # not for decode-only or prefill-only batches, tables past 8192 keys,
+    # or more Q-blocks than one round of workgroups (the mixed benchmark batch)
+    assert pa.pa_plan(None, c, 256, 8, 8, MB, (8, 1))["prefill_qmin"] == 2
+    assert pa.pa_plan(None, c, 256, T, S, MB, (0, 128))["prefill_qmin"] == 2
+    assert pa.pa_plan(None, c, 256, T, S, 8192 // 16 + 1, (8, 128))["prefill_qmin"] == 2
+    w = W.make_config(4, device="cpu", poison=False)
+    assert pa.pa_plan(None, c, 256, w.num_tokens, w.num_seqs, int(w.block_table.shape[1]),
+                      (120, 512))["prefill_qmin"] == 2
+    monkeypatch.setenv("PA_UNIFY_MAX_KEYS", "0")
+    assert pa.pa_plan(None, c, 256, T, S, MB, (8, 128))["prefill_qmin"] == 2
+
+
 def test_decode_unit_heads_make_runs_of_256_bytes():
     F8 = pa.PA_DTYPE_FP8_E4M3
     assert plan(cfg(32, 8, 128))["decode_unit_heads"] == 1          # 256-byte bf16 rows
@@ -309,7 +332,7 @@ def test_plan_q_block_rows_can_be_forced(monkeypatch):
 def test_config_validation(Hq, Hkv, d, bs, kv, status):
     c = cfg(Hq, Hkv, d, bs, kv)
     info = pa.pa_plan_info()
-    st = pa.load_library().pa_plan(None, ctypes.byref(c), 256, 10, 2, 4, ctypes.byref(info))
+    st = pa.load_library().pa_plan(None, ctypes.byref(c), 256, 10, 2, 4, None, ctypes.byref(info))
     assert st == status, pa.pa_last_error()
     if st != pa.PA_OK:
         assert pa.pa_last_error()

@@ -40,8 +40,16 @@ def test_hinted_equals_plain_forward(name, no_split):
                      name=name, token_pad=2)
     att = attention_for(w, no_split_kv=no_split)
     plain = _run(w, att, None)
-    hinted = _run(w, att, _hint_of(w))
-    assert torch.equal(plain.view(torch.int16), hinted.view(torch.int16))
+    hint = _hint_of(w)
+    hinted = _run(w, att, hint)
+    route = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]), hint)["prefill_qmin"]
+    if name == "mixed":   # small mixed batch: every row as Q-blocks when hinted
+        assert route == 1
+    if route == 1 and not no_split:
+        ref = _run(w, attention_for(w, no_split_kv=True), None)   # the no-split path's kernels
+    else:
+        ref = plain
+    assert torch.equal(ref.view(torch.int16), hinted.view(torch.int16))
     unknown = _run(w, att, (-1, -1))
     assert torch.equal(plain.view(torch.int16), unknown.view(torch.int16))
     T = valid_token_count(w)
@@ -117,3 +125,54 @@ def test_in_kernel_list_replays_from_a_hip_graph():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), f"replay {rep}"
+
+
+def test_whole_pairs_replay_from_a_hip_graph_with_new_metadata():
+    # Short sequences (table width 13 blocks of 16 = 6.5 steps of 32 keys):
+    # whole pairs per workgroup, merged inside it, the decode list built in
+    # the kernel (hinted decode-only call), no merge launch.  The graph
+    # captured on batch A replays on batch B's contents (same shapes, other
+    # lengths), and on A again, bitwise equal to the eager call.
+    seqs_a = [((37 * i) % 200, 1) for i in range(70)]
+    seqs_b = [((53 * i + 11) % 200, 1) for i in range(70)]
+    need = max(sum((c + q + 15) // 16 for c, q in s) for s in (seqs_a, seqs_b))
+    wa = W.make_batch(seqs_a, 32, 8, 128, seed=seed_of("whole_a"), pool_blocks=need, table_width=13,
+                      name="whole_a").to("cuda")
+    wb = W.make_batch(seqs_b, 32, 8, 128, seed=seed_of("whole_b"), pool_blocks=need, table_width=13,
+                      name="whole_b").to("cuda")
+    att = attention_for(wa, max_blocks=13)
+    assert att.plan(wa.num_tokens, wa.num_seqs, 13)["decode_whole_units"] == 1
+    args = (wa.q, wa.k_cache, wa.v_cache, wa.block_table, wa.seq_lens, wa.query_start_loc, wa.scale)
+    hint = _hint_of(wa)
+    eager = torch.empty_like(wa.q)
+    att.forward(*args, out=eager, hint=hint)
+    torch.cuda.synchronize()
+    T = valid_token_count(wa)
+    check_close(eager.cpu()[:T], oracle_full(wa)[:T], False, "whole pairs, eager")
+    out = torch.empty_like(wa.q)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        att.forward(*args, out=out, hint=hint)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        att.forward(*args, out=out, hint=hint)
+    saved = [x.clone() for x in args[:6]]
+    for dst, src in zip(args[:6], (wb.q, wb.k_cache, wb.v_cache, wb.block_table, wb.seq_lens,
+                                   wb.query_start_loc)):
+        dst.copy_(src)
+    for rep in range(2):
+        out.fill_(SENTINEL)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        check_close(out.cpu()[:T], oracle_full(wb)[:T], False, f"whole pairs, replay {rep} on batch B")
+    for dst, src in zip(args[:6], saved):
+        dst.copy_(src)
+    out.fill_(SENTINEL)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), "replay on batch A"
