@@ -49,7 +49,7 @@ typedef struct ihipStream_t *pa_stream;
 typedef enum pa_status {
   PA_OK = 0,
   PA_ERR_INVALID_ARG = 1,  /* malformed argument (shape, dtype, stride, null) */
-  PA_ERR_UNSUPPORTED = 2,  /* well-formed but not supported by this build */
+  PA_ERR_UNSUPPORTED = 2,  /* well-formed but not supported by this library */
   PA_ERR_WORKSPACE = 3,    /* workspace missing or too small */
   PA_ERR_DEVICE = 4,       /* HIP error, or PA_FLAG_VALIDATE found bad metadata */
 } pa_status;
