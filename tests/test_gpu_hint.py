@@ -29,6 +29,9 @@ CASES = {
     "prefill_only": ([(0, 300), (40, 77), (0, 2)], 16, 4, 128, "bf16", 16),
     "mixed": ([(1200, 1), (0, 90), (30, 1), (400, 65), (5000, 1), (0, 2)], 32, 8, 128, "fp8", 48),
     "decode_only_fp8": ([(3000, 1), (9, 1)], 16, 2, 128, "fp8", 16),
+    # small mixed batches in other kernel shapes: every row as Q-blocks when hinted
+    "mixed_d64": ([(300, 1), (0, 50), (40, 1), (100, 20), (700, 1)], 8, 2, 64, "bf16", 16),
+    "mixed_fp8_d64": ([(0, 50), (130, 1), (60, 20), (2000, 1)], 8, 2, 64, "fp8", 32),
 }
 
 
@@ -43,7 +46,7 @@ def test_hinted_equals_plain_forward(name, no_split):
     hint = _hint_of(w)
     hinted = _run(w, att, hint)
     route = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]), hint)["prefill_qmin"]
-    if name == "mixed":   # small mixed batch: every row as Q-blocks when hinted
+    if name.startswith("mixed"):   # small mixed batches: every row as Q-blocks when hinted
         assert route == 1
     if route == 1 and not no_split:
         ref = _run(w, attention_for(w, no_split_kv=True), None)   # the no-split path's kernels
