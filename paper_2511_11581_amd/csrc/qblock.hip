@@ -302,9 +302,12 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     }
   };
   // fp8: the wave's staging stage of tile t (K rows, then V rows at + 1 KB)
-  auto stg = [&](int t) { return SBASE + ((t % SSTG) * W + wave) * SWB; };
-  auto issue8_k = [&](int t) { dma16(kp + koff[0], lds_addr(lds + stg(t))); };
-  auto issue8_v = [&](int t) { dma16(vp + voff[0], lds_addr(lds + stg(t) + 1024)); };
+  auto stg_s = [&](int sg) { return SBASE + (sg * W + wave) * SWB; };   // staging stage sg
+  auto stg = [&](int t) { return stg_s(t % SSTG); };
+  auto issue8_k_s = [&](int sg) { dma16(kp + koff[0], lds_addr(lds + stg_s(sg))); };
+  auto issue8_v_s = [&](int sg) { dma16(vp + voff[0], lds_addr(lds + stg_s(sg) + 1024)); };
+  auto issue8_k = [&](int t) { issue8_k_s(t % SSTG); };
+  auto issue8_v = [&](int t) { issue8_v_s(t % SSTG); };
   auto issue8 = [&](int t) {
     issue_prep(t);
     issue8_k(t);
@@ -319,29 +322,30 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   const int r8 = wrow + lane / SCH;
   const int w8k = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fK(r8));
   const int w8v = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fV(r8));
-  auto read8 = [&](int t, int tensor) -> u32x4 {
-    return *(const u32x4*)(lds + stg(t) + 1024 * tensor + 16 * lane);
+  // (The _s forms take the ring and staging stages of tile t as given.)
+  auto read8_s = [&](int sg, int tensor) -> u32x4 {
+    return *(const u32x4*)(lds + stg_s(sg) + 1024 * tensor + 16 * lane);
   };
-  auto put8_k = [&](int t, const u32x4& raw) {
+  auto put8_k_s = [&](int ksg, const u32x4& raw) {
     bf16x8 lo, hi;
     fp8x16_to_bf16(raw, lo, hi);
-    uint8_t* base = lds + kst(t) * TB;
+    uint8_t* base = lds + ksg * TB;
     *(bf16x8*)(base + w8k) = lo;
     *(bf16x8*)(base + (w8k ^ 16)) = hi;
   };
-  auto put8_v = [&](int t, const u32x4& raw) {
+  auto put8_v_s = [&](int vsg, int t, const u32x4& raw) {
     bf16x8 lo, hi;
     fp8x16_to_bf16(raw, lo, hi);
     if (t * kTile + r8 >= kv_len) {   // past the end: zeros (the bytes may be NaN codes)
       lo = bf16x8{};
       hi = bf16x8{};
     }
-    uint8_t* base = lds + VBASE + vst(t) * TB;
+    uint8_t* base = lds + VBASE + vsg * TB;
     *(bf16x8*)(base + w8v) = lo;
     *(bf16x8*)(base + (w8v ^ 16)) = hi;
   };
-  auto widen8_k = [&](int t) { put8_k(t, read8(t, 0)); };
-  auto widen8_v = [&](int t) { put8_v(t, read8(t, 1)); };
+  auto widen8_k = [&](int t) { put8_k_s(kst(t), read8_s(t % SSTG, 0)); };
+  auto widen8_v = [&](int t) { put8_v_s(vst(t), t, read8_s(t % SSTG, 1)); };
   // V rows at or past kv_len (last tile only) may hold anything, NaN
   // included, and would poison P V even with zero weights: each lane zeroes
   // the chunks it loaded, after its own loads have landed.
@@ -480,10 +484,17 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   static_assert(!FP8 || 14 < NS, "fp8: widening and copies between the score products");
   static_assert(kSplit ? 3 + 4 * NLD <= NS + NP : 2 + 3 * ND <= NS + 1,
                 "tile loads fit between the products");
-  auto period = [&](int t, auto full_tag) {
+  auto period = [&](int t, auto full_tag, auto stage_tag) {
     constexpr bool kFullP = decltype(full_tag)::value;
-    const uint8_t* ks = lds + kst(t + 1) * TB;
-    uint8_t* vs = lds + vst(t) * TB;
+    // t mod the unroll length of the main loop (a multiple of every ring's
+    // size) where the caller knows it, else -1: then the stages of tile t + x
+    // are constants and the LDS offsets immediates.
+    constexpr int S4 = decltype(stage_tag)::value;
+    auto kst_at = [&](int x) { return S4 >= 0 ? (S4 + x) % KSTG : kst(t + x); };
+    auto vst_at = [&](int x) { return S4 >= 0 ? (S4 + x) % VSTG : vst(t + x); };
+    auto sst_at = [&](int x) { return S4 >= 0 ? (S4 + x) % SSTG : (t + x) % SSTG; };
+    const uint8_t* ks = lds + kst_at(1) * TB;
+    uint8_t* vs = lds + vst_at(0) * TB;
     auto rd = [&](int i) -> bf16x8 {   // operand of product i (i < NS: K, else V^T)
       if (i < NS) return *(const bf16x8*)(ks + kaddr[i >> 1] + 32 * RB * (i & 1));
       const int u = (i - NS) / NDB, db = (i - NS) % NDB;
@@ -516,16 +527,16 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
           if (i == 0) {
             if (t + 3 < ntiles) wait_vm<2>();
             else wait_vm<0>();
-            raw8 = read8(t + 2, 0);
+            raw8 = read8_s(sst_at(2), 0);
           }
-          if (i == 3) put8_k(t + 2, raw8);
-          if (i == 6) raw8 = read8(t + 2, 1);
-          if (i == 9) put8_v(t + 2, raw8);
+          if (i == 3) put8_k_s(kst_at(2), raw8);
+          if (i == 6) raw8 = read8_s(sst_at(2), 1);
+          if (i == 9) put8_v_s(vst_at(2), t + 2, raw8);
         }
         if (t + 4 < ntiles) {
           if (i == 11) issue_prep(t + 4);
-          if (i == 12) issue8_k(t + 4);
-          if (i == 14) issue8_v(t + 4);
+          if (i == 12) issue8_k_s(sst_at(4));
+          if (i == 14) issue8_v_s(sst_at(4));
         }
       }
       if constexpr (kFullP && !kSplit && !FP8) {
@@ -534,8 +545,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
           if (i == 1) issue_prep(t + 3);
           if (i >= 2 && i < 2 + 3 * ND && (i - 2) % 3 == 0) {
             const int j = (i - 2) / 3;
-            if (j & 1) issue_vpart(t + 3, j >> 1);
-            else issue_kpart(t + 3, j >> 1);
+            if (j & 1) dma16(vp + voff[j >> 1], lds_addr(lds + VBASE + vst_at(3) * TB + (wave * NLD + (j >> 1)) * 1024));
+            else dma16(kp + koff[j >> 1], lds_addr(lds + kst_at(3) * TB + (wave * NLD + (j >> 1)) * 1024));
           }
         }
       }
@@ -544,11 +555,13 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
         // second product
         if (t + 1 < ntiles) {
           if (i == 1) issue_prep(t + 1);
-          if (i >= 2 && i < 2 + 2 * NLD && (i & 1) == 0) issue_vpart(t + 1, (i - 2) / 2);
+          if (i >= 2 && i < 2 + 2 * NLD && (i & 1) == 0)
+            dma16(vp + voff[(i - 2) / 2], lds_addr(lds + VBASE + vst_at(1) * TB + (wave * NLD + (i - 2) / 2) * 1024));
         }
         if (t + 3 < ntiles) {
           if (i == 2 + 2 * NLD) issue_prep(t + 3);
-          if (i >= 3 + 2 * NLD && i < 3 + 4 * NLD && ((i - 3) & 1) == 0) issue_kpart(t + 3, (i - 3 - 2 * NLD) / 2);
+          if (i >= 3 + 2 * NLD && i < 3 + 4 * NLD && ((i - 3) & 1) == 0)
+            dma16(kp + koff[(i - 3 - 2 * NLD) / 2], lds_addr(lds + kst_at(3) * TB + (wave * NLD + (i - 3 - 2 * NLD) / 2) * 1024));
         }
       }
       if constexpr (kFullP) {
@@ -734,15 +747,33 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   constexpr std::true_type kFull{};
   constexpr std::false_type kPvOnly{};
   int t = 0;
-  for (; t + 1 < nact; ++t) {
-    sync(t);
+  // Full periods, unrolled by L (a multiple of every ring's size: 4, 3 + 2
+  // or 3) so that the stages inside them are constants; the rest one by one.
+  constexpr std::integral_constant<int, -1> sN{};
+  constexpr int L = FP8 ? 3 : (KSTG == 4 && VSTG == 4 ? 4 : 6);
+  static_assert(L % KSTG == 0 && L % VSTG == 0 && (!FP8 || L % SSTG == 0), "unroll length");
+  auto full = [&](int tt, auto stage_tag) {
+    sync(tt);
     rescale();
-    period(t, kFull);   // issues this period's loads as well
-  }
+    period(tt, kFull, stage_tag);   // issues this period's loads as well
+  };
+  auto unrolled = [&](auto... stage_tags) {
+    for (; t + L < nact; t += L) (full(t + decltype(stage_tags)::value, stage_tags), ...);
+  };
+  using std::integral_constant;
+  if constexpr (L == 3)
+    unrolled(integral_constant<int, 0>{}, integral_constant<int, 1>{}, integral_constant<int, 2>{});
+  else if constexpr (L == 4)
+    unrolled(integral_constant<int, 0>{}, integral_constant<int, 1>{}, integral_constant<int, 2>{},
+             integral_constant<int, 3>{});
+  else
+    unrolled(integral_constant<int, 0>{}, integral_constant<int, 1>{}, integral_constant<int, 2>{},
+             integral_constant<int, 3>{}, integral_constant<int, 4>{}, integral_constant<int, 5>{});
+  for (; t + 1 < nact; ++t) full(t, sN);
   sync(t);
   load_next(t);
   rescale();
-  period(t, kPvOnly);
+  period(t, kPvOnly, sN);
   for (++t; t < ntiles; ++t) {
     sync(t);
     load_next(t);
