@@ -56,10 +56,11 @@ def test_noalloc_matches_pa_forward_twice_second_smaller(kv):
 
 
 def test_noalloc_rejects_a_batch_beyond_the_static_scratch():
-    # 200M query rows (stride-0 views, nothing is read): the Q-block work
-    # list alone needs more than the scratch holds; refused before launch.
+    # 10^9 query rows (stride-0 views, nothing is read): the Q-block work
+    # list alone needs ~375 MB, more than the scratch holds; refused before
+    # launch.
     w = W.make_batch([(10, 1)], 8, 2, 128, seed=1, device="cuda")
-    T = 200_000_000
+    T = 1_000_000_000
     q = torch.zeros(1, 8, 128, dtype=torch.bfloat16, device="cuda").expand(T, 8, 128)
     out = torch.zeros(1, 8, 128, dtype=torch.bfloat16, device="cuda").expand(T, 8, 128)
     h = _handle_without_workspace(w)
