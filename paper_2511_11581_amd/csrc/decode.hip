@@ -95,9 +95,10 @@ struct Piece {
 // M = max_k m_k, out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k, lanes
 // over d.  Piece k sits with worker w0 + k (slot 1 for the pair's first
 // worker, slot 0 for the others), head hu of its unit, query head hh of the
-// group; the result goes to row `tok`, query head g G + hh.  The pieces'
-// (m, l) are read one per lane, 64 at a time, and their weights reach the
-// lanes by readlane.
+// group; the result goes to row `tok`, query head g G + hh.  Up to 8 pieces
+// are read in one round (every lane reads their (m, l)); more are read 64
+// (m, l) at a time, one per lane, their weights reaching the lanes by
+// readlane.
 template <int D>
 __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePlan& p, int w0, int n,
                                              int hu, int hh, int tok, int g) {
@@ -105,6 +106,39 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
   const int lane = threadIdx.x & 63;
   const int HU = p.unit_heads, G = a.group;
   auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
+  uint8_t* orow = a.out + (int64_t)tok * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
+  auto store = [&](const float (&num)[DPT], float den) {
+    const float inv = a.v_scale / den;
+    if constexpr (DPT == 2) *(uint32_t*)orow = pack_bf16(num[0] * inv, num[1] * inv);
+    else *(__bf16*)orow = (__bf16)(num[0] * inv);
+  };
+  if (n <= 8) {
+    // Up to 8 pieces: their (m, l) (the same for every lane) and their
+    // partials in one round of loads.
+    f32x2 ml[8];
+    float v[8][DPT];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = min(i, n - 1);
+      ml[i] = *(const f32x2*)(p.part_ml + row_of(k) * 2);
+      const float* po = p.part_o + row_of(k) * D + lane * DPT;
+#pragma unroll
+      for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
+    }
+    float M = ml[0][0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) M = i < n ? fmaxf(M, ml[i][0]) : M;
+    float num[DPT] = {}, den = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float wi = i < n ? fast_exp2(ml[i][0] - M) : 0.f;
+      den += wi * ml[i][1];
+#pragma unroll
+      for (int x = 0; x < DPT; ++x) num[x] += wi * v[i][x];
+    }
+    store(num, den);
+    return;
+  }
   float M = kNegInf;
   for (int k0 = 0; k0 < n; k0 += 64) {
     const int k = k0 + lane;
@@ -149,10 +183,7 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
   den += __shfl_xor(den, 4);
   den += __shfl_xor(den, 2);
   den += __shfl_xor(den, 1);
-  const float inv = a.v_scale / den;
-  uint8_t* orow = a.out + (int64_t)tok * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
-  if constexpr (DPT == 2) *(uint32_t*)orow = pack_bf16(num[0] * inv, num[1] * inv);
-  else *(__bf16*)orow = (__bf16)(num[0] * inv);
+  store(num, den);
 }
 
 // GATHER: the same partition, block-table walk and loads, but every loaded
@@ -239,6 +270,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
       if (tid == 0) {
         p.meta[0] = J;
         p.meta[1] = Wn;
+        p.meta[2] = nsteps;
       }
     }
   } else {
@@ -699,13 +731,16 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
   const int jj = blockIdx.x, G = a.group;
   const int hh = uniform(blockIdx.y * 4 + (threadIdx.x >> 6));   // head within the group
   const int g = blockIdx.z;
-  const int J = p.meta[0], Wn = p.meta[1];
+  // The counters and the pair's two list entries in one round of loads
+  // (entries jj, jj + 1 <= S exist whatever J is).
+  const int J = p.meta[0], Wn = p.meta[1], PJ = p.meta[2];
+  const int4 e = p.dec[jj];
+  const int4 e1 = p.dec[jj + 1];
   if (jj >= J || hh >= G) return;
   const int HU = p.unit_heads, Hu = a.num_kv_heads / HU;
   const int gu = g / HU, hu = g - gu * HU;
-  const int4 e = p.dec[jj];
-  const int nt = p.dec[jj + 1].w - e.w;
-  const int64_t Ttot = (int64_t)Hu * p.dec[J].w;
+  const int nt = e1.w - e.w;
+  const int64_t Ttot = (int64_t)Hu * PJ;
   const int64_t ta = (int64_t)Hu * e.w + (int64_t)gu * nt;
   const int w0 = worker_of(ta, Ttot, Wn), w1 = worker_of(ta + nt - 1, Ttot, Wn);
   if (w0 == w1) return;

@@ -97,7 +97,7 @@ struct DecodePlan {
   // no unit is split and no merge follows.
   int32_t whole_units;
   int32_t unit_heads;  // HU: adjacent kv heads one worker computes together
-  int32_t* meta;       // [2] written by the plan kernel: decode sequences J, active workers
+  int32_t* meta;       // [3] written by the plan kernel: decode sequences J, active workers, P(J)
   int4* dec;           // [J + 1] {sequence, token row, length, prefix P(j) of step counts}
   // fused = 1 (decode-only batches): each workgroup builds the decode list
   // in LDS itself, the plan kernel's pass over the sequences, and workgroup

@@ -19,9 +19,14 @@ namespace pa {
 
 namespace {
 
-constexpr int kPlanThreads = 1024;
+// 256 threads: the work is a few passes over the sequences and Q-blocks,
+// and each block-wide scan costs fewer barrier rounds than with 1024
+// (measured 6.7 against 7.6 us per call on a 4-sequence prefill batch).
+constexpr int kPlanThreads = 256;
 constexpr int kPlanSortCap = 8192;   // larger Q-block lists keep the natural order
-constexpr int kPlanBuckets = 2048;   // key-tile counts are clamped to this
+// Key-tile counts are clamped to the last bucket: Q-blocks of more than
+// 32K keys all sort first, in batch order among themselves.
+constexpr int kPlanBuckets = 512;
 
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodePlan dp, PrefillPlan pp,
@@ -66,6 +71,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     dp.dec[njs] = make_int4(0, 0, 0, nsteps);
     dp.meta[0] = njs;
     dp.meta[1] = active_workers((int64_t)(a.num_kv_heads / dp.unit_heads) * nsteps, dp.min_steps, dp.workers);
+    dp.meta[2] = nsteps;
     if (with_prefill) {
       pp.seq_start[S] = nqb;
       pp.count[0] = min(nqb, pp.work_items);
