@@ -242,9 +242,9 @@ def test_small_mixed_batch_runs_every_row_as_q_blocks(monkeypatch):
     assert pa.pa_plan(None, c, 256, 8, 8, MB, (8, 1))["prefill_qmin"] == 2
     assert pa.pa_plan(None, c, 256, T, S, MB, (0, 128))["prefill_qmin"] == 2
     assert pa.pa_plan(None, c, 256, T, S, 8192 // 16 + 1, (8, 128))["prefill_qmin"] == 2
-    w = W.make_config(4, device="cpu", poison=False)
-    assert pa.pa_plan(None, c, 256, w.num_tokens, w.num_seqs, int(w.block_table.shape[1]),
-                      (120, 512))["prefill_qmin"] == 2
+    seqs = W.config_seqs(4)[0]   # its shape only: 128 sequences, 4216 tokens
+    T4, MB4 = sum(q for _, q in seqs), max(-(-(c + q) // 16) for c, q in seqs)
+    assert pa.pa_plan(None, c, 256, T4, len(seqs), MB4, (120, 512))["prefill_qmin"] == 2
     monkeypatch.setenv("PA_UNIFY_MAX_KEYS", "0")
     assert pa.pa_plan(None, c, 256, T, S, MB, (8, 128))["prefill_qmin"] == 2
 
