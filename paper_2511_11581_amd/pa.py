@@ -15,6 +15,8 @@ from __future__ import annotations
 
 import ctypes
 import os
+import struct
+import threading
 from typing import Optional
 
 import torch
@@ -171,6 +173,32 @@ def describe(t: torch.Tensor) -> pa_tensor:
     return d
 
 
+# The per-call path packs the descriptors with struct into one array per
+# thread (the same bytes as describe(), ~1.3 us per tensor against ~3.8 us
+# for field-by-field ctypes assignment, which dominated small calls).
+_PACK = struct.Struct("=Qii4q4q")
+assert _PACK.size == ctypes.sizeof(pa_tensor)
+_ZEROS = ((), (0,), (0, 0), (0, 0, 0), (0, 0, 0, 0))
+_tls = threading.local()
+
+
+def _descs(*tensors):
+    """Pointers to descriptors of `tensors`, valid until this thread's next call."""
+    arr = getattr(_tls, "arr", None)
+    if arr is None:
+        arr = _tls.arr = (pa_tensor * 8)()
+        _tls.refs = tuple(ctypes.byref(arr[i]) for i in range(8))   # views of arr's buffer
+    for i, t in enumerate(tensors):
+        sh = t.shape
+        n = len(sh)
+        if n > PA_MAX_DIMS:
+            raise ValueError("at most 4 dimensions")
+        z = _ZEROS[PA_MAX_DIMS - n]
+        _PACK.pack_into(arr, i * _PACK.size, t.data_ptr() if t.numel() > 0 else 0,
+                        _DTYPES.get(t.dtype, -1), n, *sh, *z, *t.stride(), *z)
+    return _tls.refs[:len(tensors)]
+
+
 def make_config(num_q_heads, num_kv_heads, head_dim, block_size=16, kv_dtype=PA_DTYPE_BF16,
                 k_scale=1.0, v_scale=1.0, flags=0, workspace=0, workspace_bytes=0) -> pa_config:
     c = pa_config()
@@ -248,9 +276,8 @@ def _stream(stream):
 
 def pa_forward(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
                stream=None) -> None:
-    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
-    _check(load_library().pa_forward(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
-                                     ctypes.byref(ds[6]), _stream(stream)))
+    d = _descs(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)
+    _check(load_library().pa_forward(h, *d[:6], float(scale), d[6], _stream(stream)))
 
 
 def pa_forward_hinted(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
@@ -258,39 +285,35 @@ def pa_forward_hinted(h, q, k_cache, v_cache, block_table, seq_lens, query_start
     """pa_forward with the host's knowledge of the batch (-1: unknown): no
     decode rows skips the decode + merge launches, max_query_len <= 1 the
     Q-block launch."""
-    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
+    d = _descs(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)
     hint = pa_batch_hint(int(num_decode_seqs), int(max_query_len))
-    _check(load_library().pa_forward_hinted(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
-                                            ctypes.byref(ds[6]), ctypes.byref(hint), _stream(stream)))
+    _check(load_library().pa_forward_hinted(h, *d[:6], float(scale), d[6], ctypes.byref(hint),
+                                            _stream(stream)))
 
 
 def pa_forward_noalloc(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale, out,
                        stream=None) -> None:
     """pa_forward with the library's static device scratch instead of a
     workspace (for callers that cannot allocate)."""
-    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
-    _check(load_library().pa_forward_noalloc(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
-                                             ctypes.byref(ds[6]), _stream(stream)))
+    d = _descs(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)
+    _check(load_library().pa_forward_noalloc(h, *d[:6], float(scale), d[6], _stream(stream)))
 
 
 def pa_forward_baseline(h, q, k_cache, v_cache, block_table, seq_lens, query_start_loc, scale,
                         out, stream=None) -> None:
-    ds = [describe(t) for t in (q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)]
-    _check(load_library().pa_forward_baseline(h, *(ctypes.byref(d) for d in ds[:6]), float(scale),
-                                              ctypes.byref(ds[6]), _stream(stream)))
+    d = _descs(q, k_cache, v_cache, block_table, seq_lens, query_start_loc, out)
+    _check(load_library().pa_forward_baseline(h, *d[:6], float(scale), d[6], _stream(stream)))
 
 
 def pa_debug_gather(h, k_cache, v_cache, block_table, seq_lens, query_start_loc, num_tokens,
                     k_dense, v_dense, stream=None) -> None:
-    ds = [describe(t) for t in (k_cache, v_cache, block_table, seq_lens, query_start_loc)]
-    dn = [describe(t) for t in (k_dense, v_dense)]
-    _check(load_library().pa_debug_gather(h, *(ctypes.byref(d) for d in ds), int(num_tokens),
-                                          *(ctypes.byref(d) for d in dn), _stream(stream)))
+    d = _descs(k_cache, v_cache, block_table, seq_lens, query_start_loc, k_dense, v_dense)
+    _check(load_library().pa_debug_gather(h, *d[:5], int(num_tokens), *d[5:], _stream(stream)))
 
 
 def pa_cache_write(h, key, value, slot_mapping, k_cache, v_cache, stream=None) -> None:
-    ds = [describe(t) for t in (key, value, slot_mapping, k_cache, v_cache)]
-    _check(load_library().pa_cache_write(h, *(ctypes.byref(d) for d in ds), _stream(stream)))
+    d = _descs(key, value, slot_mapping, k_cache, v_cache)
+    _check(load_library().pa_cache_write(h, *d, _stream(stream)))
 
 
 class PagedAttention:
