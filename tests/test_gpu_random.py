@@ -15,7 +15,8 @@ from gpu_util import SENTINEL, attention_for, check_close, oracle_full, valid_to
 
 pytestmark = pytest.mark.gpu
 
-HEADS = [(8, 2, 64), (32, 8, 128), (16, 2, 128), (8, 8, 128), (64, 8, 128), (16, 1, 64), (4, 4, 64)]
+HEADS = [(8, 2, 64), (32, 8, 128), (16, 2, 128), (8, 8, 128), (64, 8, 128), (16, 1, 64), (4, 4, 64),
+         (16, 1, 128), (4, 2, 128), (16, 8, 64)]
 BLOCKS = [16, 32, 48, 64, 400]
 MAX_KEYS = 60_000          # keys of the batch (cache size)
 MAX_WORK = 2e9             # (query row, key) pairs x query heads x d: the oracle's work
