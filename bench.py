@@ -418,7 +418,13 @@ def cpu_baseline(w, budget_s=15.0, flops=False):
     m = max(1, min(w.num_seqs, int(budget_s / max(per_seq, 1e-6))))
     s = sub(m)
     t = run(s) if m != probe.num_seqs else tp
-    value, unit = (alg_flops(s) / t / 1e12, "TFLOP/s") if flops else (alg_bytes(s) / t / 1e9, "GB/s")
+    # a whole batch that takes well under the budget is run repeatedly
+    passes = 1
+    if m == w.num_seqs and t < budget_s / 2:
+        passes = max(1, min(100, int(budget_s / max(t, 1e-6))))
+        t = sum(run(s) for _ in range(passes))
+    work = alg_flops(s) if flops else alg_bytes(s)
+    value, unit = (work * passes / t / 1e12, "TFLOP/s") if flops else (work * passes / t / 1e9, "GB/s")
     model = "unknown"
     try:
         with open("/proc/cpuinfo") as fh:
@@ -427,8 +433,8 @@ def cpu_baseline(w, budget_s=15.0, flops=False):
         pass
     return {"value": value, "unit": unit, "cores": threads, "kind": "oracle", "cpu_model": model,
             "nproc": os.cpu_count(),
-            "sample": f"first {m} of {w.num_seqs} sequences (sum_L={sum(s.seq_len_list)}), "
-                      f"fp64 C oracle, {t:.1f} s"}
+            "sample": f"first {m} of {w.num_seqs} sequences (sum_L={sum(s.seq_len_list)})"
+                      + (f", {passes} passes" if passes > 1 else "") + f", fp64 C oracle, {t:.1f} s"}
 
 
 def main():
