@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libpa.so")
 BUILD = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.cpp", "plan.hip", "decode.hip", "prefill.hip", "qblock.hip", "misc.hip", "cache.hip", "baseline.hip"]
+SOURCES = ["api.cpp", "plan.hip", "decode.hip", "qblock.hip", "misc.hip", "cache.hip", "baseline.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(HERE, "..", "include")]

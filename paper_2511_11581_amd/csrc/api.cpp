@@ -12,8 +12,7 @@
 //   3. the log-sum-exp merge of pairs that span several workers;
 //   4. the Q-block kernel for rows with two or more query tokens (Sec. 4.4),
 //      BLOCK_M = 256 or 128 rows (bf16 caches, chosen from the batch shape),
-//      256 (fp8 caches, d = 128) or 128 (fp8, d = 64), i.e. BLOCK_Q =
-//      BLOCK_M / G tokens.
+//      256 (fp8 caches), i.e. BLOCK_Q = BLOCK_M / G tokens.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -160,9 +159,8 @@ int decode_step_keys(const pa_config& c) {
 
 int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 
-// Rows per Q-block.  fp8 caches: 256 for d = 128 (the bf16 kernel's 8-wave
-// shape, widening its copies to bf16 in LDS), 128 for d = 64 (a
-// register-staged kernel).  bf16 caches: 256
+// Rows per Q-block.  fp8 caches: 256 (the bf16 kernel's 8-wave shape,
+// widening its copies to bf16 in LDS).  bf16 caches: 256
 // (8 waves, one workgroup per CU) or 128 (4 waves, two workgroups per CU),
 // chosen from host-visible sizes by a decision tree fitted offline to the
 // faster of the two on 47 prefill-heavy shapes (1-64 sequences, 16-4096 new
@@ -174,7 +172,7 @@ int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 constexpr int kBlockMMin = 128;
 constexpr int kBlockMMax = 256;   // one workgroup per CU; 128 rows: two
 int block_m(const pa_config& c, const pa_tunables& tun, int cus, int64_t T, int64_t S, int64_t MB) {
-  if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return c.head_dim == 128 ? 256 : 128;
+  if (c.kv_dtype == PA_DTYPE_FP8_E4M3) return 256;   // the fp8 staging runs 8 waves
   if (tun.qblock_rows) return tun.qblock_rows;
   if (T < 2 || S < 1) return 256;
   const int G = c.num_q_heads / c.num_kv_heads;
@@ -805,7 +803,7 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   }
   if (run_qblock) {
     e = timed_launch(h, PA_KERNEL_PREFILL, st,
-                     [&] { return pa::launch_prefill(a, pp, c.head_dim, fp8, st); });
+                     [&] { return pa::launch_qblock(a, pp, c.head_dim, fp8, st); });
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }
   return PA_OK;
@@ -946,7 +944,7 @@ pa_status pa_debug_gather(pa_handle* h, const pa_tensor* k_cache, const pa_tenso
     if (e != hipSuccess) return hip_fail(e, "decode gather launch");
   }
   if (p.prefill_launch) {
-    e = pa::launch_prefill(a, pp, c.head_dim, fp8, st, true);
+    e = pa::launch_qblock(a, pp, c.head_dim, fp8, st, true);
     if (e != hipSuccess) return hip_fail(e, "Q-block gather launch");
   }
   return PA_OK;

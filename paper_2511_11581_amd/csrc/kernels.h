@@ -7,10 +7,10 @@
 namespace pa {
 
 constexpr int kPrefillTileKeys = 64;   // keys per tile of the Q-block kernels
-// Q-block kernels: waves of 32 rows.  bf16 caches: 8 waves (BLOCK_M = 256,
+// Q-block kernel: waves of 32 rows.  bf16 caches: 8 waves (BLOCK_M = 256,
 // one workgroup per CU, two waves per SIMD) or 4 waves (BLOCK_M = 128, two
-// workgroups per CU), tiles copied straight into LDS; fp8 caches: 4 waves
-// (BLOCK_M = 128), tiles converted to bf16 on their way into LDS.
+// workgroups per CU), tiles copied straight into LDS; fp8 caches: 8 waves,
+// tiles copied into per-wave staging and widened to bf16 in LDS.
 constexpr int kQblockWaveRows = 32;
 // Decode workgroup: 4 waves, one workgroup per CU (its LDS use keeps a
 // second one out), so one wave per SIMD.  With two waves on a SIMD the
@@ -168,8 +168,6 @@ hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, 
 hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st);
 hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
                        bool with_prefill, hipStream_t st);
-hipError_t launch_prefill(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
-                          hipStream_t st, bool gather = false);
 hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
                          hipStream_t st, bool gather = false);
 

@@ -127,10 +127,11 @@ __device__ __forceinline__ void wait_lds() {
 // 2; period t loads V of tile t + 1 and K of tile t + 3), so that one
 // workgroup's barrier waits and start-up run under the other's products.
 //
-// FP8 (e4m3 caches; W = 8, d = 128): the copies land in a staging area
-// private to each wave (3 stages of its 8 K rows and 8 V rows, 2 KB a
-// stage), and the wave itself widens its rows to bf16 into the K and V
-// rings (3 stages each), exactly: every e4m3 value is a bf16 value, and the
+// FP8 (e4m3 caches; W = 8, d = 128 or 64): the copies land in a staging
+// area private to each wave (3 stages of its 8 K rows and 8 V rows, 2 KB a
+// stage; with d = 64 1 KB, K and V rows in one copy instruction, lanes
+// 0..31 K and 32..63 V, and one read and widening), and the wave itself
+// widens its rows to bf16 into the K and V rings (3 stages each), exactly: every e4m3 value is a bf16 value, and the
 // per-tensor scales act on the scores (k_scale, folded into c) and on the
 // output (v_scale).  Period t widens tile t + 2, which landed during
 // periods t - 2 and t - 1, and copies tile t + 4 into the staging stage
@@ -156,14 +157,18 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   constexpr int SROW = kTile / W;                  // rows per wave and tile
   constexpr int SCH = D / 16;                      // 16-byte chunks per fp8 row
   constexpr int SSTG = 3;                          // staging stages
-  constexpr int SWB = 2 * 1024;                    // staging bytes per wave and stage
+  // d = 64: a wave's K and V rows of a tile are one 16-byte copy per lane
+  // (lanes 0..31 K, 32..63 V); d = 128: one copy per tensor
+  constexpr bool KV1 = FP8 && SROW * SCH == 32;
+  constexpr int SWB = KV1 ? 1024 : 2 * 1024;       // staging bytes per wave and stage
+  constexpr int NCP = KV1 ? 1 : 2;                 // copy instructions per wave and tile
   constexpr int SBYTES = FP8 ? SSTG * W * SWB : 0;
   constexpr int SBASE = KSTG * TB;                 // staging after the K ring
   constexpr int VBASE = KSTG * TB + SBYTES;        // V ring after the K ring (and the staging)
   static_assert(kQblockWaveRows == 32 && (W == 8 || W == 4), "8 or 4 waves x 32 rows");
   static_assert(NLD >= 1 && NLD * RPI * W == kTile, "tile loads");
   static_assert(RPI <= 16, "one instruction stays inside one 16-key block");
-  static_assert(!FP8 || (W == 8 && D == 128 && SROW * SCH == 64), "fp8: 8 waves, d = 128");
+  static_assert(!FP8 || (W == 8 && (SROW * SCH == 64 || SROW * SCH == 32)), "fp8: 8 waves, d = 64 or 128");
   static_assert(((KSTG + VSTG) * TB + SBYTES) * (8 / W) <= 160 * 1024, "workgroups per CU fit the LDS");
   static_assert(kQblockWaveRows * W * RB <= KSTG * TB + SBYTES, "output staging below the V ring");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[(KSTG + VSTG) * TB + SBYTES];
@@ -230,9 +235,11 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   auto fV = [](int r) { return (CPR / 4) * (r & 3) + (CPR / 8) * ((r >> 2) & 1); };
   int koff[NLD], voff[NLD];
   if constexpr (FP8) {
-    // lane i copies chunk i % SCH of row wrow + i / SCH (16 fp8 values)
-    koff[0] = (lane / SCH) * (int)a.kg.slot + 16 * (lane % SCH);
-    voff[0] = (lane / SCH) * (int)a.vg.slot + 16 * (lane % SCH);
+    // lane i copies chunk i % SCH of row wrow + i / SCH (16 fp8 values);
+    // d = 64: lane i of 32..63 the same chunk of V as lane i - 32 of K
+    const int l = KV1 ? (lane & 31) : lane;
+    koff[0] = (l / SCH) * (int)a.kg.slot + 16 * (l % SCH);
+    voff[0] = (l / SCH) * (int)a.vg.slot + 16 * (l % SCH);
   } else {
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
@@ -306,12 +313,17 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   auto stg = [&](int t) { return stg_s(t % SSTG); };
   auto issue8_k_s = [&](int sg) { dma16(kp + koff[0], lds_addr(lds + stg_s(sg))); };
   auto issue8_v_s = [&](int sg) { dma16(vp + voff[0], lds_addr(lds + stg_s(sg) + 1024)); };
-  auto issue8_k = [&](int t) { issue8_k_s(t % SSTG); };
-  auto issue8_v = [&](int t) { issue8_v_s(t % SSTG); };
+  auto issue8_kv_s = [&](int sg) {   // d = 64: K rows to bytes 0..511, V rows to 512..1023
+    dma16(lane < 32 ? kp + koff[0] : vp + voff[0], lds_addr(lds + stg_s(sg)));
+  };
   auto issue8 = [&](int t) {
     issue_prep(t);
-    issue8_k(t);
-    issue8_v(t);
+    if constexpr (KV1) {
+      issue8_kv_s(t % SSTG);
+    } else {
+      issue8_k_s(t % SSTG);
+      issue8_v_s(t % SSTG);
+    }
   };
   // fp8: widen the wave's staged rows of tile t to bf16 in the K and V
   // rings, at the places the bf16 copies would have put them (its copies
@@ -319,9 +331,10 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   // c8 = i % SCH, i.e. bf16 chunks 2 c8 and 2 c8 + 1, whose swizzled
   // slots differ in bit 0 (both swizzles keep it or flip it for the pair).
   // read8 fetches the 16 codes, put8_k / put8_v write the bf16 values.
-  const int r8 = wrow + lane / SCH;
-  const int w8k = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fK(r8));
-  const int w8v = r8 * RB + 16 * ((2 * (lane % SCH)) ^ fV(r8));
+  const int l8 = KV1 ? (lane & 31) : lane;
+  const int r8 = wrow + l8 / SCH;
+  const int w8k = r8 * RB + 16 * ((2 * (l8 % SCH)) ^ fK(r8));
+  const int w8v = r8 * RB + 16 * ((2 * (l8 % SCH)) ^ fV(r8));
   // (The _s forms take the ring and staging stages of tile t as given.)
   auto read8_s = [&](int sg, int tensor) -> u32x4 {
     return *(const u32x4*)(lds + stg_s(sg) + 1024 * tensor + 16 * lane);
@@ -344,8 +357,28 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     *(bf16x8*)(base + w8v) = lo;
     *(bf16x8*)(base + (w8v ^ 16)) = hi;
   };
-  auto widen8_k = [&](int t) { put8_k_s(kst(t), read8_s(t % SSTG, 0)); };
-  auto widen8_v = [&](int t) { put8_v_s(vst(t), t, read8_s(t % SSTG, 1)); };
+  // d = 64: lanes 0..31 widen K rows, 32..63 V rows, from one read
+  auto put8_kv_s = [&](int ksg, int vsg, int t, const u32x4& raw) {
+    bf16x8 lo, hi;
+    fp8x16_to_bf16(raw, lo, hi);
+    const bool isv = lane >= 32;
+    if (isv && t * kTile + r8 >= kv_len) {   // past the end: zeros (the bytes may be NaN codes)
+      lo = bf16x8{};
+      hi = bf16x8{};
+    }
+    const int off = isv ? VBASE + vsg * TB : ksg * TB;
+    const int w8 = isv ? w8v : w8k;
+    *(bf16x8*)(lds + off + w8) = lo;
+    *(bf16x8*)(lds + off + (w8 ^ 16)) = hi;
+  };
+  auto widen8 = [&](int t) {   // tile t's copies have landed
+    if constexpr (KV1) {
+      put8_kv_s(kst(t), vst(t), t, read8_s(t % SSTG, 0));
+    } else {
+      put8_k_s(kst(t), read8_s(t % SSTG, 0));
+      put8_v_s(vst(t), t, read8_s(t % SSTG, 1));
+    }
+  };
   // V rows at or past kv_len (last tile only) may hold anything, NaN
   // included, and would poison P V even with zero weights: each lane zeroes
   // the chunks it loaded, after its own loads have landed.
@@ -481,7 +514,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   // LDS operands are read kAhead products ahead into a small register ring;
   // a scheduling fence after every product keeps each step's work in place.
   constexpr int kAhead = 4;
-  static_assert(!FP8 || 14 < NS, "fp8: widening and copies between the score products");
+  static_assert(!FP8 || 14 < NS + NP, "fp8: widening and copies between the products");
   static_assert(kSplit ? 3 + 4 * NLD <= NS + NP : 2 + 3 * ND <= NS + 1,
                 "tile loads fit between the products");
   auto period = [&](int t, auto full_tag, auto stage_tag) {
@@ -525,18 +558,26 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
         // still fly), then copy tile t + 4 into the staging stage of t + 1
         if (t + 2 < ntiles) {
           if (i == 0) {
-            if (t + 3 < ntiles) wait_vm<2>();
+            if (t + 3 < ntiles) wait_vm<NCP>();
             else wait_vm<0>();
             raw8 = read8_s(sst_at(2), 0);
           }
-          if (i == 3) put8_k_s(kst_at(2), raw8);
-          if (i == 6) raw8 = read8_s(sst_at(2), 1);
-          if (i == 9) put8_v_s(vst_at(2), t + 2, raw8);
+          if constexpr (KV1) {
+            if (i == 3) put8_kv_s(kst_at(2), vst_at(2), t + 2, raw8);
+          } else {
+            if (i == 3) put8_k_s(kst_at(2), raw8);
+            if (i == 6) raw8 = read8_s(sst_at(2), 1);
+            if (i == 9) put8_v_s(vst_at(2), t + 2, raw8);
+          }
         }
         if (t + 4 < ntiles) {
           if (i == 11) issue_prep(t + 4);
-          if (i == 12) issue8_k_s(sst_at(4));
-          if (i == 14) issue8_v_s(sst_at(4));
+          if constexpr (KV1) {
+            if (i == 12) issue8_kv_s(sst_at(4));
+          } else {
+            if (i == 12) issue8_k_s(sst_at(4));
+            if (i == 14) issue8_v_s(sst_at(4));
+          }
         }
       }
       if constexpr (kFullP && !kSplit && !FP8) {
@@ -581,16 +622,20 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     const int64_t kd0 = (int64_t)seq * a.d_seq + (int64_t)g * a.d_head;
     if constexpr (FP8) {
       // each wave stores the raw codes of its staged rows
-      const int r = wrow + lane / SCH, c8 = lane % SCH;
+      const int r = wrow + l8 / SCH, c8 = l8 % SCH;
       for (int t = 0; t < ntiles; ++t) {
         issue8(t);
         wait_vm<0>();
-        const u32x4 kw = *(const u32x4*)(lds + stg(t) + 16 * lane);
-        const u32x4 vw = *(const u32x4*)(lds + stg(t) + 1024 + 16 * lane);
         const int key = t * kTile + r;
-        if (key < kv_len) {
-          *(u32x4*)(a.kd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = kw;
-          *(u32x4*)(a.vd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = vw;
+        const u32x4 w0 = *(const u32x4*)(lds + stg(t) + 16 * lane);
+        if constexpr (KV1) {   // lanes 0..31 hold K codes, 32..63 V codes
+          if (key < kv_len) *(u32x4*)((lane < 32 ? a.kd : a.vd) + kd0 + (int64_t)key * a.d_tok + 16 * c8) = w0;
+        } else {
+          const u32x4 vw = *(const u32x4*)(lds + stg(t) + 1024 + 16 * lane);
+          if (key < kv_len) {
+            *(u32x4*)(a.kd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = w0;
+            *(u32x4*)(a.vd + kd0 + (int64_t)key * a.d_tok + 16 * c8) = vw;
+          }
         }
       }
       return;
@@ -633,16 +678,14 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
     issue8(0);
     if (ntiles > 1) issue8(1);
     if (ntiles > 2) issue8(2);
-    if (ntiles > 2) wait_vm<4>();
-    else if (ntiles == 2) wait_vm<2>();
+    if (ntiles > 2) wait_vm<2 * NCP>();
+    else if (ntiles == 2) wait_vm<NCP>();
     else wait_vm<0>();
-    widen8_k(0);
-    widen8_v(0);
+    widen8(0);
     if (ntiles > 1) {
-      if (ntiles > 2) wait_vm<2>();
+      if (ntiles > 2) wait_vm<NCP>();
       else wait_vm<0>();
-      widen8_k(1);
-      widen8_v(1);
+      widen8(1);
     }
     wait_lds();
     if (ntiles > 3) issue8(3);
@@ -724,10 +767,9 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   auto load_next = [&](int t) {   // period t's loads, outside the products
     if constexpr (FP8) {
       if (t + 2 < ntiles) {
-        if (t + 3 < ntiles) wait_vm<2>();
+        if (t + 3 < ntiles) wait_vm<NCP>();
         else wait_vm<0>();
-        widen8_k(t + 2);
-        widen8_v(t + 2);
+        widen8(t + 2);
       }
       if (t + 4 < ntiles) issue8(t + 4);
     } else if constexpr (!kSplit) {
@@ -819,9 +861,16 @@ hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim,
   const int W = p.block_m / kQblockWaveRows;
   const dim3 grid((unsigned)blocks), block(64 * W);
   if (fp8) {
-    if (W != 8 || head_dim != 128) return hipErrorInvalidValue;
-    if (gather) qblock_kernel<128, 8, true, true><<<grid, block, 0, st>>>(a, p);
-    else qblock_kernel<128, 8, true, false><<<grid, block, 0, st>>>(a, p);
+    if (W != 8) return hipErrorInvalidValue;
+    if (head_dim == 128) {
+      if (gather) qblock_kernel<128, 8, true, true><<<grid, block, 0, st>>>(a, p);
+      else qblock_kernel<128, 8, true, false><<<grid, block, 0, st>>>(a, p);
+    } else if (head_dim == 64) {
+      if (gather) qblock_kernel<64, 8, true, true><<<grid, block, 0, st>>>(a, p);
+      else qblock_kernel<64, 8, true, false><<<grid, block, 0, st>>>(a, p);
+    } else {
+      return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   }
 #define PA_QB(DD, WW, GG) qblock_kernel<DD, WW, false, GG><<<grid, block, 0, st>>>(a, p)

@@ -281,11 +281,11 @@ def test_plan_prefill_grid_bounds_the_q_blocks():
     need = sum(-(-q // 64) for q in qs)
     assert p["prefill_units"] >= need * 8
     assert p["prefill_grid"][0] == p["prefill_units"]   # one workgroup per (Q-block, kv head)
-    # fp8 caches: the 8-wave kernel for d = 128, the register-staged one (128 rows) for d = 64
+    # fp8 caches: the 8-wave kernel (its staging needs 8 waves) for d = 128 and 64
     pf = plan(cfg(32, 8, 128, 16, pa.PA_DTYPE_FP8_E4M3), cus=256, T=6589, S=4, MB=188)
     assert pf["block_m"] == 256 and pf["block_q"] == 64
     pf64 = plan(cfg(32, 8, 64, 16, pa.PA_DTYPE_FP8_E4M3), cus=256, T=6589, S=4, MB=188)
-    assert pf64["block_m"] == 128 and pf64["block_q"] == 32
+    assert pf64["block_m"] == 256 and pf64["block_q"] == 64
     p1 = plan(cfg(), T=1, S=1, MB=4)
     assert p1["prefill_launch"] == 0
 
