@@ -6,9 +6,10 @@ loads for a batch and stores the bytes each loader reads; every key a row
 attends to must arrive exactly as the oracle's independent block-table walk
 copies it.  Sequences with query length 1 go through the decode kernel's
 loader (its block-id window, 16-key block addressing and head units),
-those with query length >= 2 through the Q-block kernel of the cache dtype
-(bf16: the copies straight into the LDS ring and its swizzles; fp8: the
-register-staged loads); sequences with no query rows are read by nothing.
+those with query length >= 2 through the Q-block kernel's loader (bf16:
+the copies straight into the LDS ring and its swizzles; fp8: the copies
+into each wave's staging area, then the widening into the same ring);
+sequences with no query rows are read by nothing.
 """
 import numpy as np
 import pytest
