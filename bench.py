@@ -32,6 +32,10 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2516.6
 METRIC = "paged-attn decode HBM GB/s & prefill TFLOP/s (% of MI355X roofline), µs/batch"
+# Parity tolerances against the fp64 oracle (max / mean abs error of the
+# bf16 output): bf16 caches, fp8 e4m3 caches.
+TOL_BF16 = (2e-2, 2e-3)
+TOL_FP8 = (5e-2, 5e-3)
 
 
 def alg_bytes(w):
@@ -76,23 +80,36 @@ def kernel_source_hash(kernel):
     return h.hexdigest()
 
 
-def measured_traffic(kernel, workload):
-    """HBM bytes per launch of `kernel` on `workload` from the rocprofv3
-    FETCH_SIZE / WRITE_SIZE runs recorded in profiles/traffic.json (each
-    counter scaled by what it reads for a plain device copy of known size),
-    or None when no record exists or the kernel's sources have changed since
-    the counters were taken."""
+def rocprof_record(key, workload):
+    """The rocprofv3 record of kernel `key` ("decode_kernel", "qblock_kernel",
+    "@fp8" for fp8 caches) on `workload` in profiles/traffic.json: HBM bytes
+    per launch from the FETCH_SIZE / WRITE_SIZE runs (each counter scaled by
+    what it reads for a plain device copy of known size), the trace's
+    average duration and, for the Q-block kernel, the matrix-core busy
+    fraction.  None when no record exists or the kernel's sources have
+    changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
             rec = json.load(fh)
-        k = rec["kernels"][kernel]
+        k = rec["kernels"][key]
     except (OSError, KeyError, ValueError):
         return None
-    if k.get("workload") != workload or k.get("source_sha256") != kernel_source_hash(kernel):
+    if k.get("workload") != workload or k.get("source_sha256") != kernel_source_hash(key.split("@")[0]):
         return None
     cal = rec["calibration"]
-    return (k["fetch_kib"] * 1024 * cal["fetch_scale"] + k["write_kib"] * 1024 * cal["write_scale"])
+    out = {"kernel": key.split("@")[0],
+           "dram_bytes": k["fetch_kib"] * 1024 * cal["fetch_scale"] + k["write_kib"] * 1024 * cal["write_scale"],
+           "avg_us_trace": k.get("avg_us_trace")}
+    if "mfma_busy_frac" in k:
+        out["mfma_busy"] = k["mfma_busy_frac"]
+    return out
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` (rocprof_record), or None."""
+    r = rocprof_record(kernel, workload)
+    return r["dram_bytes"] if r else None
 
 
 def make_attention(w, profile=False, no_split_kv=False):
@@ -218,12 +235,18 @@ def sampled_error(w, out, nrows=256, seed=0):
         return oracle.rows(wc.q, wc.k_cache, wc.v_cache, wc.block_table, wc.seq_lens,
                            wc.query_start_loc, wc.scale, ch, k_scale=wc.k_scale, v_scale=wc.v_scale)
 
+    t_or = time.perf_counter()
     with cf.ThreadPoolExecutor(max_workers=len(chunks)) as ex:
         ref = np.concatenate(list(ex.map(one, chunks)), 0)
+    t_or = time.perf_counter() - t_or
     got = out.cpu()
     g = np.stack([got[t, h].double().numpy() for t, h in rows])
     err = np.abs(g - ref)
-    return {"rows": len(rows), "max_abs_err": float(err.max()), "mean_abs_err": float(err.mean())}
+    tol = TOL_FP8 if w.kv_fp8 else TOL_BF16
+    mx, mn = float(err.max()), float(err.mean())
+    return {"rows": len(rows), "max_abs_err": mx, "mean_abs_err": mn,
+            "tolerance": {"max": tol[0], "mean": tol[1]}, "pass": bool(mx <= tol[0] and mn <= tol[1]),
+            "oracle_s": t_or, "oracle_threads": len(chunks)}
 
 
 def measure(k, steps, warmup, block_size=None, with_error=True, kv_dtype=None):
@@ -268,6 +291,13 @@ def measure(k, steps, warmup, block_size=None, with_error=True, kv_dtype=None):
     }
     if err:
         res["error_vs_oracle"] = err
+    # the rocprofv3 record of the batch's dominant kernel, where one was taken
+    rkey = {2: "decode_kernel", 3: "qblock_kernel", 5: "decode_kernel"}.get(k) if block_size is None else None
+    if rkey is not None:
+        wname = W.CONFIG_NAMES[k] + (" (fp8 e4m3 caches)" if kv_dtype is not None and k == 3 else "")
+        rp = rocprof_record(rkey + ("@fp8" if w.kv_fp8 else ""), wname)
+        if rp is not None:
+            res["rocprof"] = rp
     res["frac_hbm"] = res["GBps"] / HBM_PEAK_GBS
     res["frac_mfma"] = res["TFLOPs"] / BF16_PEAK_TFLOPS
     db, pf = decode_bytes(w), prefill_flops(w)
@@ -506,8 +536,8 @@ def main():
               f"({100 * r['frac_hbm']:.1f}% HBM), {r['TFLOPs']:.1f} TFLOP/s "
               f"({100 * r['frac_mfma']:.1f}% MFMA), kernels {r['per_kernel_us']}, "
               f"error vs oracle max {e.get('max_abs_err', float('nan')):.2e} "
-              f"mean {e.get('mean_abs_err', float('nan')):.2e} ({e.get('rows', 0)} rows)", file=sys.stderr,
-              flush=True)
+              f"mean {e.get('mean_abs_err', float('nan')):.2e} ({e.get('rows', 0)} rows, "
+              f"{'pass' if e.get('pass') else 'FAIL'})", file=sys.stderr, flush=True)
 
     headline_w, headline = measure(args.config, args.steps, args.warmup)
     configs[args.config] = headline
@@ -540,7 +570,7 @@ def main():
             _, r = measure(k, args.steps, args.warmup, kv_dtype="fp8")
             kv_fp8[f"config{k}_fp8"] = {kk: r[kk] for kk in (
                 "us_per_batch", "us_median", "GBps", "frac_hbm", "TFLOPs", "frac_mfma",
-                "per_kernel_us", "error_vs_oracle") if kk in r}
+                "per_kernel_us", "error_vs_oracle", "rocprof") if kk in r}
             for kk in ("prefill_kernel_TFLOPs", "decode_kernel_GBps"):
                 if kk in r:
                     kv_fp8[f"config{k}_fp8"][kk] = r[kk]

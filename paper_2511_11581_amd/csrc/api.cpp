@@ -455,21 +455,28 @@ hipError_t flush_ring(pa_handle* h, int kind) {
   return hipSuccess;
 }
 
-// Launch through `fn`, bracketed by an event pair when profiling.
+// Launch through `fn(tm)`.  When profiling, tm carries the next event pair
+// of the kernel kind's ring: the launcher has the runtime stamp the
+// kernel's own start and end into it; a launcher that finds nothing to
+// launch leaves it unused, and the pair is then recorded back to back (a
+// zero duration).
 template <class F>
 hipError_t timed_launch(pa_handle* h, int kind, hipStream_t st, F&& fn) {
-  if (!h->profile) return fn();
+  if (!h->profile) return fn(nullptr);
   pa_event_ring& r = h->ring[kind];
   if (r.used == kRingCap) {
     hipError_t e = flush_ring(h, kind);
     if (e != hipSuccess) return e;
   }
-  hipError_t e = hipEventRecord(r.start[r.used], st);
+  pa::KernelTiming tm{r.start[r.used], r.stop[r.used], false};
+  hipError_t e = fn(&tm);
   if (e != hipSuccess) return e;
-  e = fn();
-  if (e != hipSuccess) return e;
-  e = hipEventRecord(r.stop[r.used], st);
-  if (e != hipSuccess) return e;
+  if (!tm.used) {
+    e = hipEventRecord(tm.start, st);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(tm.stop, st);
+    if (e != hipSuccess) return e;
+  }
   r.used += 1;
   return hipSuccess;
 }
@@ -782,28 +789,31 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
   if (fused) {
     dp.fused = 1;
     e = timed_launch(h, PA_KERNEL_DECODE, st,
-                     [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+                     [&](pa::KernelTiming* tm) { return pa::launch_decode(a, dp, c.head_dim, fp8, st, false, tm); });
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     if (p.merge_launch) {
-      e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+      e = timed_launch(h, PA_KERNEL_MERGE, st,
+                       [&](pa::KernelTiming* tm) { return pa::launch_merge(a, dp, c.head_dim, st, tm); });
       if (e != hipSuccess) return hip_fail(e, "merge launch");
     }
     return PA_OK;
   }
-  e = timed_launch(h, PA_KERNEL_PLAN, st, [&] { return pa::launch_plan(a, dp, pp, run_qblock, st); });
+  e = timed_launch(h, PA_KERNEL_PLAN, st,
+                   [&](pa::KernelTiming* tm) { return pa::launch_plan(a, dp, pp, run_qblock, st, tm); });
   if (e != hipSuccess) return hip_fail(e, "plan launch");
   if (run_decode) {
     e = timed_launch(h, PA_KERNEL_DECODE, st,
-                     [&] { return pa::launch_decode(a, dp, c.head_dim, fp8, st); });
+                     [&](pa::KernelTiming* tm) { return pa::launch_decode(a, dp, c.head_dim, fp8, st, false, tm); });
     if (e != hipSuccess) return hip_fail(e, "decode launch");
     if (p.merge_launch) {
-      e = timed_launch(h, PA_KERNEL_MERGE, st, [&] { return pa::launch_merge(a, dp, c.head_dim, st); });
+      e = timed_launch(h, PA_KERNEL_MERGE, st,
+                       [&](pa::KernelTiming* tm) { return pa::launch_merge(a, dp, c.head_dim, st, tm); });
       if (e != hipSuccess) return hip_fail(e, "merge launch");
     }
   }
   if (run_qblock) {
     e = timed_launch(h, PA_KERNEL_PREFILL, st,
-                     [&] { return pa::launch_qblock(a, pp, c.head_dim, fp8, st); });
+                     [&](pa::KernelTiming* tm) { return pa::launch_qblock(a, pp, c.head_dim, fp8, st, false, tm); });
     if (e != hipSuccess) return hip_fail(e, "prefill launch");
   }
   return PA_OK;

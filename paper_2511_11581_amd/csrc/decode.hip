@@ -749,17 +749,17 @@ __global__ __launch_bounds__(256) void merge_kernel(BatchArgs a, DecodePlan p) {
 
 template <bool GATHER>
 hipError_t launch_decode_t(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
-                           hipStream_t st) {
+                           hipStream_t st, KernelTiming* tm) {
   const dim3 grid((unsigned)((p.workers + kDecodeWaves - 1) / kDecodeWaves)), block(64 * kDecodeWaves);
   const int hu = p.unit_heads;
-  if (head_dim == 128 && !fp8 && hu == 1) decode_kernel<128, false, 1, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 128 && fp8 && hu == 2) decode_kernel<128, true, 2, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 128 && fp8 && hu == 1) decode_kernel<128, true, 1, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && !fp8 && hu == 2) decode_kernel<64, false, 2, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && !fp8 && hu == 1) decode_kernel<64, false, 1, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 4) decode_kernel<64, true, 4, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 2) decode_kernel<64, true, 2, GATHER><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64 && fp8 && hu == 1) decode_kernel<64, true, 1, GATHER><<<grid, block, 0, st>>>(a, p);
+  if (head_dim == 128 && !fp8 && hu == 1) launch_k(decode_kernel<128, false, 1, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 128 && fp8 && hu == 2) launch_k(decode_kernel<128, true, 2, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 128 && fp8 && hu == 1) launch_k(decode_kernel<128, true, 1, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 64 && !fp8 && hu == 2) launch_k(decode_kernel<64, false, 2, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 64 && !fp8 && hu == 1) launch_k(decode_kernel<64, false, 1, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 64 && fp8 && hu == 4) launch_k(decode_kernel<64, true, 4, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 64 && fp8 && hu == 2) launch_k(decode_kernel<64, true, 2, GATHER>, grid, block, st, tm, a, p);
+  else if (head_dim == 64 && fp8 && hu == 1) launch_k(decode_kernel<64, true, 1, GATHER>, grid, block, st, tm, a, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -767,15 +767,16 @@ hipError_t launch_decode_t(const BatchArgs& a, const DecodePlan& p, int head_dim
 }  // namespace
 
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
-                         hipStream_t st, bool gather) {
-  return gather ? launch_decode_t<true>(a, p, head_dim, fp8, st)
-                : launch_decode_t<false>(a, p, head_dim, fp8, st);
+                         hipStream_t st, bool gather, KernelTiming* tm) {
+  return gather ? launch_decode_t<true>(a, p, head_dim, fp8, st, tm)
+                : launch_decode_t<false>(a, p, head_dim, fp8, st, tm);
 }
 
-hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st) {
+hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st,
+                        KernelTiming* tm) {
   const dim3 grid(a.num_seqs, (a.group + 3) / 4, a.num_kv_heads), block(256);
-  if (head_dim == 128) merge_kernel<128><<<grid, block, 0, st>>>(a, p);
-  else if (head_dim == 64) merge_kernel<64><<<grid, block, 0, st>>>(a, p);
+  if (head_dim == 128) launch_k(merge_kernel<128>, grid, block, st, tm, a, p);
+  else if (head_dim == 64) launch_k(merge_kernel<64>, grid, block, st, tm, a, p);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

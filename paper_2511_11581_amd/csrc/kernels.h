@@ -1,6 +1,7 @@
 // Argument blocks and launchers shared by the host API and the HIP kernels.
 // All strides are in bytes unless named otherwise.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -160,16 +161,39 @@ struct ValidateArgs {
   uint32_t* error_word;
 };
 
+// Start and end stamps of one launch (PA_FLAG_PROFILE).  A launcher given
+// one launches through hipExtLaunchKernel, so that the runtime stamps the
+// kernel's dispatch itself: the duration is the kernel's own, without the
+// dispatch latency that event markers recorded around the launch add.
+// `used` tells whether a kernel was launched (an empty batch launches none).
+struct KernelTiming {
+  hipEvent_t start;
+  hipEvent_t stop;
+  bool used;
+};
+
+// Launch `kernel` on `st` (no dynamic LDS), timed into *tm when tm is given.
+template <typename F, typename... Args>
+inline void launch_k(F kernel, dim3 grid, dim3 block, hipStream_t st, KernelTiming* tm, Args... args) {
+  if (tm) {
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, tm->start, tm->stop, 0, args...);
+    tm->used = true;
+  } else {
+    kernel<<<grid, block, 0, st>>>(args...);
+  }
+}
+
 // Launchers (return hipGetLastError() of the launch).  With gather = true
 // the attention kernels run their K/V loaders only and store the loaded
 // bytes of every valid key into a.kd / a.vd (pa_debug_gather).
 hipError_t launch_decode(const BatchArgs& a, const DecodePlan& p, int head_dim, bool fp8,
-                         hipStream_t st, bool gather = false);
-hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st);
+                         hipStream_t st, bool gather = false, KernelTiming* tm = nullptr);
+hipError_t launch_merge(const BatchArgs& a, const DecodePlan& p, int head_dim, hipStream_t st,
+                        KernelTiming* tm = nullptr);
 hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
-                       bool with_prefill, hipStream_t st);
+                       bool with_prefill, hipStream_t st, KernelTiming* tm = nullptr);
 hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
-                         hipStream_t st, bool gather = false);
+                         hipStream_t st, bool gather = false, KernelTiming* tm = nullptr);
 
 // KV-cache write (csrc/cache.hip).
 struct CacheWriteArgs {

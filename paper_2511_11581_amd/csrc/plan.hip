@@ -150,9 +150,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
 }  // namespace
 
 hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
-                       bool with_prefill, hipStream_t st) {
+                       bool with_prefill, hipStream_t st, KernelTiming* tm) {
   if (a.num_seqs <= 0) return hipSuccess;
-  plan_kernel<<<dim3(1), dim3(kPlanThreads), 0, st>>>(a, dp, pp, with_prefill ? 1 : 0);
+  launch_k(plan_kernel, dim3(1), dim3(kPlanThreads), st, tm, a, dp, pp, with_prefill ? 1 : 0);
   return hipGetLastError();
 }
 

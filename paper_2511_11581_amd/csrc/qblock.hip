@@ -855,7 +855,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
 }  // namespace
 
 hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim, bool fp8,
-                         hipStream_t st, bool gather) {
+                         hipStream_t st, bool gather, KernelTiming* tm) {
   const int64_t blocks = (int64_t)p.work_items * a.num_kv_heads;
   if (blocks <= 0) return hipSuccess;
   const int W = p.block_m / kQblockWaveRows;
@@ -863,17 +863,17 @@ hipError_t launch_qblock(const BatchArgs& a, const PrefillPlan& p, int head_dim,
   if (fp8) {
     if (W != 8) return hipErrorInvalidValue;
     if (head_dim == 128) {
-      if (gather) qblock_kernel<128, 8, true, true><<<grid, block, 0, st>>>(a, p);
-      else qblock_kernel<128, 8, true, false><<<grid, block, 0, st>>>(a, p);
+      if (gather) launch_k(qblock_kernel<128, 8, true, true>, grid, block, st, tm, a, p);
+      else launch_k(qblock_kernel<128, 8, true, false>, grid, block, st, tm, a, p);
     } else if (head_dim == 64) {
-      if (gather) qblock_kernel<64, 8, true, true><<<grid, block, 0, st>>>(a, p);
-      else qblock_kernel<64, 8, true, false><<<grid, block, 0, st>>>(a, p);
+      if (gather) launch_k(qblock_kernel<64, 8, true, true>, grid, block, st, tm, a, p);
+      else launch_k(qblock_kernel<64, 8, true, false>, grid, block, st, tm, a, p);
     } else {
       return hipErrorInvalidValue;
     }
     return hipGetLastError();
   }
-#define PA_QB(DD, WW, GG) qblock_kernel<DD, WW, false, GG><<<grid, block, 0, st>>>(a, p)
+#define PA_QB(DD, WW, GG) launch_k(qblock_kernel<DD, WW, false, GG>, grid, block, st, tm, a, p)
   if (W == 8) {
     if (head_dim == 128) gather ? PA_QB(128, 8, true) : PA_QB(128, 8, false);
     else if (head_dim == 64) gather ? PA_QB(64, 8, true) : PA_QB(64, 8, false);
