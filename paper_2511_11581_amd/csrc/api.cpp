@@ -33,14 +33,13 @@ struct pa_event_ring {
   int used = 0;
 };
 
-// Launch-planner knob: the fewest decode steps a worker is given when the
-// batch has enough work (PA_DECODE_MIN_STEPS, 1..4096), read when a handle
-// is created.
+// Launch-planner knobs, read from the environment when a handle is created
+// (defaults: the offline tuning's rules below).
 struct pa_tunables {
-  int decode_min_steps;
-  int decode_whole_steps;
-  int64_t unify_max_keys;
-  int qblock_rows;   // 0: chosen from the batch shape; else 128 or 256 (bf16 caches)
+  int decode_min_steps;    // fewest decode steps per active worker group (PA_DECODE_MIN_STEPS, 1..4096)
+  int decode_whole_steps;  // whole pairs per worker up to this many steps (PA_DECODE_WHOLE_STEPS; 0: off)
+  int64_t unify_max_keys;  // hinted mixed batches as Q-blocks only up to this many keys (PA_UNIFY_MAX_KEYS)
+  int qblock_rows;         // 0: chosen from the batch shape; else 128 or 256 (PA_QBLOCK_ROWS, bf16 caches)
 };
 
 struct pa_handle {
@@ -143,7 +142,6 @@ pa_status check_config(const pa_config* c) {
   return PA_OK;
 }
 
-// Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) + (#sequences with q_i >= 2).
 // Q-block slots of the prefill grid: sum_i ceil(q_i / BQ) <= ceil(T / BQ) +
 // (#sequences with q_i >= qmin), qmin = 2 (1 when single-token rows also
 // take Q-blocks).
@@ -156,8 +154,6 @@ int decode_step_keys(const pa_config& c) {
   const int eb = c.kv_dtype == PA_DTYPE_FP8_E4M3 ? 1 : 2;
   return pa::decode_step_keys(decode_unit_heads(c) * c.head_dim * eb, eb);
 }
-
-int64_t prefill_items(int64_t T, int64_t S, int64_t bq, int qmin);
 
 // Rows per Q-block.  fp8 caches: 256 (the bf16 kernel's 8-wave shape,
 // widening its copies to bf16 in LDS).  bf16 caches: 256
