@@ -6,10 +6,11 @@ passed through.  Every attention step runs in the library's HIP kernels;
 there is no fallback: if ``libpa.so`` is missing or fails to load, the first
 call raises.
 
-The functions keep the C names: ``pa_workspace_bytes``, ``pa_create``,
-``pa_forward``, ``pa_debug_gather``, ``pa_plan``, ``pa_destroy``,
-``pa_last_error``.  ``PagedAttention`` bundles a handle with a
-workspace allocated through torch.
+The functions keep the C names (``EXPORTS`` lists every entry point of the
+header, from ``pa_workspace_bytes`` and ``pa_create`` to ``pa_forward``,
+``pa_forward_hinted``, ``pa_forward_noalloc`` and ``pa_cache_write``).
+``PagedAttention`` bundles a handle with a workspace allocated through
+torch.
 """
 from __future__ import annotations
 
