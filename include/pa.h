@@ -78,9 +78,12 @@ typedef struct pa_tensor {
  * returns PA_ERR_DEVICE on a violation.  Debug only. */
 #define PA_FLAG_VALIDATE 1u
 
-/* Record a pair of HIP events around every kernel launch of pa_forward, on
- * the caller's stream, so that pa_profile_read can report per-kernel
- * durations.  Adds two event records per launch; off by default. */
+/* Time every kernel launch of pa_forward so that pa_profile_read can report
+ * per-kernel durations: each kernel is launched through hipExtLaunchKernel
+ * with a pair of the handle's HIP events, which the runtime stamps at the
+ * kernel's own dispatch start and end (the timestamps a rocprofv3 kernel
+ * trace reports).  Off by default; not meant for calls under HIP-graph
+ * capture. */
 #define PA_FLAG_PROFILE 2u
 
 /* Ablation only (the middle rung of the optimisation ladder of Sec. 7):
