@@ -91,21 +91,19 @@ struct Piece {
   int head, tail;      // the pair starts before / continues after this worker
 };
 
-// The log-sum-exp merge of one query head's pieces (Sec. 4.5), by one wave:
-// M = max_k m_k, out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k, lanes
-// over d.  Piece k sits with worker w0 + k (slot 1 for the pair's first
-// worker, slot 0 for the others), head hu of its unit, query head hh of the
-// group; the result goes to row `tok`, query head g G + hh.  Up to 8 pieces
-// are read in one round (every lane reads their (m, l)); more are read 64
-// (m, l) at a time, one per lane, their weights reaching the lanes by
-// readlane.
-template <int D>
-__device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePlan& p, int w0, int n,
-                                             int hu, int hh, int tok, int g) {
+// The log-sum-exp merge of one query head's n pieces (Sec. 4.5), by one
+// wave: M = max_k m_k, out = sum_k 2^(m_k - M) acc_k / sum_k 2^(m_k - M) l_k,
+// lanes over d; the result goes to row `tok`, query head g G + hh.  Piece k
+// is read through ml_of(k) (its (m, l)) and po_of(k) (its d partials).  Up
+// to 8 pieces are read in one round (every lane reads their (m, l)); more
+// are read 64 (m, l) at a time, one per lane, their weights reaching the
+// lanes by readlane.
+template <int D, class MlOf, class PoOf>
+__device__ __forceinline__ void merge_rows(const BatchArgs& a, int n, int hh, int tok, int g,
+                                           MlOf ml_of, PoOf po_of) {
   constexpr int DPT = D / 64;   // d values per lane
   const int lane = threadIdx.x & 63;
-  const int HU = p.unit_heads, G = a.group;
-  auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
+  const int G = a.group;
   uint8_t* orow = a.out + (int64_t)tok * a.o_tok + (int64_t)(g * G + hh) * a.o_head + 2 * lane * DPT;
   auto store = [&](const float (&num)[DPT], float den) {
     const float inv = a.v_scale / den;
@@ -120,8 +118,8 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int k = min(i, n - 1);
-      ml[i] = *(const f32x2*)(p.part_ml + row_of(k) * 2);
-      const float* po = p.part_o + row_of(k) * D + lane * DPT;
+      ml[i] = ml_of(k);
+      const float* po = po_of(k) + lane * DPT;
 #pragma unroll
       for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
     }
@@ -142,7 +140,7 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
   float M = kNegInf;
   for (int k0 = 0; k0 < n; k0 += 64) {
     const int k = k0 + lane;
-    const float m = k < n ? p.part_ml[row_of(k) * 2] : kNegInf;
+    const float m = k < n ? ml_of(k)[0] : kNegInf;
     M = fmaxf(M, m);
   }
   M = xor16_max(M);
@@ -155,7 +153,7 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
   for (int k0 = 0; k0 < n; k0 += 64) {
     const int k = k0 + lane;
     f32x2 ml = {kNegInf, 0.f};
-    if (k < n) ml = *(const f32x2*)(p.part_ml + row_of(k) * 2);
+    if (k < n) ml = ml_of(k);
     const float wk = k < n ? fast_exp2(ml[0] - M) : 0.f;
     den += wk * ml[1];
     const int kn = min(64, n - k0);
@@ -165,7 +163,7 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int kk = min(i0 + i, kn - 1);
-        const float* po = p.part_o + row_of(k0 + kk) * D + lane * DPT;
+        const float* po = po_of(k0 + kk) + lane * DPT;
 #pragma unroll
         for (int x = 0; x < DPT; ++x) v[i][x] = po[x];
       }
@@ -184,6 +182,19 @@ __device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePla
   den += __shfl_xor(den, 2);
   den += __shfl_xor(den, 1);
   store(num, den);
+}
+
+// Pieces in the workspace: piece k sits with worker w0 + k (slot 1 for the
+// pair's first worker, slot 0 for the others), head hu of its unit, query
+// head hh of the group.
+template <int D>
+__device__ __forceinline__ void merge_pieces(const BatchArgs& a, const DecodePlan& p, int w0, int n,
+                                             int hu, int hh, int tok, int g) {
+  const int HU = p.unit_heads, G = a.group;
+  auto row_of = [&](int k) { return (((int64_t)(w0 + k) * 2 + (k == 0 ? 1 : 0)) * HU + hu) * G + hh; };
+  merge_rows<D>(
+      a, n, hh, tok, g, [&](int k) { return *(const f32x2*)(p.part_ml + row_of(k) * 2); },
+      [&](int k) { return (const float*)(p.part_o + row_of(k) * D); });
 }
 
 // GATHER: the same partition, block-table walk and loads, but every loaded
@@ -220,6 +231,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
   constexpr int kLdsBytes = decode_tile_lds(D, EB, HU);
   constexpr int kListCap = decode_list_cap(D, EB, HU);
   static_assert(WB == decode_wave_lds(D, EB, HU) && kLdsBytes >= kDecodeWaves * WB, "tile LDS");
+  static_assert(HU * 16 * (4 * D + 8) <= WB, "a whole pair's partials (G <= 16) fit the wave's LDS");
   static_assert(kLdsBytes <= 160 * 1024 && 2 * kLdsBytes > 160 * 1024, "one workgroup per CU");
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
   __shared__ int4 list_lds[GATHER ? 1 : kListCap + 1];
@@ -579,6 +591,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
                                 pack_bf16(o[hu][db][2] * inv, o[hu][db][3] * inv)};
               *(u32x2*)(orow + 2 * (16 * db + 4 * q4)) = v2;
             }
+          } else if (!GATHER && p.whole_units) {
+            // the workgroup merges this pair: the partials stay in this
+            // wave's LDS ([HU G][d] floats, then [HU G] (m, l)), free since
+            // the piece's last products read their operands
+            float* po = (float*)wl + (hu * G + c16) * D;
+  #pragma unroll
+            for (int db = 0; db < NDB; ++db) *(f32x4*)(po + 16 * db + 4 * q4) = o[hu][db];
+            if (q4 == 0) *(f32x2*)((float*)wl + HU * G * D + (hu * G + c16) * 2) = f32x2{m_run[hu], l_tot};
           } else {
             const int64_t row = (((int64_t)w * 2 + (cur.head ? 0 : 1)) * HU + hu) * G + c16;
             float* po = p.part_o + row * D;
@@ -708,8 +728,11 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 1) void decode_kernel(BatchArgs 
         if (n > 1) {
           __syncthreads();   // the pieces' partials are stored
           const int tok = dec[j].y;
-          for (int x = wave; x < HU * G; x += kDecodeWaves)
-            merge_pieces<D>(a, p, (int)blockIdx.x * kDecodeWaves, n, x / G, x % G, tok, gu * HU + x / G);
+          for (int x = wave; x < HU * G; x += kDecodeWaves)   // piece k: wave k's LDS
+            merge_rows<D>(
+                a, n, x % G, tok, gu * HU + x / G,
+                [&](int k) { return *(const f32x2*)((const float*)(lds + k * WB) + HU * G * D + x * 2); },
+                [&](int k) { return (const float*)(lds + k * WB) + x * D; });
           __syncthreads();   // read before the next pair's pieces reuse the slots
         }
       }
