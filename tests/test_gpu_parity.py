@@ -84,6 +84,11 @@ SMALL = {
     # unit) pairs per workgroup, merged inside it; more pairs than
     # workgroups, so a workgroup runs several pairs in turn
     "decode_many_short": ([((37 * i) % 207, 1) for i in range(300)], 32, 8, 128, "bf16", 16, {}),
+    # whole pairs (table width <= 8 steps) with the largest pieces the
+    # workgroup merges from LDS: 4 heads per unit, and 16 query heads per kv head
+    "decode_whole_hu4_fp8_d64": ([(200, 1), (31, 1), (129, 1), (250, 1)], 16, 4, 64, "fp8", 16, {}),
+    "decode_whole_g16": ([(255, 1), (100, 1), (17, 1)], 16, 1, 128, "bf16", 16, {}),
+    "decode_whole_g16_d64_hu2": ([(240, 1), (64, 1), (1, 1)], 32, 2, 64, "bf16", 16, {}),
     "decode_many_short_fp8_g8": ([((53 * i) % 250 + 1, 1) for i in range(100)], 64, 8, 128, "fp8", 16, {}),
     "mixed_short_g16_d64": ([((29 * i) % 120, 1) for i in range(40)] + [(0, 60), (50, 30), (3, 2)],
                             32, 2, 64, "bf16", 16, {}),
