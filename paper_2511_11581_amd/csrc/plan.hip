@@ -29,7 +29,30 @@ constexpr int kPlanSortCap = 8192;   // larger Q-block lists keep the natural or
 constexpr int kPlanBuckets = 512;
 
 
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodePlan dp, PrefillPlan pp,
+// Exclusive scan of NV values per thread with the block totals: one wave
+// (NT = 64) scans with lane shuffles alone, larger blocks with block_scan.
+template <int NV, int NT>
+__device__ __forceinline__ void plan_scan(const int (&v)[NV], int (&ex)[NV], int (&tot)[NV]) {
+  if constexpr (NT == 64) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int x = v[i];
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+      }
+      ex[i] = x - v[i];
+      tot[i] = __shfl(x, 63);
+    }
+  } else {
+    block_scan<NV, NT>(v, ex, tot);
+  }
+}
+
+template <int NT>
+__global__ __launch_bounds__(NT) void plan_kernel(BatchArgs a, DecodePlan dp, PrefillPlan pp,
                                                             int with_prefill) {
   __shared__ int hist[kPlanBuckets];
   __shared__ int keys[kPlanSortCap];
@@ -41,7 +64,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
 
   // ---- one pass over the sequences: decode flag, decode steps, Q-blocks
   int njs = 0, nsteps = 0, nqb = 0;
-  for (int base = 0; base < S; base += kPlanThreads) {
+  for (int base = 0; base < S; base += NT) {
     const int i = base + tid;
     int v[3] = {0, 0, 0};
     int t0 = 0, L = 0;
@@ -57,7 +80,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
       }
     }
     int ex[3], tot[3];
-    block_scan<3, kPlanThreads>(v, ex, tot);
+    plan_scan<3, NT>(v, ex, tot);
     if (v[0]) dp.dec[njs + ex[0]] = make_int4(i, t0, L, nsteps + ex[1]);
     if (with_prefill && i < S) {
       pp.seq_start[i] = nqb + ex[2];
@@ -108,7 +131,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     pp.rec[at] = make_int4(seq, t0 + qb * bq, min(bq, q - qb * bq), (L - q) + qb * bq);
   };
   if (N > kPlanSortCap) {
-    for (int idx = tid; idx < N; idx += kPlanThreads) {
+    for (int idx = tid; idx < N; idx += NT) {
       int seq, qb;
       locate(idx, seq, qb);
       place(idx, seq, qb);
@@ -116,9 +139,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
     return;
   }
   // counting sort by decreasing key-tile count
-  for (int k = tid; k < kPlanBuckets; k += kPlanThreads) hist[k] = 0;
+  for (int k = tid; k < kPlanBuckets; k += NT) hist[k] = 0;
   __syncthreads();
-  for (int idx = tid; idx < N; idx += kPlanThreads) {
+  for (int idx = tid; idx < N; idx += NT) {
     int seq, qb;
     locate(idx, seq, qb);
     const int t0 = a.qsl[seq], q = a.qsl[seq + 1] - t0;
@@ -131,16 +154,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
   __syncthreads();
   // exclusive scan of the histogram in decreasing key order: bucket offsets
   int hcarry = 0;
-  for (int base = 0; base < kPlanBuckets; base += kPlanThreads) {
+  for (int base = 0; base < kPlanBuckets; base += NT) {
     const int b = kPlanBuckets - 1 - (base + tid);
     const int v[1] = {hist[b]};
     int ex[1], tot[1];
-    block_scan<1, kPlanThreads>(v, ex, tot);
+    plan_scan<1, NT>(v, ex, tot);
     hist[b] = hcarry + ex[0];  // bucket b is read and written by this thread only
     hcarry += tot[0];
   }
   __syncthreads();
-  for (int idx = tid; idx < N; idx += kPlanThreads) {
+  for (int idx = tid; idx < N; idx += NT) {
     int seq, qb;
     locate(idx, seq, qb);
     place(atomicAdd(&hist[keys[idx]], 1), seq, qb);
@@ -152,7 +175,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(BatchArgs a, DecodeP
 hipError_t launch_plan(const BatchArgs& a, const DecodePlan& dp, const PrefillPlan& pp,
                        bool with_prefill, hipStream_t st, KernelTiming* tm) {
   if (a.num_seqs <= 0) return hipSuccess;
-  launch_k(plan_kernel, dim3(1), dim3(kPlanThreads), st, tm, a, dp, pp, with_prefill ? 1 : 0);
+  // Small batches (at most 64 sequences and 64 Q-block slots): one wave,
+  // whose scans need no workgroup barriers (0.3 us shorter on a 128-token
+  // prompt; with a hundred Q-blocks the block's 256 threads are faster).
+  if (a.num_seqs <= 64 && (!with_prefill || pp.work_items <= 64))
+    launch_k(plan_kernel<64>, dim3(1), dim3(64), st, tm, a, dp, pp, with_prefill ? 1 : 0);
+  else
+    launch_k(plan_kernel<kPlanThreads>, dim3(1), dim3(kPlanThreads), st, tm, a, dp, pp, with_prefill ? 1 : 0);
   return hipGetLastError();
 }
 
