@@ -211,7 +211,9 @@ pa_status pa_create(const pa_config *cfg, pa_handle **out);
  * All base pointers and all non-unit strides must be 16-byte aligned in
  * bytes.  Sequences with query length 1 run on the persistent split-KV
  * decode kernel (+ merge), the others on the Q-block kernel; a one-workgroup
- * plan kernel builds both work lists on the device first. */
+ * plan kernel builds both work lists on the device first (batches of at most
+ * 16 sequences with no decode launch, whose Q-blocks fit one round of
+ * workgroups, skip it: each Q-block workgroup finds its own work item). */
 pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *v_cache, const pa_tensor *block_table,
                      const pa_tensor *seq_lens, const pa_tensor *query_start_loc, float scale,

@@ -411,6 +411,7 @@ void device_plans(const pa_config& c, const pa_plan_info& p, uint8_t* ws, int64_
   pp->list_qb = reinterpret_cast<int32_t*>(ws + wl.list_qb);
   pp->count = reinterpret_cast<int32_t*>(ws + wl.count);
   pp->rec = reinterpret_cast<int4*>(ws + wl.rec);
+  pp->fused = 0;
 }
 
 // floor(p / bs) by multiply-high and shift (see pa::BlockDiv).
@@ -792,6 +793,18 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
                        [&](pa::KernelTiming* tm) { return pa::launch_merge(a, dp, c.head_dim, st, tm); });
       if (e != hipSuccess) return hip_fail(e, "merge launch");
     }
+    return PA_OK;
+  }
+  // Few sequences, no split-KV decode launch, and Q-blocks that fit one
+  // round of workgroups: the Q-block workgroups derive their records
+  // themselves (~1.4 us each, in parallel), so no plan launch precedes them.
+  if (run_qblock && !run_decode && sh.S <= pa::kFusedPlanSeqs &&
+      p.prefill_units <= (int64_t)h->cus * (256 / p.block_m)) {
+    pp.fused = 1;
+    e = timed_launch(h, PA_KERNEL_PREFILL, st, [&](pa::KernelTiming* tm) {
+      return pa::launch_qblock(a, pp, c.head_dim, fp8, st, false, tm);
+    });
+    if (e != hipSuccess) return hip_fail(e, "prefill launch");
     return PA_OK;
   }
   e = timed_launch(h, PA_KERNEL_PLAN, st,

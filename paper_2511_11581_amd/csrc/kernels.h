@@ -147,7 +147,13 @@ struct PrefillPlan {
   int32_t* list_qb;    // [work_items] Q-block index inside that sequence
   int32_t* count;      // [1] number of Q-blocks
   int4* rec;           // [work_items] (sequence, first token, rows, keys before the first row)
+  // fused = 1 (batches of at most kFusedPlanSeqs sequences with no split-KV
+  // decode launch, whose Q-blocks fit one round of workgroups): no plan
+  // launch; each Q-block workgroup derives its own record, the one of its
+  // rank in the plan kernel's order.
+  int32_t fused;
 };
+constexpr int kFusedPlanSeqs = 16;
 
 struct ValidateArgs {
   const int32_t* bt;

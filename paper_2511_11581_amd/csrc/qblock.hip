@@ -115,6 +115,71 @@ __device__ __forceinline__ void wait_lds() {
   asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");
 }
 
+// The Q-block record of rank wi in the plan kernel's order (decreasing
+// key-tile count; ties in sequence, then block order), derived by the wave
+// itself from the batch metadata, for launches without a plan kernel (at
+// most kFusedPlanSeqs sequences; block_q a power of two).  Lane j holds
+// sequence j.  Q-block b of a sequence with q query rows and ctx earlier
+// keys needs ctx + min((b + 1) bq, q) keys, so the count C(K) of Q-blocks
+// with at least K key tiles is a sum of closed forms; the rank's tile
+// count K* is the largest K with C(K) > wi (C falls as K rises), found by
+// a 64-way search with one candidate per lane, and the record is then the
+// (wi - C(K* + 1))-th Q-block with K* tiles.  False if wi >= the count.
+__device__ bool fused_record(const BatchArgs& a, const PrefillPlan& pp, int wi, int4& rec) {
+  const int lane = __builtin_amdgcn_workitem_id_x() & 63, S = a.num_seqs;
+  const int bq = pp.block_q, bsh = __builtin_ctz((unsigned)bq);
+  const int cap = a.mb * a.block_size;
+  int t0 = 0, ql = 0, ctx = 0, nqb = 0, kt = 0;
+  if (lane < S) {
+    t0 = a.qsl[lane];
+    const int q = a.qsl[lane + 1] - t0, L = min(a.seq_lens[lane], cap);
+    if (q >= pp.qmin && t0 >= 0 && t0 + q <= a.num_tokens && L >= q) {
+      ql = q;
+      ctx = L - q;
+      nqb = (q + bq - 1) >> bsh;
+      kt = (L + kTile - 1) / kTile;   // tiles of its last Q-block, the most
+    }
+  }
+  // Q-blocks of sequence j (readlane'd) with at least K key tiles
+  auto cnt = [&](int j, int K) {
+    const int n = __builtin_amdgcn_readlane(nqb, j), q = __builtin_amdgcn_readlane(ql, j);
+    const int x = kTile * (K - 1) - __builtin_amdgcn_readlane(ctx, j);   // need min((b+1) bq, q) > x
+    return (n == 0 || q <= x) ? 0 : n - (x < 0 ? 0 : (x >> bsh));
+  };
+  int count = 0, kmax = 0;
+  for (int j = 0; j < S; ++j) {
+    count += __builtin_amdgcn_readlane(nqb, j);
+    kmax = max(kmax, __builtin_amdgcn_readlane(kt, j));
+  }
+  count = min(count, pp.work_items);
+  if (wi >= count) return false;
+  // largest K in [1, kmax] with C(K) > wi: C(lo) > wi, C(hi) <= wi
+  int lo = 1, hi = kmax + 1;
+  while (hi - lo > 1) {
+    const int step = (hi - lo + 63) / 64;
+    const int K = lo + lane * step;
+    int c = 0;
+    for (int j = 0; j < S; ++j) c += cnt(j, K);
+    const bool ok = K < hi && c > wi;
+    lo += (63 - __builtin_clzll(__ballot(ok))) * step;
+    hi = min(hi, lo + step);
+  }
+  int r = wi;
+  for (int j = 0; j < S; ++j) r -= cnt(j, lo + 1);   // rank among the Q-blocks with lo tiles
+  for (int j = 0; j < S; ++j) {
+    const int hi_j = cnt(j, lo), e = hi_j - cnt(j, lo + 1);
+    if (r < e) {
+      const int b = __builtin_amdgcn_readlane(nqb, j) - hi_j + r;
+      const int q = __builtin_amdgcn_readlane(ql, j);
+      rec = make_int4(j, __builtin_amdgcn_readlane(t0, j) + b * bq, min(bq, q - b * bq),
+                      __builtin_amdgcn_readlane(ctx, j) + b * bq);
+      return true;
+    }
+    r -= e;
+  }
+  return false;   // (not reached: C(lo) > wi)
+}
+
 // GATHER: only the last Q-block of each sequence runs; it walks the block
 // table and copies every tile into the ring with the same loads, then
 // stores the bytes of every valid key into the dense outputs a.kd / a.vd:
@@ -188,10 +253,16 @@ __global__ __launch_bounds__(64 * W, 8 / W) void qblock_kernel(BatchArgs a, Pref
   const int wg = __builtin_amdgcn_workgroup_id_x();
   const int g = wg % Hkv;
   const int wi = wg / Hkv;
-  if (wi >= load_s32(pp.count)) return;
-  // The Q-block's record from the plan kernel, in one scalar load: its
-  // sequence, first token, tokens, and the keys before its first token.
-  const int4 rec = load_rec(pp.rec + wi);
+  // The Q-block's record (its sequence, first token, tokens, and the keys
+  // before its first token): from the plan kernel, in one scalar load, or
+  // derived here.
+  int4 rec;
+  if (!GATHER && pp.fused) {
+    if (!fused_record(a, pp, wi, rec)) return;
+  } else {
+    if (wi >= load_s32(pp.count)) return;
+    rec = load_rec(pp.rec + wi);
+  }
   const int seq = rec.x;
   const int t0 = rec.y;        // token of the block's row 0 (rows are relative to it)
   const int tok_lo = 0;

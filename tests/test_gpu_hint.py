@@ -179,3 +179,75 @@ def test_whole_pairs_replay_from_a_hip_graph_with_new_metadata():
     g.replay()
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), "replay on batch A"
+
+
+def _prefill_seqs(n, seed, ctx_max=3000, q_max=600):
+    g = torch.Generator().manual_seed(seed)
+    return [(int(torch.randint(0, ctx_max + 1, (1,), generator=g)),
+             int(torch.randint(2, q_max + 1, (1,), generator=g))) for _ in range(n)]
+
+
+FUSED = {
+    # name: (seqs, Hq, Hkv, d, kv, bs, forced Q-block rows or None, hinted)
+    "pf8_short_prompts": ([(0, 200)] * 8, 32, 8, 128, "bf16", 16, None, True),
+    "pf16_g4": (_prefill_seqs(16, 1, 2000, 120), 32, 8, 128, "bf16", 16, None, True),
+    "pf9_g8_d64": (_prefill_seqs(9, 2, 3000, 200), 16, 2, 64, "bf16", 32, None, True),
+    "pf6_fp8": (_prefill_seqs(6, 3, 3000, 150), 32, 8, 128, "fp8", 16, None, True),
+    "pf5_fp8_d64": (_prefill_seqs(5, 7, 3000, 150), 16, 4, 64, "fp8", 16, None, True),
+    "pf5_rows128": (_prefill_seqs(5, 4, 3000, 300), 32, 8, 128, "bf16", 16, 128, True),
+    "pf4_g1_bs400": (_prefill_seqs(4, 5, 1500, 300), 8, 8, 128, "bf16", 400, None, True),
+    "pf3_long_ctx": ([(40000, 130), (0, 2), (9000, 700)], 32, 8, 128, "bf16", 16, None, True),
+    # a small mixed batch run as Q-blocks only (single-token rows included)
+    "mixed_small_unified": ([(300, 1), (0, 50), (40, 1), (100, 20), (700, 1)], 8, 2, 64, "bf16", 16, None,
+                            True),
+    # beyond the route: more sequences, or more Q-blocks than one round
+    "pf17_planned": (_prefill_seqs(17, 6, 800, 100), 32, 8, 128, "bf16", 16, None, True),
+    "pf4_two_rounds": ([(0, 3000), (0, 2048), (0, 1500), (0, 1000)], 32, 8, 128, "bf16", 16, None, True),
+}
+
+
+@pytest.mark.parametrize("name", list(FUSED))
+def test_fused_plan_route(name, monkeypatch):
+    # Batches of at most 16 sequences with no split-KV decode launch, whose
+    # Q-blocks fit one round of workgroups, launch the Q-block kernel alone,
+    # each workgroup deriving its record; the results equal the planned
+    # launch's bit for bit (a Q-block's result does not depend on which
+    # workgroup computes it) and the oracle's within tolerance.
+    seqs, Hq, Hkv, d, kv, bs, rows, hinted = FUSED[name]
+    if rows is not None:
+        monkeypatch.setenv("PA_QBLOCK_ROWS", str(rows))
+    w = W.make_batch(seqs, Hq, Hkv, d, kv_dtype=kv, block_size=bs, seed=seed_of("fused" + name),
+                     name=name, token_pad=3)
+    wd = w.to("cuda")
+    att = pa.PagedAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size,
+                            w.k_cache.dtype, w.k_scale, w.v_scale, max_tokens=w.num_tokens,
+                            max_seqs=w.num_seqs, max_blocks_per_seq=int(w.block_table.shape[1]),
+                            profile=True)
+
+    def run(hint):
+        out = torch.full(wd.q.shape, SENTINEL, dtype=torch.bfloat16, device="cuda")
+        att.profile(reset=True)
+        att.forward(wd.q, wd.k_cache, wd.v_cache, wd.block_table, wd.seq_lens,
+                    wd.query_start_loc, w.scale, out=out, hint=hint)
+        torch.cuda.synchronize()
+        return out.cpu(), att.profile(reset=True)
+
+    hint = _hint_of(w)
+    plan = att.plan(w.num_tokens, w.num_seqs, int(w.block_table.shape[1]), hint)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    no_decode = plan["prefill_qmin"] == 1 or hint[0] == 0   # no split-KV decode launch
+    fused_route = (w.num_seqs <= 16 and no_decode and plan["prefill_launch"] == 1
+                   and plan["prefill_units"] <= cus * (256 // plan["block_m"]))
+    # the planned launch: the unhinted call (the plan kernel in front of the
+    # Q-blocks; for the mixed batch the decode rows split instead)
+    planned, prof_p = run(None)
+    fused, prof_f = run(hint)
+    assert prof_p["plan"][0] == 1 and prof_p["prefill"][0] == 1
+    assert prof_f["prefill"][0] == 1 and prof_f["decode"][0] == 0
+    assert prof_f["plan"][0] == (0 if fused_route else 1), (name, plan)
+    T = valid_token_count(w)
+    if plan["prefill_qmin"] == 2:   # the same Q-blocks either way: equal bit for bit
+        assert torch.equal(planned.view(torch.int16), fused.view(torch.int16)), name
+    check_close(fused[:T], oracle_full(w)[:T], w.kv_fp8, name)
+    assert (fused[T:].float() == SENTINEL).all()
+    att.close()
