@@ -251,3 +251,57 @@ def test_fused_plan_route(name, monkeypatch):
     check_close(fused[:T], oracle_full(w)[:T], w.kv_fp8, name)
     assert (fused[T:].float() == SENTINEL).all()
     att.close()
+
+
+def test_plan_free_q_blocks_replay_from_a_hip_graph_with_new_metadata():
+    # A hinted prefill batch small enough that each Q-block workgroup finds
+    # its own work item (no plan launch): the graph captured on batch A
+    # replays on batch B's contents (same shapes, other lengths and
+    # contexts), each replay checked against the oracle, and on A again,
+    # bitwise equal to the eager call.
+    seqs_a = [(500, 100), (0, 50), (230, 30), (61, 20), (399, 40), (7, 60)]
+    seqs_b = [(30, 60), (420, 40), (0, 20), (300, 30), (125, 50), (530, 100)]
+    need = max(sum((c + q + 15) // 16 for c, q in s) for s in (seqs_a, seqs_b))
+    wa = W.make_batch(seqs_a, 32, 8, 128, seed=seed_of("pfree_a"), pool_blocks=need, table_width=40,
+                      name="pfree_a").to("cuda")
+    wb = W.make_batch(seqs_b, 32, 8, 128, seed=seed_of("pfree_b"), pool_blocks=need, table_width=40,
+                      name="pfree_b").to("cuda")
+    att = attention_for(wa, max_blocks=40)
+    hint = (0, 100)
+    p = att.plan(wa.num_tokens, wa.num_seqs, 40, hint)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert wa.num_seqs <= 16 and p["prefill_units"] <= cus * (256 // p["block_m"])   # the plan-free route
+    args = (wa.q, wa.k_cache, wa.v_cache, wa.block_table, wa.seq_lens, wa.query_start_loc, wa.scale)
+    eager = torch.empty_like(wa.q)
+    att.forward(*args, out=eager, hint=hint)
+    torch.cuda.synchronize()
+    T = valid_token_count(wa)
+    check_close(eager.cpu()[:T], oracle_full(wa)[:T], False, "plan-free Q-blocks, eager")
+    out = torch.empty_like(wa.q)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        att.forward(*args, out=out, hint=hint)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        att.forward(*args, out=out, hint=hint)
+    saved = [x.clone() for x in args[:6]]
+    for dst, src in zip(args[:6], (wb.q, wb.k_cache, wb.v_cache, wb.block_table, wb.seq_lens,
+                                   wb.query_start_loc)):
+        dst.copy_(src)
+    TB = valid_token_count(wb)
+    for rep in range(2):
+        out.fill_(SENTINEL)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        check_close(out.cpu()[:TB], oracle_full(wb)[:TB], False, f"plan-free Q-blocks, replay {rep} on batch B")
+    for dst, src in zip(args[:6], saved):
+        dst.copy_(src)
+    out.fill_(SENTINEL)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), "replay on batch A"
