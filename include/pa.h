@@ -212,7 +212,7 @@ pa_status pa_create(const pa_config *cfg, pa_handle **out);
  * bytes.  Sequences with query length 1 run on the persistent split-KV
  * decode kernel (+ merge), the others on the Q-block kernel; a one-workgroup
  * plan kernel builds both work lists on the device first (batches of at most
- * 16 sequences with no decode launch, whose Q-blocks fit one round of
+ * 16 sequences with no decode launch, whose Q-blocks fit two rounds of
  * workgroups, skip it: each Q-block workgroup finds its own work item). */
 pa_status pa_forward(pa_handle *h, const pa_tensor *q, const pa_tensor *k_cache,
                      const pa_tensor *v_cache, const pa_tensor *block_table,

@@ -795,11 +795,12 @@ static pa_status forward_impl(pa_handle* h, const pa_tensor* q, const pa_tensor*
     }
     return PA_OK;
   }
-  // Few sequences, no split-KV decode launch, and Q-blocks that fit one
-  // round of workgroups: the Q-block workgroups derive their records
-  // themselves (~1.4 us each, in parallel), so no plan launch precedes them.
+  // Few sequences, no split-KV decode launch, and Q-blocks that fit two
+  // rounds of workgroups: the Q-block workgroups derive their records
+  // themselves (~1.4 us each, once per round), so no plan launch precedes
+  // them.
   if (run_qblock && !run_decode && sh.S <= pa::kFusedPlanSeqs &&
-      p.prefill_units <= (int64_t)h->cus * (256 / p.block_m)) {
+      p.prefill_units <= 2 * (int64_t)h->cus * (256 / p.block_m)) {
     pp.fused = 1;
     e = timed_launch(h, PA_KERNEL_PREFILL, st, [&](pa::KernelTiming* tm) {
       return pa::launch_qblock(a, pp, c.head_dim, fp8, st, false, tm);

@@ -148,7 +148,7 @@ struct PrefillPlan {
   int32_t* count;      // [1] number of Q-blocks
   int4* rec;           // [work_items] (sequence, first token, rows, keys before the first row)
   // fused = 1 (batches of at most kFusedPlanSeqs sequences with no split-KV
-  // decode launch, whose Q-blocks fit one round of workgroups): no plan
+  // decode launch, whose Q-blocks fit two rounds of workgroups): no plan
   // launch; each Q-block workgroup derives its own record, the one of its
   // rank in the plan kernel's order.
   int32_t fused;
